@@ -1,0 +1,179 @@
+"""Benchmark of one rank's partition path on one MI355X.
+
+A step is one pass of the whole path over one rank's state: the Adam
+partition step (compute stream), the secondary refresh and its int8
+quantization (copy stream), and the dequant-gather of one layer from the P'
+node-local secondary shards (comm stream, ordered after the quantization by
+an event: the paper's fix).
+
+Prints ONE JSON line.  `value` is the algorithmic HBM bytes of all four
+kernels of a step divided by the measured time per step (GB/s), with every
+input resident in HBM.  Per-kernel durations come from HIP timing events on
+each kernel's own stream.  The roofline entry is for the dominant kernel (the
+Adam step).  The CPU baseline times the plain CPU oracle on a bounded sample
+of the same workload on this host.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload llama-2-13b]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD's published figure
+METRIC = "achieved HBM GB/s (and % of peak) for partition step+refresh and dequant-gather"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama-2-13b")
+    ap.add_argument("--cpu-sample", type=float, default=0.25,
+                    help="fraction of the workload the CPU oracle is timed on (0 = skip)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM bytes per launch from rocprofv3 counters, if present")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, frac):
+    """Time the CPU oracle (as it stands, one thread) on a `frac` sample of the
+    workload: Adam on frac*n, refresh and quantization of frac*n, gather of a
+    frac*N layer from P' shards.  Inputs come from the same seeded
+    generators; generation is not timed."""
+    import numpy as np
+    import oracle
+    from paper_2407_01614_amd import synth
+    from paper_2407_01614_amd.workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_gather,
+                                                bytes_quant, secondary_elems)
+    B = wl.block
+    n = max(B, int(wl.n * frac) // B * B)
+    N = max(B * wl.secondary_world, int(wl.layer_elems * frac))
+    s = secondary_elems(N, wl.secondary_world, B)
+    p = synth.master_weights(n, wl.cfg_id)
+    g = synth.gradients(n, wl.cfg_id)
+    z = np.zeros(n, np.float32)
+    w = synth.bf16_weights(wl.secondary_world * s, wl.cfg_id)
+    t0 = time.perf_counter()
+    _, _, _, prim = oracle.adam_step(p, z, z, g, step=1, **wl.adam)
+    t1 = time.perf_counter()
+    sec = oracle.refresh(prim)
+    t2 = time.perf_counter()
+    oracle.quantize_blockwise_i8(sec, B)
+    t3 = time.perf_counter()
+    quants = [oracle.quantize_blockwise_i8(w[j * s:(j + 1) * s], B)
+              for j in range(wl.secondary_world)]
+    t4 = time.perf_counter()
+    oracle.dequant_gather_layer([q[0] for q in quants], [q[1] for q in quants], s, B, N)
+    t5 = time.perf_counter()
+    secs = (t1 - t0) + (t2 - t1) + (t3 - t2) + (t5 - t4)
+    nbytes = (BYTES_ADAM * n + BYTES_REFRESH * n + bytes_quant(n, B)
+              + bytes_gather(s, wl.secondary_world, N, B))
+    return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "%s at %.3g of full size: Adam+refresh+quant on %d elements, gather of a "
+                      "%d-element layer from %d shards; %.2f s of CPU time"
+                      % (wl.name, frac, n, N, wl.secondary_world, secs),
+            "seconds": {"adam": round(t1 - t0, 3), "refresh": round(t2 - t1, 3),
+                        "quant": round(t3 - t2, 3), "gather": round(t5 - t4, 3)}}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the partition path is rank-local and the other "
+              "ranks' shards are simulated in this GPU's memory; --gpus %d is not supported"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    pipe = PartitionPipeline(wl)
+    pipe.load_synthetic()
+
+    for _ in range(args.warmup):
+        pipe.step()
+    pipe.wait()
+    pipe.enable_timing()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        pipe.step()
+    pipe.wait()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    kb = pipe.kernel_bytes()
+    times = pipe.kernel_times_ms()
+    step_bytes = sum(kb.values())
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    kernels = {}
+    for k in kb:
+        ts = sorted(times[k])
+        mean = sum(ts) / len(ts)
+        med = ts[len(ts) // 2]
+        gbps = kb[k] / (mean * 1e-3) / 1e9
+        kernels[k] = {"bytes": kb[k], "mean_us": round(mean * 1e3, 2),
+                      "median_us": round(med * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
+                      "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
+    sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
+
+    traffic = None
+    if os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            tr = json.load(f)
+        if tr.get("workload") == wl.name and tr.get("kernel") == "adam":
+            traffic = tr.get("bytes_per_launch")
+
+    adam_mean_s = kernels["adam"]["mean_us"] * 1e-6
+    achieved = kb["adam"] / adam_mean_s / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "%s rank shard: n=%d fp32 master/m/v/grad, bf16 primary and "
+                               "secondary, int8 blocks of %d; gather of a %d-element layer "
+                               "from %d secondary shards of %d"
+                               % (wl.name, wl.n, wl.block, wl.layer_elems, wl.secondary_world,
+                                  wl.shard_elems),
+                   "n": wl.n, "layer_elems": wl.layer_elems, "secondary_world": wl.secondary_world,
+                   "shard_elems": wl.shard_elems, "block": wl.block},
+        "roofline": {"bound": "hbm", "kernel": "adam_partition_step",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic},
+        "step_refresh": {"GB/s": round(sr_gbps, 1), "frac_of_peak": round(sr_gbps / HBM_PEAK_GBPS, 4)},
+        "gather": {"GB/s": kernels["gather"]["GB/s"],
+                   "frac_of_peak": kernels["gather"]["frac_of_peak"]},
+        "kernels": kernels,
+        "device": torch.cuda.get_device_name(0),
+    }
+    del pipe
+    torch.cuda.empty_cache()
+    if args.cpu_sample > 0:
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,174 @@
+/*
+ * zpp.h - C ABI of the one-rank partition path of the modified ZeRO++ hpZ
+ * scheme (arXiv 2407.01614), built for AMD Instinct MI355X (gfx950).
+ *
+ * The path, per rank and iteration:
+ *   1. zpp_adam_partition_step   optimizer.step() on the rank's partition
+ *                                (Algorithm 1, last statement of the loop):
+ *                                fp32 master/moments in place, bf16 primary out.
+ *   2. zpp_refresh_secondary     fill the hpZ secondary copy (Algorithm 1,
+ *                                forward loop: allocate |L|/P' and copy the
+ *                                local rank's weights asynchronously; Eq. 1).
+ *   3. zpp_quantize_blockwise_i8 qwZ: quantize weights before they are
+ *                                gathered (Background section).
+ *   4. zpp_dequant_gather_layer  backward AllGather(L, P') over the
+ *                                node-local secondary shards, dequantizing
+ *                                on the way (Algorithm 1, backward branch of
+ *                                PrefetchAllGather).
+ * The ordering fix of the paper (the gather of a secondary copy may only
+ * start once the copy that fills it has finished; Algorithm 1, the wait in
+ * PrefetchAllGather, and the synchronization operator of the Algorithm
+ * section) is expressed with HIP events: steps 2 and 3 record `done_after`,
+ * step 4 makes its stream wait on `wait_events` on the device, without
+ * blocking the host.
+ *
+ * Conventions common to every call:
+ *   - All array pointers are DEVICE pointers (HBM of the current device),
+ *     owned by the caller.  The library never allocates, frees or blocks the
+ *     host; every call only enqueues work on `stream` and returns.
+ *   - bf16 values are passed as their uint16_t bit patterns.
+ *   - `stream == NULL` is the null stream.  Events are created by the caller;
+ *     a NULL event means "no event".
+ *   - Validation is synchronous and happens before anything is enqueued; on
+ *     any validation error nothing is enqueued (no kernel, no event).
+ *   - A size of 0 is a valid no-op that still honours the wait events and
+ *     records `done_after`, so a waiter never hangs.
+ *   - If the HIP runtime rejects a launch, the call returns ZPP_EHIP and
+ *     zpp_last_hip_error() gives the hipError_t (per host thread).  Work
+ *     enqueued before the failing HIP call stays enqueued.  Faults inside a
+ *     kernel surface at the caller's next synchronization, as for any HIP
+ *     stream operation.
+ */
+#ifndef ZPP_H
+#define ZPP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Symbols of this header are the only ones the library exports. */
+#define ZPP_API __attribute__((visibility("default")))
+
+typedef enum {
+    ZPP_OK = 0,
+    ZPP_EINVAL = 1,   /* bad argument: NULL pointer with a non-zero size, bad size or block */
+    ZPP_EALIGN = 2,   /* a pointer is not aligned to its element type */
+    ZPP_EOVERLAP = 3, /* an output range overlaps another argument's range */
+    ZPP_EHIP = 4      /* the HIP runtime returned an error; see zpp_last_hip_error() */
+} zpp_status;
+
+/* Hyperparameters of one Adam step, read at call time (the struct may be
+ * reused or freed as soon as the call returns).  The paper does not name the
+ * optimizer: this is Adam (Kingma & Ba) with decoupled weight decay
+ * (Loshchilov & Hutter) when adamw != 0, or with the L2 term wd * p added to
+ * the gradient when adamw == 0.  Bias correction uses the 1-based step t.
+ * Requirements: all floats finite, 0 <= beta1, beta2 < 1, eps >= 0,
+ * step >= 1; otherwise ZPP_EINVAL. */
+typedef struct {
+    float lr;
+    float beta1;
+    float beta2;
+    float eps;
+    float weight_decay;
+    int32_t adamw;
+    int64_t step;
+} zpp_adam_hparams;
+
+/* Partition step: optimizer.step() on one rank's ZeRO partition (Algorithm 1;
+ * the optimizer states are sharded over the P ranks, Background section).
+ * For every i < n, in fp32:
+ *     adamw ? p -= lr*wd*p : g += wd*p
+ *     m = beta1*m + (1-beta1)*g ;  v = beta2*v + (1-beta2)*g*g
+ *     p -= (lr / (1-beta1^t)) * m / (sqrt(v / (1-beta2^t)) + eps)
+ *     primary_bf16[i] = bf16(p)   (round to nearest even; NaN -> 0x7FC0)
+ * master, exp_avg, exp_avg_sq: float[n], updated in place (three distinct
+ *   arrays).  grad: float[n], read only.  primary_bf16: uint16_t[n] out, the
+ *   rank's slice of the layer the forward AllGather(L, P) assembles.
+ * None of the five ranges may overlap another (ZPP_EOVERLAP).  Pointers must
+ * be aligned to their element size (ZPP_EALIGN); 16-byte alignment of all
+ * five selects the vector kernel.  hp must be non-NULL. */
+ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float *exp_avg_sq,
+                                   const float *grad, uint16_t *primary_bf16, size_t n,
+                                   const zpp_adam_hparams *hp, hipStream_t stream);
+
+/* Secondary refresh: the copy into the hpZ secondary partition
+ * L_{i,second} of |L_i|/P' elements (Eq. 1) of the weights that belong to
+ * the local rank, taken out of the full parameter tensor (Algorithm 1,
+ * forward loop).  secondary_bf16[i] = src_bf16[i] bit for bit, i < count.
+ * Order on `stream`: wait for `wait_before` (e.g. the previous gather that
+ * still reads this buffer), copy, then record `done_after`, which the gather
+ * of this copy must wait on (the paper's fix).
+ * The two ranges must not overlap (ZPP_EOVERLAP); pointers 2-byte aligned
+ * (ZPP_EALIGN). */
+ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16, size_t count,
+                                 hipStream_t stream, hipEvent_t wait_before,
+                                 hipEvent_t done_after);
+
+/* qwZ quantization of a weight shard before it is gathered (Background
+ * section: weights are quantized before AllGather).  Symmetric absmax int8
+ * over consecutive blocks of `block` elements (the last block may be
+ * shorter), one fp32 scale per block, all decisions in fp32:
+ *   block holds an Inf or NaN  -> scale = NaN (0x7FC00000), codes 0
+ *   a = max |x| == 0           -> scale = 0, codes 0
+ *   otherwise                  -> scale = a / 127, inv = 127 / a (both
+ *       correctly rounded), code = rint(x * inv) (ties to even) in
+ *       [-127, 127]; when a < 2^-100, x and a are first multiplied by 2^64.
+ * src_bf16: uint16_t[n].  codes: int8_t[n] out.  scales: float[ceil(n/block)]
+ * out.  block: a power of two in [64, 4096], else ZPP_EINVAL.
+ * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
+ * No two of the three ranges may overlap (ZPP_EOVERLAP).  Alignment: src 2,
+ * scales 4 (ZPP_EALIGN); src 16 and codes 8 bytes select the vector kernel. */
+ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n, uint32_t block,
+                                     int8_t *codes, float *scales, hipStream_t stream,
+                                     hipEvent_t wait_before, hipEvent_t done_after);
+
+/* Maximum number of shards one gather accepts (the secondary group P'). */
+#define ZPP_MAX_SHARDS 64u
+/* Maximum number of events one gather waits on. */
+#define ZPP_MAX_WAIT_EVENTS 64u
+
+/* Backward AllGather(L, P') of one layer over its P' node-local secondary
+ * shards (Algorithm 1, backward branch; hpZ keeps this exchange inside a
+ * node), with the qwZ dequantization fused in:
+ *     out[j*shard_elems + i] = bf16(float(codes_j[i]) * scales_j[i / block])
+ * for all j*shard_elems + i < layer_elems: one fp32 multiply, then round to
+ * nearest even (NaN -> 0x7FC0).  The padding of the last shard past
+ * layer_elems is dropped.
+ * shard_codes, shard_scales: HOST arrays of num_shards DEVICE pointers
+ *   (int8_t[shard_elems] and float[ceil(shard_elems/block)] each); they are
+ *   read during the call only.  num_shards in [1, ZPP_MAX_SHARDS]; every
+ *   pointer non-NULL.  out_bf16: uint16_t[layer_elems] out.
+ * layer_elems <= num_shards * shard_elems, block a power of two in
+ *   [64, 4096] (ZPP_EINVAL otherwise).
+ * Order on `stream`: wait for every event of wait_events[0..num_wait) on the
+ * device (the paper's fix: no gather before the copies it reads are
+ * complete), gather, record `done_after` (lets the next refresh of these
+ * buffers wait for this read).  num_wait <= ZPP_MAX_WAIT_EVENTS, every event
+ * non-NULL.
+ * out must not overlap any shard range (ZPP_EOVERLAP).  Alignment: out 2,
+ * scales 4 (ZPP_EALIGN); shard_elems % 16 == 0 with 16-byte aligned codes
+ * and out selects the vector kernel. */
+ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
+                                    const float *const *shard_scales, uint32_t num_shards,
+                                    size_t shard_elems, uint32_t block, size_t layer_elems,
+                                    uint16_t *out_bf16, hipStream_t stream,
+                                    const hipEvent_t *wait_events, uint32_t num_wait,
+                                    hipEvent_t done_after);
+
+/* Static, NUL-terminated description of a status code. */
+ZPP_API const char *zpp_status_string(zpp_status s);
+
+/* hipError_t (as int) of the last call on this host thread that returned
+ * ZPP_EHIP; 0 if none. */
+ZPP_API int zpp_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZPP_H */

@@ -1,0 +1,222 @@
+// C ABI of the partition path (declared in include/zpp.h): argument checks,
+// stream ordering with events, and dispatch to the kernels.
+#include <math.h>
+#include <stdint.h>
+
+#include "zpp.h"
+#include "zpp_launch.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+zpp_status hip_fail(hipError_t e) {
+    g_last_hip_error = (int)e;
+    return ZPP_EHIP;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Do [a, a + abytes) and [b, b + bbytes) share a byte?
+bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes) {
+    if (abytes == 0 || bbytes == 0)
+        return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+bool valid_block(uint32_t block) {
+    return block >= 64 && block <= 4096 && (block & (block - 1)) == 0;
+}
+
+// Largest element count whose byte ranges (up to 16 B per element) cannot
+// overflow a size_t.
+constexpr size_t kMaxElems = SIZE_MAX / 16;
+
+zpp_status wait_on(hipStream_t stream, hipEvent_t ev) {
+    if (!ev)
+        return ZPP_OK;
+    const hipError_t e = hipStreamWaitEvent(stream, ev, 0);
+    return e == hipSuccess ? ZPP_OK : hip_fail(e);
+}
+
+zpp_status record(hipStream_t stream, hipEvent_t ev) {
+    if (!ev)
+        return ZPP_OK;
+    const hipError_t e = hipEventRecord(ev, stream);
+    return e == hipSuccess ? ZPP_OK : hip_fail(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float *exp_avg_sq,
+                                   const float *grad, uint16_t *primary_bf16, size_t n,
+                                   const zpp_adam_hparams *hp, hipStream_t stream) {
+    if (!hp)
+        return ZPP_EINVAL;
+    if (!isfinite(hp->lr) || !isfinite(hp->beta1) || !isfinite(hp->beta2) ||
+        !isfinite(hp->eps) || !isfinite(hp->weight_decay))
+        return ZPP_EINVAL;
+    if (hp->beta1 < 0.0f || hp->beta1 >= 1.0f || hp->beta2 < 0.0f || hp->beta2 >= 1.0f ||
+        hp->eps < 0.0f || hp->step < 1)
+        return ZPP_EINVAL;
+    if (n == 0)
+        return ZPP_OK;
+    if (n > kMaxElems)
+        return ZPP_EINVAL;
+    if (!master || !exp_avg || !exp_avg_sq || !grad || !primary_bf16)
+        return ZPP_EINVAL;
+    if (!aligned(master, 4) || !aligned(exp_avg, 4) || !aligned(exp_avg_sq, 4) ||
+        !aligned(grad, 4) || !aligned(primary_bf16, 2))
+        return ZPP_EALIGN;
+    const void *ptrs[5] = {master, exp_avg, exp_avg_sq, grad, primary_bf16};
+    const size_t bytes[5] = {4 * n, 4 * n, 4 * n, 4 * n, 2 * n};
+    for (int x = 0; x < 5; ++x)
+        for (int y = x + 1; y < 5; ++y)
+            if (overlaps(ptrs[x], bytes[x], ptrs[y], bytes[y]))
+                return ZPP_EOVERLAP;
+
+    zpp::AdamConsts c;
+    const double b1 = hp->beta1, b2 = hp->beta2, lr = hp->lr, wd = hp->weight_decay;
+    const double bc1 = 1.0 - pow(b1, (double)hp->step);
+    const double bc2 = 1.0 - pow(b2, (double)hp->step);
+    c.lr_wd = (float)(lr * wd);
+    c.wd = hp->weight_decay;
+    c.beta1 = hp->beta1;
+    c.one_minus_beta1 = (float)(1.0 - b1);
+    c.beta2 = hp->beta2;
+    c.one_minus_beta2 = (float)(1.0 - b2);
+    c.step_size = (float)(lr / bc1);
+    c.inv_bc2 = (float)(1.0 / bc2);
+    c.eps = hp->eps;
+    c.adamw = hp->adamw ? 1 : 0;
+    const bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
+                     aligned(grad, 16) && aligned(primary_bf16, 16);
+    const hipError_t e =
+        zpp::launch_adam(master, exp_avg, exp_avg_sq, grad, primary_bf16, n, c, vec, stream);
+    return e == hipSuccess ? ZPP_OK : hip_fail(e);
+}
+
+ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16, size_t count,
+                                 hipStream_t stream, hipEvent_t wait_before,
+                                 hipEvent_t done_after) {
+    if (count > kMaxElems)
+        return ZPP_EINVAL;
+    if (count) {
+        if (!secondary_bf16 || !src_bf16)
+            return ZPP_EINVAL;
+        if (!aligned(secondary_bf16, 2) || !aligned(src_bf16, 2))
+            return ZPP_EALIGN;
+        if (overlaps(secondary_bf16, 2 * count, src_bf16, 2 * count))
+            return ZPP_EOVERLAP;
+    }
+    zpp_status st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (count) {
+        const bool vec = aligned(secondary_bf16, 16) && aligned(src_bf16, 16);
+        const hipError_t e = zpp::launch_refresh(secondary_bf16, src_bf16, count, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n, uint32_t block,
+                                     int8_t *codes, float *scales, hipStream_t stream,
+                                     hipEvent_t wait_before, hipEvent_t done_after) {
+    if (!valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    const size_t nblocks = (n + block - 1) / block;
+    if (n) {
+        if (!src_bf16 || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(src_bf16, 2) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        if (overlaps(src_bf16, 2 * n, codes, n) || overlaps(src_bf16, 2 * n, scales, 4 * nblocks) ||
+            overlaps(codes, n, scales, 4 * nblocks))
+            return ZPP_EOVERLAP;
+    }
+    zpp_status st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (n) {
+        const bool vec = aligned(src_bf16, 16) && aligned(codes, 8);
+        const hipError_t e = zpp::launch_quantize(src_bf16, n, block, codes, scales, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
+                                    const float *const *shard_scales, uint32_t num_shards,
+                                    size_t shard_elems, uint32_t block, size_t layer_elems,
+                                    uint16_t *out_bf16, hipStream_t stream,
+                                    const hipEvent_t *wait_events, uint32_t num_wait,
+                                    hipEvent_t done_after) {
+    if (num_shards == 0 || num_shards > ZPP_MAX_SHARDS || !valid_block(block))
+        return ZPP_EINVAL;
+    if (shard_elems == 0 || shard_elems > kMaxElems / num_shards)
+        return ZPP_EINVAL;
+    if (layer_elems > (size_t)num_shards * shard_elems)
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!shard_codes || !shard_scales)
+        return ZPP_EINVAL;
+    const size_t nblocks = (shard_elems + block - 1) / block;
+    zpp::GatherShards shards = {};
+    bool vec = (shard_elems % 16 == 0) && aligned(out_bf16, 16);
+    for (uint32_t j = 0; j < num_shards; ++j) {
+        if (!shard_codes[j] || !shard_scales[j])
+            return ZPP_EINVAL;
+        if (!aligned(shard_scales[j], 4))
+            return ZPP_EALIGN;
+        shards.codes[j] = shard_codes[j];
+        shards.scales[j] = shard_scales[j];
+        vec = vec && aligned(shard_codes[j], 16);
+    }
+    if (layer_elems) {
+        if (!out_bf16)
+            return ZPP_EINVAL;
+        if (!aligned(out_bf16, 2))
+            return ZPP_EALIGN;
+        for (uint32_t j = 0; j < num_shards; ++j)
+            if (overlaps(out_bf16, 2 * layer_elems, shard_codes[j], shard_elems) ||
+                overlaps(out_bf16, 2 * layer_elems, shard_scales[j], 4 * nblocks))
+                return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        const zpp_status st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (layer_elems) {
+        const hipError_t e = zpp::launch_gather(shards, num_shards, shard_elems, block,
+                                                layer_elems, out_bf16, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API const char *zpp_status_string(zpp_status s) {
+    switch (s) {
+    case ZPP_OK: return "ok";
+    case ZPP_EINVAL: return "invalid argument";
+    case ZPP_EALIGN: return "misaligned pointer";
+    case ZPP_EOVERLAP: return "overlapping buffers";
+    case ZPP_EHIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+ZPP_API int zpp_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

@@ -1,0 +1,44 @@
+// Device-side helpers shared by the partition-path kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zpp {
+
+constexpr int kThreads = 256;  // 4 wave64 per workgroup
+constexpr int kWave = 64;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// float -> bf16 bits, round to nearest even.  Adding 0x7FFF plus the lowest
+// kept bit carries into the kept half exactly when the dropped half is above
+// one half ulp, or exactly one half with an odd kept half.  NaN maps to the
+// canonical 0x7FC0; +-Inf and overflow come out as +-Inf by the same carry.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    return ((u & 0x7FFFFFFFu) > 0x7F800000u) ? 0x7FC0u : r;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return bf16_rne_bits(lo) | (bf16_rne_bits(hi) << 16);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Streaming accesses: every byte is touched once, so loads and stores are
+// marked non-temporal.
+template <typename T>
+__device__ __forceinline__ T ld_nt(const T *p) {
+    return __builtin_nontemporal_load(p);
+}
+template <typename T>
+__device__ __forceinline__ void st_nt(T *p, T v) {
+    __builtin_nontemporal_store(v, p);
+}
+
+}  // namespace zpp

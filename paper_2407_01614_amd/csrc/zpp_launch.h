@@ -1,0 +1,42 @@
+// Internal launchers behind the C ABI.  Arguments are already validated; each
+// launcher only enqueues its kernel on `stream` and returns the launch error.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace zpp {
+
+struct AdamConsts {
+    float lr_wd;      // lr * weight_decay (decoupled decay)
+    float wd;         // weight_decay (L2 form)
+    float beta1, one_minus_beta1;
+    float beta2, one_minus_beta2;
+    float step_size;  // lr / (1 - beta1^t)
+    float inv_bc2;    // 1 / (1 - beta2^t)
+    float eps;
+    int adamw;
+};
+
+hipError_t launch_adam(float *p, float *m, float *v, const float *g, uint16_t *out, size_t n,
+                       const AdamConsts &c, bool vector_path, hipStream_t stream);
+
+hipError_t launch_refresh(uint16_t *dst, const uint16_t *src, size_t count, bool vector_path,
+                          hipStream_t stream);
+
+hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
+                           float *scales, bool vector_path, hipStream_t stream);
+
+constexpr uint32_t kMaxShards = 64;
+
+struct GatherShards {
+    const int8_t *codes[kMaxShards];
+    const float *scales[kMaxShards];
+};
+
+hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t shard_elems,
+                         uint32_t block, size_t layer_elems, uint16_t *out, bool vector_path,
+                         hipStream_t stream);
+
+}  // namespace zpp

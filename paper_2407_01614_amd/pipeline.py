@@ -1,0 +1,160 @@
+"""One simulated rank's partition path on three HIP streams.
+
+Per iteration (Algorithm 1 seen from one rank, one GPU):
+  compute stream : optimizer step on the rank's partition -> bf16 primary
+  copy stream    : refresh the hpZ secondary copy from the primary, then
+                   quantize it (qwZ)
+  comm stream    : backward gather of one layer from the P' node-local
+                   secondary shards, dequantizing on the way
+
+Local rank 0's shard of the gathered layer is the first s codes of this
+rank's own freshly quantized secondary; the other P' - 1 shards stand for the
+peers of the secondary group and live in this GPU's memory.  The gather waits
+on the quantize's event (the ordering fix); the next iteration's optimizer
+step waits for the gather, which closes the write-after-read edges on the
+primary, the secondary and the codes.
+
+Buffers are laid out flat in HBM, one allocation per array, 256-byte
+aligned (torch's allocator), so every kernel takes its 16-byte vector path.
+"""
+import numpy as np
+import torch
+
+from . import synth
+from . import zpp
+from .workloads import BYTES_ADAM, BYTES_REFRESH, bytes_gather, bytes_quant
+
+
+class PartitionPipeline:
+    def __init__(self, wl, device="cuda"):
+        self.wl = wl
+        self.dev = device
+        n, s, B = wl.n, wl.shard_elems, wl.block
+        if s > n:
+            raise ValueError("the local gather shard (%d) must fit in the rank partition (%d)"
+                             % (s, n))
+        f32 = dict(dtype=torch.float32, device=device)
+        self.master = torch.empty(n, **f32)
+        self.exp_avg = torch.zeros(n, **f32)
+        self.exp_avg_sq = torch.zeros(n, **f32)
+        self.grad = torch.empty(n, **f32)
+        self.primary = torch.empty(n, dtype=torch.int16, device=device)
+        self.secondary = torch.empty(n, dtype=torch.int16, device=device)
+        self.codes = torch.empty(n, dtype=torch.int8, device=device)
+        self.scales = torch.empty((n + B - 1) // B, **f32)
+        P2 = wl.secondary_world
+        self.peer_codes = [torch.empty(s, dtype=torch.int8, device=device) for _ in range(P2 - 1)]
+        self.peer_scales = [torch.empty(s // B, **f32) for _ in range(P2 - 1)]
+        self.out = torch.empty(wl.layer_elems, dtype=torch.int16, device=device)
+        self.compute = torch.cuda.Stream(device)
+        self.copy = torch.cuda.Stream(device)
+        self.comm = torch.cuda.Stream(device)
+        self.ev_primary = zpp.Event()
+        self.ev_quant = zpp.Event()
+        self.ev_gather = zpp.Event()
+        self.step_count = 0
+        self.timing = None
+
+    # ------------------------------------------------------------------
+    # inputs
+    # ------------------------------------------------------------------
+    def load(self, master, grad, peer_codes=None, peer_scales=None):
+        """Copy host arrays in: the fp32 master shard and its gradient; the
+        peers' quantized shards if given (else see `quantize_peers`)."""
+        self.master.copy_(torch.from_numpy(master))
+        self.grad.copy_(torch.from_numpy(grad))
+        self.exp_avg.zero_()
+        self.exp_avg_sq.zero_()
+        if peer_codes is not None:
+            for t, a in zip(self.peer_codes, peer_codes):
+                t.copy_(torch.from_numpy(a))
+            for t, a in zip(self.peer_scales, peer_scales):
+                t.copy_(torch.from_numpy(a))
+        self.step_count = 0
+        torch.cuda.synchronize(self.dev)
+
+    def quantize_peers(self, cfg):
+        """Fill the peer shards by quantizing synthetic bf16 weights with the
+        library's own quantizer (set-up work, not part of a step)."""
+        s = self.wl.shard_elems
+        for j, (c, sc) in enumerate(zip(self.peer_codes, self.peer_scales)):
+            w = synth.device_bf16_weights(s, cfg, rank=j + 1, device=self.dev)
+            zpp.quantize_blockwise_i8(w, c, sc, block=self.wl.block)
+            torch.cuda.synchronize(self.dev)
+            del w
+
+    def load_synthetic(self):
+        """Seeded synthetic state drawn on the device: master ~ N(0, 0.02),
+        grad ~ N(0, 1e-3), zero moments, peers quantized from N(0, 0.02)."""
+        wl = self.wl
+        self.master.copy_(synth.device_normal_f32(wl.n, synth.WEIGHT_STD, wl.cfg_id,
+                                                  synth.KIND_MASTER, device=self.dev))
+        self.grad.copy_(synth.device_normal_f32(wl.n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD,
+                                                device=self.dev))
+        self.exp_avg.zero_()
+        self.exp_avg_sq.zero_()
+        self.step_count = 0
+        torch.cuda.synchronize(self.dev)
+        self.quantize_peers(wl.cfg_id)
+
+    # ------------------------------------------------------------------
+    # one iteration
+    # ------------------------------------------------------------------
+    def enable_timing(self):
+        """Record a HIP timing-event pair around every kernel, on the stream
+        that kernel runs on."""
+        self.timing = {k: [] for k in ("adam", "refresh", "quant", "gather")}
+
+    def _timed(self, name, stream, fn):
+        if self.timing is None:
+            fn()
+            return
+        a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        self.timing[name].append((a, b))
+
+    def step(self):
+        wl = self.wl
+        n, s, B = wl.n, wl.shard_elems, wl.block
+        self.step_count += 1
+        t = self.step_count
+        if t > 1:
+            zpp.stream_wait(self.compute, self.ev_gather)
+        self._timed("adam", self.compute, lambda: zpp.adam_partition_step(
+            self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
+            stream=self.compute, **wl.adam))
+        self.ev_primary.record(self.compute)
+        zpp.stream_wait(self.copy, self.ev_primary)
+        self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
+            self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary))
+        self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
+            self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
+            done_after=self.ev_quant))
+        zpp.stream_wait(self.comm, self.ev_quant)
+        self._timed("gather", self.comm, lambda: zpp.dequant_gather_layer(
+            [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
+            wl.layer_elems, self.out, block=B, stream=self.comm, wait_events=[self.ev_quant],
+            done_after=self.ev_gather))
+
+    def wait(self):
+        self.ev_gather.synchronize()
+        torch.cuda.synchronize(self.dev)
+
+    # ------------------------------------------------------------------
+    # accounting
+    # ------------------------------------------------------------------
+    def kernel_bytes(self):
+        wl = self.wl
+        return {
+            "adam": BYTES_ADAM * wl.n,
+            "refresh": BYTES_REFRESH * wl.n,
+            "quant": float(bytes_quant(wl.n, wl.block)),
+            "gather": float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems,
+                                         wl.block)),
+        }
+
+    def kernel_times_ms(self):
+        """Per-kernel list of event-measured durations (ms); call after wait()."""
+        return {k: [a.elapsed_ms(b) for a, b in v] for k, v in self.timing.items()}

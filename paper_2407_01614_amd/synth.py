@@ -64,6 +64,55 @@ def bf16_weights(n, cfg, rank=0, it=0, std=WEIGHT_STD):
     return (f.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
+# --------------------------------------------------------------------------
+# Device-side draws (torch's seeded GPU generator): same distributions, drawn
+# in HBM directly, for the full-size workloads where host generation would
+# dominate set-up time.  The host copies of what a test samples are taken
+# from these tensors, so both sides still see identical inputs.
+# --------------------------------------------------------------------------
+def _device_gen(cfg, kind, rank, it, device):
+    seed = int(np.random.SeedSequence([int(cfg), int(kind), int(rank), int(it)]).generate_state(1)[0])
+    gen = torch_mod().Generator(device=device)
+    gen.manual_seed(seed)
+    return gen
+
+
+def torch_mod():
+    import torch
+    return torch
+
+
+def device_normal_f32(n, std, cfg, kind, rank=0, it=0, device="cuda"):
+    torch = torch_mod()
+    out = torch.empty(n, dtype=torch.float32, device=device)
+    out.normal_(0.0, float(std), generator=_device_gen(cfg, kind, rank, it, device))
+    return out
+
+
+def device_bf16_weights(n, cfg, rank=0, it=0, std=WEIGHT_STD, device="cuda"):
+    """bf16 bit patterns (as int16) of N(0, std^2) draws: the high halves of
+    float32 draws, as in `bf16_weights`."""
+    torch = torch_mod()
+    f = device_normal_f32(n, std, cfg, KIND_LAYER, rank, it, device)
+    return (f.view(torch.int32) >> 16).to(torch.int16)
+
+
+def device_random_codes(n, cfg, rank=0, device="cuda"):
+    """int8 codes uniform in [-127, 127], drawn on the device."""
+    torch = torch_mod()
+    return torch.randint(-127, 128, (n,), dtype=torch.int8, device=device,
+                         generator=_device_gen(cfg, KIND_CODES, rank, 0, device))
+
+
+def device_random_scales(nblocks, cfg, rank=0, lo=1e-5, hi=1e-3, device="cuda"):
+    """Positive float32 scales, log-uniform in [lo, hi], drawn on the device."""
+    torch = torch_mod()
+    e = torch.empty(nblocks, dtype=torch.float64, device=device)
+    e.uniform_(float(np.log(lo)), float(np.log(hi)),
+               generator=_device_gen(cfg, KIND_SCALES, rank, 0, device))
+    return e.exp().to(torch.float32)
+
+
 def random_bits16(n, cfg, rank=0):
     """Arbitrary 16-bit patterns, NaN and Inf payloads included."""
     return rng(cfg, KIND_BITS, rank).integers(0, 1 << 16, size=n, dtype=np.uint16)

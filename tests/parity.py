@@ -1,0 +1,115 @@
+"""Comparison rules between the HIP path and the oracle, and host<->device
+plumbing for the GPU tests.
+
+Tolerances:
+  * refresh, int8 codes, fp32 scales, gathered bf16: bit for bit (one correct
+    result exists for identical inputs);
+  * Adam fp32 master / moments: max relative error 1e-5, with the relative
+    error of element i taken as |a - r| / max(|r|, tau): tau = lr for the
+    master weights (a weight that lands within one update of zero after the
+    decay and the update cancel has no meaningful relative error) and
+    tau = 1e-6 * max|r| for each moment array;
+  * Adam bf16 primary: within 1 bf16 ulp (the fp32 results may differ in the
+    last bits, which can move a value across a bf16 rounding boundary).
+"""
+import numpy as np
+import torch
+
+REL_TOL = 1e-5
+
+
+def rel_err(a, r, tau):
+    a = np.asarray(a, np.float64)
+    r = np.asarray(r, np.float64)
+    return np.abs(a - r) / np.maximum(np.abs(r), tau)
+
+
+def assert_same_nan(a, r, what):
+    na, nr = np.isnan(a), np.isnan(r)
+    assert np.array_equal(na, nr), "%s: NaN positions differ (%d vs %d)" % (what, na.sum(), nr.sum())
+    return ~na
+
+
+def assert_adam_close(got, ref, lr, what=""):
+    """got/ref: (p, m, v, bf16) tuples of numpy arrays."""
+    gp, gm, gv, gb = got
+    rp, rm, rv, rb = ref
+    ok = assert_same_nan(gp, rp, what + " master")
+    e = rel_err(gp[ok], rp[ok], lr)
+    assert e.size == 0 or e.max() <= REL_TOL, "%s master rel err %.3g" % (what, e.max())
+    for a, r, name in ((gm, rm, "exp_avg"), (gv, rv, "exp_avg_sq")):
+        ok = assert_same_nan(a, r, what + " " + name)
+        if ok.any():
+            tau = max(1e-6 * float(np.abs(r[ok]).max()), np.finfo(np.float32).tiny)
+            e = rel_err(a[ok], r[ok], tau)
+            assert e.max() <= REL_TOL, "%s %s rel err %.3g" % (what, name, e.max())
+    assert_bf16_within_ulp(gb, rb, what + " bf16")
+
+
+def bf16_ordered(h):
+    h = np.asarray(h, np.uint16).astype(np.int32)
+    mag = h & 0x7FFF
+    return np.where(h & 0x8000, -mag, mag)
+
+
+def bf16_is_nan(h):
+    h = np.asarray(h, np.uint16)
+    return ((h & 0x7F80) == 0x7F80) & ((h & 0x007F) != 0)
+
+
+def assert_bf16_within_ulp(got, ref, what=""):
+    gn, rn = bf16_is_nan(got), bf16_is_nan(ref)
+    assert np.array_equal(gn, rn), what + ": NaN positions differ"
+    assert np.all(np.asarray(got)[gn] == 0x7FC0), what + ": NaN not canonical"
+    d = np.abs(bf16_ordered(got)[~gn] - bf16_ordered(ref)[~gn])
+    assert d.size == 0 or d.max() <= 1, "%s: bf16 differs by %d ulp" % (what, d.max())
+
+
+def assert_bits_equal(got, ref, what=""):
+    got = np.asarray(got)
+    ref = np.asarray(ref)
+    assert got.shape == ref.shape, "%s: shape %s vs %s" % (what, got.shape, ref.shape)
+    g = got.view(np.uint8) if got.dtype.itemsize else got
+    r = ref.view(np.uint8) if ref.dtype.itemsize else ref
+    if not np.array_equal(g, r):
+        gw = got.view({1: np.uint8, 2: np.uint16, 4: np.uint32}[got.dtype.itemsize])
+        rw = ref.view({1: np.uint8, 2: np.uint16, 4: np.uint32}[ref.dtype.itemsize])
+        bad = np.nonzero(gw != rw)[0]
+        raise AssertionError("%s: %d of %d elements differ; first at %d: got %#x want %#x"
+                             % (what, bad.size, got.size, bad[0], int(gw[bad[0]]),
+                                int(rw[bad[0]])))
+
+
+# ---------------------------------------------------------------------------
+# host <-> device
+# ---------------------------------------------------------------------------
+_TORCH_OF = {np.dtype(np.float32): torch.float32, np.dtype(np.int8): torch.int8,
+             np.dtype(np.uint16): torch.int16}
+
+
+def to_dev(a, device="cuda", pad=0):
+    """numpy -> new contiguous device tensor (uint16 travels as int16);
+    ``pad`` extra zero elements are allocated in front, and the returned
+    tensor is the view that starts ``pad`` elements in (misaligned views)."""
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    t = torch.from_numpy(a)
+    if pad:
+        buf = torch.zeros(a.size + pad, dtype=t.dtype, device=device)
+        buf[pad:].copy_(t.to(device))
+        return buf[pad:]
+    return t.to(device).contiguous()
+
+
+def empty_dev(n, np_dtype, device="cuda", pad=0, fill=None):
+    dt = _TORCH_OF[np.dtype(np_dtype)]
+    buf = torch.empty(n + pad, dtype=dt, device=device)
+    if fill is not None:
+        buf.fill_(fill)
+    return buf[pad:] if pad else buf
+
+
+def to_host(t, np_dtype):
+    a = t.detach().cpu().numpy()
+    return a.view(np_dtype)

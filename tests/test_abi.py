@@ -1,0 +1,176 @@
+"""The C ABI, on the CPU: the library loads, exports every function the
+header declares, and rejects bad arguments before any HIP call.
+
+Only argument combinations that fail validation (or are zero-size no-ops
+without events) are passed here; fake device pointers are never dereferenced
+because validation returns first.  Nothing here launches a kernel.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zpp.h")
+LIB = os.path.join(ROOT, "paper_2407_01614_amd", "libzpp.so")
+
+
+@pytest.fixture(scope="module")
+def zpp():
+    if not os.path.exists(LIB):
+        from paper_2407_01614_amd import build
+        build.build()
+    from paper_2407_01614_amd import zpp as mod
+    return mod
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"ZPP_API\s+[\w\s\*]*?\b(zpp_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for fn in ("zpp_adam_partition_step", "zpp_refresh_secondary", "zpp_quantize_blockwise_i8",
+               "zpp_dequant_gather_layer", "zpp_status_string", "zpp_last_hip_error"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol(zpp):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for fn in declared_functions():
+        assert fn in exported, fn
+        assert hasattr(zpp.raw, fn)
+    # nothing else of the library's own is exported
+    own = {s for s in exported if "zpp" in s.lower()}
+    assert own == set(declared_functions())
+
+
+def test_header_compiles_as_c():
+    src = '#include "zpp.h"\nint main(void){ return (int)sizeof(zpp_adam_hparams) - 32; }\n'
+    r = subprocess.run(["gcc", "-x", "c", "-std=c99", "-fsyntax-only", "-Wall", "-Werror",
+                        "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                        "-I", "/opt/rocm/include", "-"], input=src, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def test_hparams_layout(zpp):
+    assert ctypes.sizeof(zpp.AdamHParams) == 32
+    assert zpp.AdamHParams.step.offset == 24
+
+
+def test_status_strings(zpp):
+    for s in range(5):
+        assert zpp.raw.zpp_status_string(s)
+    assert zpp.raw.zpp_status_string(99) == b"unknown status"
+
+
+# fake, never-dereferenced device addresses
+A = 0x7F0000000000
+B = 0x7F0010000000
+C = 0x7F0020000000
+D = 0x7F0030000000
+E = 0x7F0040000000
+
+
+def hp(zpp, **kw):
+    base = dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, adamw=1, step=1)
+    base.update(kw)
+    return zpp.AdamHParams(base["lr"], base["beta1"], base["beta2"], base["eps"],
+                           base["weight_decay"], base["adamw"], base["step"])
+
+
+def adam(zpp, ptrs=(A, B, C, D, E), n=1024, h=None):
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_adam_partition_step(*ptrs, n, ctypes.byref(h) if h is not False else None,
+                                           None)
+
+
+def test_adam_validation(zpp):
+    assert adam(zpp, h=False) == zpp.ZPP_EINVAL
+    assert adam(zpp, n=0) == zpp.ZPP_OK  # no-op, nothing enqueued
+    assert adam(zpp, ptrs=(None, B, C, D, E)) == zpp.ZPP_EINVAL
+    assert adam(zpp, ptrs=(A, B, C, D, None)) == zpp.ZPP_EINVAL
+    assert adam(zpp, ptrs=(A + 2, B, C, D, E)) == zpp.ZPP_EALIGN
+    assert adam(zpp, ptrs=(A, B, C, D, E + 1)) == zpp.ZPP_EALIGN
+    assert adam(zpp, ptrs=(A, A, C, D, E)) == zpp.ZPP_EOVERLAP
+    assert adam(zpp, ptrs=(A, B, C, D, A + 4 * 1023)) == zpp.ZPP_EOVERLAP
+    assert adam(zpp, ptrs=(A, B, C, B + 4, E)) == zpp.ZPP_EOVERLAP
+    for bad in (dict(step=0), dict(beta1=1.0), dict(beta2=-0.1), dict(eps=-1.0),
+                dict(lr=float("nan")), dict(weight_decay=float("inf"))):
+        assert adam(zpp, h=hp(zpp, **bad)) == zpp.ZPP_EINVAL, bad
+    assert adam(zpp, n=(1 << 64) - 1) == zpp.ZPP_EINVAL
+
+
+def test_refresh_validation(zpp):
+    r = zpp.raw.zpp_refresh_secondary
+    assert r(None, None, 0, None, None, None) == zpp.ZPP_OK
+    assert r(None, B, 16, None, None, None) == zpp.ZPP_EINVAL
+    assert r(A + 1, B, 16, None, None, None) == zpp.ZPP_EALIGN
+    assert r(A, A + 30, 16, None, None, None) == zpp.ZPP_EOVERLAP
+    assert r(A, A, 16, None, None, None) == zpp.ZPP_EOVERLAP
+    assert r(A, B, (1 << 63), None, None, None) == zpp.ZPP_EINVAL
+
+
+def test_quant_validation(zpp):
+    q = zpp.raw.zpp_quantize_blockwise_i8
+    for blk in (0, 32, 100, 192, 8192):
+        assert q(A, 1024, blk, B, C, None, None, None) == zpp.ZPP_EINVAL, blk
+    assert q(None, 0, 256, None, None, None, None, None) == zpp.ZPP_OK
+    assert q(None, 0, 3, None, None, None, None, None) == zpp.ZPP_EINVAL
+    assert q(A, 1024, 256, None, C, None, None, None) == zpp.ZPP_EINVAL
+    assert q(A + 1, 1024, 256, B, C, None, None, None) == zpp.ZPP_EALIGN
+    assert q(A, 1024, 256, B, C + 2, None, None, None) == zpp.ZPP_EALIGN
+    assert q(A, 1024, 256, A + 2046, C, None, None, None) == zpp.ZPP_EOVERLAP
+    assert q(A, 1024, 256, B, B + 1020, None, None, None) == zpp.ZPP_EOVERLAP
+    assert q(A, 1024, 256, B, A + 2044, None, None, None) == zpp.ZPP_EOVERLAP
+
+
+def gather(zpp, codes, scales, num=None, s=1024, block=256, N=None, out=E, waits=None, nwait=0):
+    P = ctypes.c_void_p
+    k = len(codes if codes is not None else scales)
+    carr = (P * max(k, 1))(*codes) if codes is not None else None
+    sarr = (P * max(k, 1))(*scales) if scales is not None else None
+    num = k if num is None else num
+    N = num * s if N is None else N
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    return zpp.raw.zpp_dequant_gather_layer(carr, sarr, num, s, block, N, out, None, warr, nwait,
+                                            None)
+
+
+def test_gather_validation(zpp):
+    cs = [A, B]
+    ss = [C, D]
+    assert gather(zpp, cs, ss, num=0) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, num=65) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, block=100) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, s=0) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, N=2 * 1024 + 1) == zpp.ZPP_EINVAL
+    assert gather(zpp, None, ss) == zpp.ZPP_EINVAL
+    assert gather(zpp, [A, None], ss) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, [C, D + 2]) == zpp.ZPP_EALIGN
+    assert gather(zpp, cs, ss, out=E + 1) == zpp.ZPP_EALIGN
+    assert gather(zpp, cs, ss, out=None) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, out=B + 100) == zpp.ZPP_EOVERLAP
+    assert gather(zpp, cs, ss, out=D - 100) == zpp.ZPP_EOVERLAP
+    assert gather(zpp, cs, ss, nwait=1, waits=None) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, nwait=1, waits=[None]) == zpp.ZPP_EINVAL
+    assert gather(zpp, cs, ss, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
+    # an empty layer is a valid no-op (no events given: no HIP call)
+    assert gather(zpp, cs, ss, N=0, out=None) == zpp.ZPP_OK
+
+
+def test_no_oracle_in_product_path():
+    """The product package never reaches for the oracle, nor for any CPU
+    fallback of the computation."""
+    pkg = os.path.join(ROOT, "paper_2407_01614_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle|liboracle|zpp_oracle|orc_",
+                                     text, re.M), f

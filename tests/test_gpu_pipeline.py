@@ -1,0 +1,237 @@
+"""The whole partition path on streams, and the ordering fix of the paper.
+
+Stream layout (one simulated rank, as in the benchmark):
+  compute stream : Adam partition step  -> event `primary_ready`
+  copy stream    : wait primary_ready, refresh secondary, quantize -> `quant_done`
+  comm stream    : wait quant_done (the fix), dequant-gather -> `gather_done`
+The next iteration's refresh waits on `gather_done` (the buffer it overwrites
+is still being read until then).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_01614_amd import synth
+from paper_2407_01614_amd.workloads import WORKLOADS
+from parity import assert_adam_close, assert_bits_equal, empty_dev, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+TINY = WORKLOADS["tiny"]
+
+
+@pytest.fixture(scope="module")
+def zpp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2407_01614_amd import zpp as mod
+    return mod
+
+
+def f32hp(hp):
+    return {k: float(np.float32(v)) for k, v in hp.items()}
+
+
+def oracle_tiny_pipeline(hp):
+    """The Tiny workload on the oracle: 4 ranks step their partitions, the
+    forward-gathered layer is their concatenation, local rank j of the
+    secondary group (P' = 2) copies its slice, quantizes it, and the backward
+    gather rebuilds the layer."""
+    n, P, P2, B = TINY.n, TINY.world, TINY.secondary_world, TINY.block
+    N = TINY.layer_elems
+    ranks = []
+    layer = np.empty(N, np.uint16)
+    for r in range(P):
+        p = synth.master_weights(n, TINY.cfg_id, r)
+        g = synth.gradients(n, TINY.cfg_id, r)
+        z = np.zeros(n, np.float32)
+        res = oracle.adam_step(p, z, z, g, step=1, **hp)
+        ranks.append(res)
+        b, e = oracle.primary_slice(N, P, r)
+        layer[b:e] = res[3]
+    s = oracle.secondary_shard_elems(N, P2, B)
+    secondaries = []
+    quants = []
+    for j in range(P2):
+        b, e = oracle.secondary_slice(N, P2, j, B)
+        sec = np.zeros(s, np.uint16)
+        sec[:e - b] = oracle.refresh(layer[b:e])
+        secondaries.append(sec)
+        quants.append(oracle.quantize_blockwise_i8(sec, B))
+    out = oracle.dequant_gather_layer([q[0] for q in quants], [q[1] for q in quants], s, B, N)
+    return ranks, layer, secondaries, quants, out
+
+
+def assert_downstream(g_prim, r_prim, g_codes, g_scales, r_codes, r_scales, B, what):
+    """Quantized results computed from the GPU's and the oracle's own primary:
+    bit-exact in every block whose inputs agree (the primaries may differ by 1
+    bf16 ulp at a few elements); elsewhere codes move by at most 1."""
+    same = (g_prim.reshape(-1, B) == r_prim.reshape(-1, B)).all(axis=1)
+    assert same.mean() > 0.99, what
+    gc, rc = g_codes.reshape(-1, B), r_codes.reshape(-1, B)
+    assert_bits_equal(gc[same], rc[same], what + " codes")
+    assert_bits_equal(g_scales[same], r_scales[same], what + " scales")
+    assert np.abs(gc[~same].astype(int) - rc[~same]).max(initial=0) <= 1
+    return same
+
+
+def test_tiny_pipeline_on_streams(zpp):
+    hp = f32hp(TINY.adam)
+    n, P, P2, B, N = TINY.n, TINY.world, TINY.secondary_world, TINY.block, TINY.layer_elems
+    s = TINY.shard_elems
+    compute, copy, comm = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    layer = empty_dev(N, np.uint16, fill=0x7FC0)
+    states, grads = [], []
+    for r in range(P):
+        states.append((to_dev(synth.master_weights(n, TINY.cfg_id, r)),
+                       torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")))
+        grads.append(to_dev(synth.gradients(n, TINY.cfg_id, r)))
+    torch.cuda.synchronize()
+    primary_ready = zpp.Event()
+    for r in range(P):
+        p, m, v = states[r]
+        zpp.adam_partition_step(p, m, v, grads[r], layer[r * n:(r + 1) * n], step=1,
+                                stream=compute, **hp)
+    primary_ready.record(compute)
+    secs = [empty_dev(s, np.uint16, fill=0x7FC0) for _ in range(P2)]
+    codes = [empty_dev(s, np.int8, fill=0) for _ in range(P2)]
+    scales = [empty_dev(s // B, np.float32, fill=float("nan")) for _ in range(P2)]
+    quant_done = [zpp.Event() for _ in range(P2)]
+    gather_done = zpp.Event()
+    for j in range(P2):
+        zpp.refresh_secondary(secs[j], layer[j * s:(j + 1) * s], stream=copy,
+                              wait_before=primary_ready)
+        zpp.quantize_blockwise_i8(secs[j], codes[j], scales[j], block=B, stream=copy,
+                                  done_after=quant_done[j])
+    out = empty_dev(N, np.uint16, fill=0x5A5A)
+    zpp.dequant_gather_layer(codes, scales, s, N, out, block=B, stream=comm,
+                             wait_events=quant_done, done_after=gather_done)
+    gather_done.synchronize()
+    torch.cuda.synchronize()
+
+    ranks, ref_layer, ref_secs, ref_quants, ref_out = oracle_tiny_pipeline(hp)
+    for r in range(P):
+        p, m, v = states[r]
+        got = (to_host(p, np.float32), to_host(m, np.float32), to_host(v, np.float32),
+               to_host(layer[r * n:(r + 1) * n], np.uint16))
+        assert_adam_close(got, ranks[r], hp["lr"], "rank %d" % r)
+    glayer = to_host(layer, np.uint16)
+    same_blocks = []
+    for j in range(P2):
+        gsec = to_host(secs[j], np.uint16)
+        assert_bits_equal(gsec, glayer[j * s:(j + 1) * s], "secondary %d = its slice" % j)
+        same_blocks.append(assert_downstream(gsec, ref_secs[j], to_host(codes[j], np.int8),
+                                             to_host(scales[j], np.float32), ref_quants[j][0],
+                                             ref_quants[j][1], B, "shard %d" % j))
+    same = np.concatenate(same_blocks)
+    gout = to_host(out, np.uint16).reshape(-1, B)
+    assert_bits_equal(gout[same], ref_out.reshape(-1, B)[same], "gathered layer")
+
+
+def run_race(zpp, fixed, s=1 << 20, B=256, spin_cycles=100_000_000):
+    """Refresh + quantize shard 0 on the copy stream behind a long device-side
+    spin; gather on the comm stream, waiting on the quantize's event only when
+    `fixed`.  The secondary starts as NaN poison, standing in for the
+    uninitialised torch.empty buffer of the paper's allocation."""
+    src = synth.bf16_weights(s, 90, 0)
+    peer = synth.bf16_weights(s, 90, 1)
+    pc, ps = oracle.quantize_blockwise_i8(peer, B)
+    sc, ss = oracle.quantize_blockwise_i8(src, B)
+    expect = oracle.dequant_gather_layer([sc, pc], [ss, ps], s, B, 2 * s)
+    tsrc, tpc, tps = to_dev(src), to_dev(pc), to_dev(ps)
+    copy, comm = torch.cuda.Stream(), torch.cuda.Stream()
+    sec = empty_dev(s, np.uint16, fill=0x7FC0)
+    codes = empty_dev(s, np.int8, fill=0)
+    scales = empty_dev(s // B, np.float32, fill=float("nan"))
+    out = empty_dev(2 * s, np.uint16, fill=0)
+    torch.cuda.synchronize()
+    done = zpp.Event()
+    with torch.cuda.stream(copy):
+        torch.cuda._sleep(spin_cycles)  # bounded spin kernel: the copy is still queued
+    zpp.refresh_secondary(sec, tsrc, stream=copy)
+    zpp.quantize_blockwise_i8(sec, codes, scales, block=B, stream=copy, done_after=done)
+    zpp.dequant_gather_layer([codes, tpc], [scales, tps], s, 2 * s, out, block=B, stream=comm,
+                             wait_events=[done] if fixed else [])
+    torch.cuda.synchronize()
+    return to_host(out, np.uint16), expect
+
+
+def test_fix_orders_gather_after_refresh(zpp):
+    """With the event wait (the paper's fix) the gather is exact, every time."""
+    for _ in range(5):
+        got, expect = run_race(zpp, fixed=True)
+        assert_bits_equal(got, expect, "gather after the fix")
+
+
+def test_race_without_the_fix_reads_poison(zpp):
+    """Without the wait the gather runs while the copy is still queued behind
+    the spin and reads the poisoned shard: NaN in the gathered layer, as the
+    paper reports for stock hpZ."""
+    got, expect = run_race(zpp, fixed=False)
+    s = 1 << 20
+    nan = (got & 0x7FFF) > 0x7F80
+    assert nan[:s].mean() > 0.99, "the racy gather did not see the poison"
+    assert_bits_equal(got[s:], expect[s:], "peer shard")
+
+
+def test_iterations_with_buffer_reuse(zpp):
+    """Three iterations reusing the same secondary, codes and scale buffers:
+    each refresh waits for the new primary and for the previous gather
+    (write-after-read), each gather for the quantize; every iteration's state
+    and gathered layer is checked against the oracle's own trajectory."""
+    hp = f32hp(TINY.adam)
+    n = 1 << 18
+    B = 256
+    P2 = 2
+    s = n  # the local shard is this rank's primary; the peer shard is settled
+    compute, copy, comm = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    p0 = synth.master_weights(n, 91)
+    tp, tm, tv = to_dev(p0), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+    prim = empty_dev(n, np.uint16)
+    sec = empty_dev(s, np.uint16, fill=0x7FC0)
+    codes = empty_dev(s, np.int8)
+    scales = empty_dev(s // B, np.float32)
+    peer = synth.bf16_weights(s, 91, 1)
+    pc, ps = oracle.quantize_blockwise_i8(peer, B)
+    tpc, tps = to_dev(pc), to_dev(ps)
+    out = empty_dev(P2 * s, np.uint16)
+    ev_prim, ev_refresh, ev_quant, ev_gather = zpp.Event(), zpp.Event(), zpp.Event(), zpp.Event()
+    grads = [synth.gradients(n, 91, it=t) for t in range(1, 4)]
+    dgrads = [to_dev(g) for g in grads]
+    torch.cuda.synchronize()
+    snaps = []
+    for t in range(1, 4):
+        if t > 1:
+            zpp.stream_wait(compute, ev_refresh)  # the last refresh has read the primary
+        zpp.adam_partition_step(tp, tm, tv, dgrads[t - 1], prim, step=t, stream=compute, **hp)
+        ev_prim.record(compute)
+        if t > 1:
+            zpp.stream_wait(copy, ev_gather)  # the last gather has read codes and scales
+        zpp.refresh_secondary(sec, prim, stream=copy, wait_before=ev_prim, done_after=ev_refresh)
+        zpp.quantize_blockwise_i8(sec, codes, scales, block=B, stream=copy, done_after=ev_quant)
+        zpp.dequant_gather_layer([codes, tpc], [scales, tps], s, P2 * s, out, block=B,
+                                 stream=comm, wait_events=[ev_quant], done_after=ev_gather)
+        snap = empty_dev(P2 * s, np.uint16)
+        with torch.cuda.stream(comm):
+            snap.copy_(out)
+        snaps.append(snap)
+    torch.cuda.synchronize()
+
+    rp, rm, rv = p0, np.zeros(n, np.float32), np.zeros(n, np.float32)
+    for t in range(1, 4):
+        rp, rm, rv, rb = oracle.adam_step(rp, rm, rv, grads[t - 1], step=t, **hp)
+        rc, rs = oracle.quantize_blockwise_i8(rb, B)
+        r_out = oracle.dequant_gather_layer([rc, pc], [rs, ps], s, B, P2 * s)
+        g_out = to_host(snaps[t - 1], np.uint16)
+        # the peer half is exact every iteration
+        assert_bits_equal(g_out[s:], r_out[s:], "peer half, iteration %d" % t)
+        # the local half is the dequantized primary of this iteration
+        d = np.abs(g_out[:s].view(np.int16).astype(np.int32) - r_out[:s].view(np.int16))
+        assert (d == 0).mean() > 0.99, "iteration %d" % t
+    got = (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
+           to_host(prim, np.uint16))
+    assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "after 3 iterations")
+    same = assert_downstream(to_host(prim, np.uint16), rb, to_host(codes, np.int8),
+                             to_host(scales, np.float32), rc, rs, B, "last iteration")
+    last = to_host(snaps[-1], np.uint16)[:s].reshape(-1, B)
+    assert_bits_equal(last[same], r_out[:s].reshape(-1, B)[same], "last gathered layer")
