@@ -73,7 +73,7 @@ def test_fullsize_adam_two_steps(zpp):
     r1 = oracle.adam_step(p0, z, z, gh1, step=1, **hp)
     assert_adam_close(got1, r1, hp["lr"], "step 1")
     r2 = oracle.adam_step(r1[0], r1[1], r1[2], gh2, step=2, **hp)
-    assert_adam_close(got2, r2, hp["lr"], "step 2")
+    assert_adam_close(got2, r2, hp["lr"], "step 2", prev=r1[:3], g=gh2, hp=hp)
     # properties on everything: finite, bf16 is the rounding of the master
     assert torch.isfinite(p).all() and torch.isfinite(v).all() and (v >= 0).all()
     hi = (p.view(torch.int32) >> 16).to(torch.int16)

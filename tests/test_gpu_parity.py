@@ -72,11 +72,13 @@ def test_adam_multistep(zpp, adamw, hp):
     for t in range(1, 8):
         g = synth.gradients(n, 40, it=t) * np.float32(5.0)
         zpp.adam_partition_step(tp, tm, tv, to_dev(g), out, step=t, adamw=adamw, **hp)
+        prev = (rp, rm, rv)
         rp, rm, rv, rb = oracle.adam_step(rp, rm, rv, g, step=t, adamw=adamw, **hp)
         torch.cuda.synchronize()
         got = (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
                to_host(out, np.uint16))
-        assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "step %d" % t)
+        assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "step %d" % t, prev=prev, g=g,
+                          hp=hp, adamw=adamw)
 
 
 @pytest.mark.parametrize("n", [1, 3, 4, 5, 1023, 2047, 2048, 2049, 3 * 2048 + 7, 100003])
@@ -88,7 +90,7 @@ def test_adam_ragged(zpp, n, pad):
     m, v = synth.moments(n, 41, n)
     got = run_adam_gpu(zpp, p, m, v, g, hp, 3, pad=pad)
     ref = oracle.adam_step(p, m, v, g, step=3, **hp)
-    assert_adam_close(got, ref, hp["lr"], "n=%d pad=%d" % (n, pad))
+    assert_adam_close(got, ref, hp["lr"], "n=%d pad=%d" % (n, pad), prev=(p, m, v), g=g, hp=hp)
 
 
 def test_adam_nonfinite_and_zero_grads(zpp):
@@ -116,7 +118,7 @@ def test_adam_large_step_count(zpp):
     m, v = synth.moments(n, 43)
     got = run_adam_gpu(zpp, p, m, v, g, hp, 123456)
     ref = oracle.adam_step(p, m, v, g, step=123456, **hp)
-    assert_adam_close(got, ref, hp["lr"])
+    assert_adam_close(got, ref, hp["lr"], prev=(p, m, v), g=g, hp=hp)
 
 
 def test_adam_checkpoint_resume_is_bitwise(zpp):
