@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama-2-13b")
-    ap.add_argument("--cpu-sample", type=float, default=0.25,
+    ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of the workload the CPU oracle is timed on (0 = skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters, if present")
@@ -164,7 +164,7 @@ def main():
         "gather": {"GB/s": kernels["gather"]["GB/s"],
                    "frac_of_peak": kernels["gather"]["frac_of_peak"]},
         "kernels": kernels,
-        "device": torch.cuda.get_device_name(0),
+        "device": torch.cuda.get_device_properties(0).gcnArchName,
     }
     del pipe
     torch.cuda.empty_cache()

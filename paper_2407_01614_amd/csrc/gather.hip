@@ -4,13 +4,14 @@
 //
 // The shard pointers travel by value in the kernel arguments; blockIdx.y picks
 // the shard, so the pointer is a uniform (scalar) load.  Vector kernel: a lane
-// turns 16 codes (one 16-byte load) and one scale (shared by the 16 lanes of
-// a 256-block, served from cache) into 16 bf16 (two 16-byte stores).
+// turns 8 codes (one 8-byte load) and one scale (shared by the 32 lanes of a
+// 256-block, served from cache) into 8 bf16 (one 16-byte store), about three
+// VALU operations per element.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
 #ifndef ZPP_GATHER_UNROLL
-#define ZPP_GATHER_UNROLL 2
+#define ZPP_GATHER_UNROLL 4
 #endif
 #ifndef ZPP_GATHER_MAX_GRID_X
 #define ZPP_GATHER_MAX_GRID_X (1u << 20)
@@ -31,21 +32,32 @@ __device__ __forceinline__ float code_f32(uint32_t w, int byte) {
     return (float)(int)(int8_t)(uint8_t)(w >> (8 * byte));
 }
 
-// 4 codes of one word -> 2 words of packed bf16; finite scale, so no NaN
-// can arise (finite * finite never is NaN) and the NaN test is skipped.
-__device__ __forceinline__ u32x2 dequant_word_finite(uint32_t w, float s) {
-    u32x2 r;
-    const uint32_t b0 = __float_as_uint(code_f32(w, 0) * s);
-    const uint32_t b1 = __float_as_uint(code_f32(w, 1) * s);
-    const uint32_t b2 = __float_as_uint(code_f32(w, 2) * s);
-    const uint32_t b3 = __float_as_uint(code_f32(w, 3) * s);
-    r.x = ((b0 + 0x7FFFu + ((b0 >> 16) & 1u)) >> 16) |
-          ((b1 + 0x7FFFu + ((b1 >> 16) & 1u)) & 0xFFFF0000u);
-    r.y = ((b2 + 0x7FFFu + ((b2 >> 16) & 1u)) >> 16) |
-          ((b3 + 0x7FFFu + ((b3 >> 16) & 1u)) & 0xFFFF0000u);
-    return r;
+// Scales in [2^-100, 2^100]: every product code * s is zero or a normal
+// float, and -128 * s is exact.  For such scales the product is formed as
+// fma(u, s, -128 s) with u = code + 128 taken straight from the byte by the
+// unsigned byte converts; u*s - 128*s equals code*s exactly, so the single
+// rounding of the fma is the rounding of code * s.  The pair is then rounded
+// to bf16 (nearest even) by the packed convert.
+__device__ __forceinline__ bool fast_scale(float s) {
+    return s >= 0x1p-100f && s <= 0x1p100f;
 }
 
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+    const bf16x2 v = __builtin_convertvector((f32x2){lo, hi}, bf16x2);
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// 4 codes (one word, biased by 0x80 per byte) -> 2 words of packed bf16
+__device__ __forceinline__ u32x2 dequant_word_fast(uint32_t biased, float s, float c) {
+    const float x0 = __builtin_fmaf((float)(biased & 0xFFu), s, c);
+    const float x1 = __builtin_fmaf((float)((biased >> 8) & 0xFFu), s, c);
+    const float x2 = __builtin_fmaf((float)((biased >> 16) & 0xFFu), s, c);
+    const float x3 = __builtin_fmaf((float)(biased >> 24), s, c);
+    return u32x2{bf16x2_rne(x0, x1), bf16x2_rne(x2, x3)};
+}
+
+// Any scale (zero, negative, tiny, huge, Inf, NaN): one rounded product and
+// the integer RNE of bf16_rne_bits, NaN made canonical.
 __device__ __forceinline__ u32x2 dequant_word_any(uint32_t w, float s) {
     u32x2 r;
     r.x = pack_bf16x2(code_f32(w, 0) * s, code_f32(w, 1) * s);
@@ -53,9 +65,13 @@ __device__ __forceinline__ u32x2 dequant_word_any(uint32_t w, float s) {
     return r;
 }
 
+// A row is one wave-wide pass: 64 lanes x 8 consecutive codes = 512 output
+// elements, read as one contiguous 512-byte load and written as one
+// contiguous 1 KiB store.  A tile is U rows per wave.
 template <int U>
 __global__ __launch_bounds__(kThreads) void gather_vec_kernel(GatherArgs a) {
-    constexpr size_t kTile = (size_t)kThreads * 16 * U;
+    constexpr size_t kRow = (size_t)kThreads * 8;  // elements per row of the workgroup
+    constexpr size_t kTile = kRow * U;
     const uint32_t j = blockIdx.y;
     const size_t lo = (size_t)j * a.shard_elems;
     if (lo >= a.layer_elems)
@@ -67,39 +83,35 @@ __global__ __launch_bounds__(kThreads) void gather_vec_kernel(GatherArgs a) {
     uint16_t *__restrict__ out = a.out + lo;
     const size_t ntiles = (valid + kTile - 1) / kTile;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-        const size_t base = t * kTile + (size_t)threadIdx.x * 16;
+        const size_t base = t * kTile + (size_t)threadIdx.x * 8;
         if ((t + 1) * kTile <= valid) {
-            u32x4 c[U];
+            u32x2 c[U];
             float s[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i = base + (size_t)u * kThreads * 16;
-                c[u] = ld_nt(reinterpret_cast<const u32x4 *>(codes + i));
+                const size_t i = base + (size_t)u * kRow;
+                c[u] = ld_nt(reinterpret_cast<const u32x2 *>(codes + i));
                 s[u] = scales[i >> a.block_shift];
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i = base + (size_t)u * kThreads * 16;
-                u32x2 r0, r1, r2, r3;
-                if (__builtin_isfinite(s[u])) {
-                    r0 = dequant_word_finite(c[u].x, s[u]);
-                    r1 = dequant_word_finite(c[u].y, s[u]);
-                    r2 = dequant_word_finite(c[u].z, s[u]);
-                    r3 = dequant_word_finite(c[u].w, s[u]);
+                const size_t i = base + (size_t)u * kRow;
+                u32x2 r0, r1;
+                if (fast_scale(s[u])) {
+                    const float cb = -128.0f * s[u];
+                    r0 = dequant_word_fast(c[u].x ^ 0x80808080u, s[u], cb);
+                    r1 = dequant_word_fast(c[u].y ^ 0x80808080u, s[u], cb);
                 } else {
                     r0 = dequant_word_any(c[u].x, s[u]);
                     r1 = dequant_word_any(c[u].y, s[u]);
-                    r2 = dequant_word_any(c[u].z, s[u]);
-                    r3 = dequant_word_any(c[u].w, s[u]);
                 }
                 st_nt(reinterpret_cast<u32x4 *>(out + i), u32x4{r0.x, r0.y, r1.x, r1.y});
-                st_nt(reinterpret_cast<u32x4 *>(out + i + 8), u32x4{r2.x, r2.y, r3.x, r3.y});
             }
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i0 = base + (size_t)u * kThreads * 16;
-                for (size_t i = i0; i < i0 + 16 && i < valid; ++i) {
+                const size_t i0 = base + (size_t)u * kRow;
+                for (size_t i = i0; i < i0 + 8 && i < valid; ++i) {
                     const float x = (float)codes[i] * scales[i >> a.block_shift];
                     out[i] = (uint16_t)bf16_rne_bits(x);
                 }
@@ -138,7 +150,7 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
     a.block_shift = (uint32_t)__builtin_ctz(block);
     const size_t per_shard = shard_elems < layer_elems ? shard_elems : layer_elems;
     if (vector_path) {
-        constexpr size_t kTile = (size_t)kThreads * 16 * ZPP_GATHER_UNROLL;
+        constexpr size_t kTile = (size_t)kThreads * 8 * ZPP_GATHER_UNROLL;
         const size_t tiles = (per_shard + kTile - 1) / kTile;
         const unsigned gx =
             (unsigned)(tiles < ZPP_GATHER_MAX_GRID_X ? tiles : ZPP_GATHER_MAX_GRID_X);

@@ -12,6 +12,9 @@ constexpr int kWave = 64;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
 // float -> bf16 bits, round to nearest even.  Adding 0x7FFF plus the lowest
 // kept bit carries into the kept half exactly when the dropped half is above

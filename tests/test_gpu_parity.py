@@ -321,6 +321,20 @@ def test_gather_special_scales(zpp):
                           "special scales")
 
 
+def test_gather_rounding_ties(zpp):
+    """Every code against scales 2^e (1 + k 2^-9): many products fall exactly
+    halfway between two bf16 values, so ties-to-even is exercised in the fast
+    path (scales inside [2^-100, 2^100]) and in the generic one (outside)."""
+    block = 256
+    ks = np.arange(1, 129, dtype=np.float64)
+    exps = [-133, -120, -101, -100, -30, 0, 7, 99, 100, 101, 110]
+    sc = np.concatenate([(1.0 + ks * 2.0 ** -9) * 2.0 ** e for e in exps]).astype(np.float32)
+    codes = np.tile(np.concatenate([np.arange(-128, 128, dtype=np.int16)]).astype(np.int8), sc.size)
+    s = codes.size
+    got = run_gather_gpu(zpp, [codes], [sc], s, block, s)
+    assert_bits_equal(got, oracle.dequant_gather_layer([codes], [sc], s, block, s), "ties")
+
+
 def test_gather_arbitrary_codes(zpp):
     P2, s, block = 8, 256 * 640, 256
     codes = [synth.random_codes(s, 63, j) for j in range(P2)]
