@@ -1,16 +1,21 @@
 // Partition step: Adam(W) over one rank's flat fp32 shard, emitting the bf16
 // primary shard (optimizer.step() of Algorithm 1 on the rank's partition).
 //
-// Pure streaming work: 16 B read + 14 B written per element and about 30
-// VALU operations, so HBM bandwidth is the bound.  Each thread owns U float4
-// groups per tile; a wave's load instruction covers 1 KiB of one array, all
-// 4*U loads of a tile are issued before any arithmetic, and every access is
-// non-temporal (nothing is reused).
+// Pure streaming work: 16 B read + 14 B written per element and about 45
+// VALU operations (correctly rounded sqrt and division included), so HBM
+// bandwidth is the bound.  Each thread owns U float4 groups per tile; a wave's
+// load instruction covers 1 KiB of one array, all 4*U loads of a tile are
+// issued before any arithmetic, and every access is non-temporal (nothing is
+// reused).  The grid is one-shot (one tile per workgroup): on this GPU a
+// persistent grid of a few thousand workgroups streams about 20% slower.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
 #ifndef ZPP_ADAM_UNROLL
-#define ZPP_ADAM_UNROLL 2
+#define ZPP_ADAM_UNROLL 1
+#endif
+#ifndef ZPP_ADAM_THREADS
+#define ZPP_ADAM_THREADS 64
 #endif
 #ifndef ZPP_ADAM_MAX_GRID
 #define ZPP_ADAM_MAX_GRID (1u << 20)
@@ -40,9 +45,11 @@ __device__ __forceinline__ void adam_update(float &p, float &m, float &v, float 
     p = p - c.step_size * (m / denom);
 }
 
+constexpr int kAdamThreads = ZPP_ADAM_THREADS;
+
 template <bool ADAMW, int U>
-__global__ __launch_bounds__(kThreads) void adam_vec_kernel(AdamArgs a) {
-    constexpr size_t kTile = (size_t)kThreads * 4 * U;
+__global__ __launch_bounds__(kAdamThreads) void adam_vec_kernel(AdamArgs a) {
+    constexpr size_t kTile = (size_t)kAdamThreads * 4 * U;
     const size_t ntiles = (a.n + kTile - 1) / kTile;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const size_t base = t * kTile + (size_t)threadIdx.x * 4;
@@ -50,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void adam_vec_kernel(AdamArgs a) {
             f32x4 P[U], M[U], V[U], G[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i = base + (size_t)u * kThreads * 4;
+                const size_t i = base + (size_t)u * kAdamThreads * 4;
                 P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
                 M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
                 V[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
@@ -58,7 +65,7 @@ __global__ __launch_bounds__(kThreads) void adam_vec_kernel(AdamArgs a) {
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i = base + (size_t)u * kThreads * 4;
+                const size_t i = base + (size_t)u * kAdamThreads * 4;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     float p = P[u][e], m = M[u][e], v = V[u][e];
@@ -80,7 +87,7 @@ __global__ __launch_bounds__(kThreads) void adam_vec_kernel(AdamArgs a) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 for (int e = 0; e < 4; ++e) {
-                    const size_t i = base + (size_t)u * kThreads * 4 + e;
+                    const size_t i = base + (size_t)u * kAdamThreads * 4 + e;
                     if (i < a.n) {
                         float p = a.p[i], m = a.m[i], v = a.v[i];
                         adam_update<ADAMW>(p, m, v, a.g[i], a.c);
@@ -115,15 +122,15 @@ hipError_t launch_adam(float *p, float *m, float *v, const float *g, uint16_t *o
                        const AdamConsts &c, bool vector_path, hipStream_t stream) {
     AdamArgs a{p, m, v, g, out, n, c};
     if (vector_path) {
-        constexpr size_t kTile = (size_t)kThreads * 4 * ZPP_ADAM_UNROLL;
+        constexpr size_t kTile = (size_t)kAdamThreads * 4 * ZPP_ADAM_UNROLL;
         size_t tiles = (n + kTile - 1) / kTile;
         const unsigned grid = (unsigned)(tiles < ZPP_ADAM_MAX_GRID ? tiles : ZPP_ADAM_MAX_GRID);
         if (c.adamw)
             hipLaunchKernelGGL((adam_vec_kernel<true, ZPP_ADAM_UNROLL>), dim3(grid),
-                               dim3(kThreads), 0, stream, a);
+                               dim3(kAdamThreads), 0, stream, a);
         else
             hipLaunchKernelGGL((adam_vec_kernel<false, ZPP_ADAM_UNROLL>), dim3(grid),
-                               dim3(kThreads), 0, stream, a);
+                               dim3(kAdamThreads), 0, stream, a);
     } else {
         size_t blocks = (n + kThreads - 1) / kThreads;
         const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));

@@ -13,12 +13,17 @@
 #ifndef ZPP_GATHER_UNROLL
 #define ZPP_GATHER_UNROLL 4
 #endif
+#ifndef ZPP_GATHER_THREADS
+#define ZPP_GATHER_THREADS 256
+#endif
 #ifndef ZPP_GATHER_MAX_GRID_X
 #define ZPP_GATHER_MAX_GRID_X (1u << 20)
 #endif
 
 namespace zpp {
 namespace {
+
+constexpr int kGatherThreads = ZPP_GATHER_THREADS;
 
 struct GatherArgs {
     GatherShards shards;
@@ -69,8 +74,8 @@ __device__ __forceinline__ u32x2 dequant_word_any(uint32_t w, float s) {
 // elements, read as one contiguous 512-byte load and written as one
 // contiguous 1 KiB store.  A tile is U rows per wave.
 template <int U>
-__global__ __launch_bounds__(kThreads) void gather_vec_kernel(GatherArgs a) {
-    constexpr size_t kRow = (size_t)kThreads * 8;  // elements per row of the workgroup
+__global__ __launch_bounds__(kGatherThreads) void gather_vec_kernel(GatherArgs a) {
+    constexpr size_t kRow = (size_t)kGatherThreads * 8;  // elements per row of the workgroup
     constexpr size_t kTile = kRow * U;
     const uint32_t j = blockIdx.y;
     const size_t lo = (size_t)j * a.shard_elems;
@@ -150,12 +155,12 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
     a.block_shift = (uint32_t)__builtin_ctz(block);
     const size_t per_shard = shard_elems < layer_elems ? shard_elems : layer_elems;
     if (vector_path) {
-        constexpr size_t kTile = (size_t)kThreads * 8 * ZPP_GATHER_UNROLL;
+        constexpr size_t kTile = (size_t)kGatherThreads * 8 * ZPP_GATHER_UNROLL;
         const size_t tiles = (per_shard + kTile - 1) / kTile;
         const unsigned gx =
             (unsigned)(tiles < ZPP_GATHER_MAX_GRID_X ? tiles : ZPP_GATHER_MAX_GRID_X);
         hipLaunchKernelGGL((gather_vec_kernel<ZPP_GATHER_UNROLL>), dim3(gx, num_shards),
-                           dim3(kThreads), 0, stream, a);
+                           dim3(kGatherThreads), 0, stream, a);
     } else {
         const size_t blocks = (per_shard + kThreads - 1) / kThreads;
         const unsigned gx = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));

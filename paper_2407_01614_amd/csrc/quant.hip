@@ -13,6 +13,12 @@
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
+#ifndef ZPP_QUANT_UNROLL
+#define ZPP_QUANT_UNROLL 2
+#endif
+#ifndef ZPP_QUANT_THREADS
+#define ZPP_QUANT_THREADS 256
+#endif
 #ifndef ZPP_QUANT_MAX_GRID
 #define ZPP_QUANT_MAX_GRID (1u << 20)
 #endif
@@ -21,6 +27,7 @@ namespace zpp {
 namespace {
 
 constexpr uint32_t kScaleNaNBits = 0x7FC00000u;
+constexpr int kQuantThreads = ZPP_QUANT_THREADS;
 
 struct BlockQuant {
     float scale;  // value stored for the block
@@ -96,14 +103,15 @@ __device__ __forceinline__ u16x2 absbits2(uint32_t w) {
     return __builtin_bit_cast(u16x2, w & 0x7FFF7FFFu);
 }
 
-template <int B>
-__global__ __launch_bounds__(kThreads) void quant_vec_kernel(const uint16_t *__restrict__ src,
+template <int B, int U>
+__global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(const uint16_t *__restrict__ src,
                                                              size_t n, int8_t *__restrict__ codes,
                                                              float *__restrict__ scales) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;  // lanes per quant block
     constexpr int V = (B / 8 > kWave) ? B / (8 * kWave) : 1;
     constexpr int kGroupsPerWave = kWave / L;
-    constexpr int kGroupsPerBlock = kGroupsPerWave * (kThreads / kWave);
+    constexpr int kGroupsPerRow = kGroupsPerWave * (kQuantThreads / kWave);
+    constexpr int kGroupsPerBlock = kGroupsPerRow * U;
     const size_t nblocks = (n + B - 1) / B;
     const int lane = threadIdx.x & (kWave - 1);
     const int gl = lane / L;
@@ -112,48 +120,60 @@ __global__ __launch_bounds__(kThreads) void quant_vec_kernel(const uint16_t *__r
 
     for (size_t g0 = (size_t)blockIdx.x * kGroupsPerBlock; g0 < nblocks;
          g0 += (size_t)gridDim.x * kGroupsPerBlock) {
-        const size_t k = g0 + (size_t)wave * kGroupsPerWave + gl;
-        const bool valid = k < nblocks;
-        u32x4 x[V];
-        u16x2 m2 = {0, 0};
+        // all U rows of loads first, then the reductions and stores
+        u32x4 x[U][V];
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const size_t i = k * B + ((size_t)v * L + li) * 8;
-            if (valid && i + 8 <= n) {
-                x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
-            } else {
-                uint32_t h[8];
+        for (int u = 0; u < U; ++u) {
+            const size_t k = g0 + (size_t)u * kGroupsPerRow + (size_t)wave * kGroupsPerWave + gl;
+            const bool valid = k < nblocks;
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    h[e] = (valid && i + e < n) ? (uint32_t)src[i + e] : 0u;
-                x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                             h[6] | (h[7] << 16)};
+            for (int v = 0; v < V; ++v) {
+                const size_t i = k * B + ((size_t)v * L + li) * 8;
+                if (valid && i + 8 <= n) {
+                    x[u][v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
+                } else {
+                    uint32_t h[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        h[e] = (valid && i + e < n) ? (uint32_t)src[i + e] : 0u;
+                    x[u][v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16),
+                                    h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+                }
             }
-            m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
-                     __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
-                     __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
         }
-        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
 #pragma unroll
-        for (int off = L / 2; off >= 1; off >>= 1)
-            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        for (int u = 0; u < U; ++u) {
+            const size_t k = g0 + (size_t)u * kGroupsPerRow + (size_t)wave * kGroupsPerWave + gl;
+            const bool valid = k < nblocks;
+            u16x2 m2 = {0, 0};
+#pragma unroll
+            for (int v = 0; v < V; ++v)
+                m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
+                         __builtin_elementwise_max(absbits2(x[u][v].x), absbits2(x[u][v].y)),
+                         __builtin_elementwise_max(absbits2(x[u][v].z), absbits2(x[u][v].w))));
+            uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+            for (int off = L / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
 
-        const BlockQuant q = block_params(mx);
+            const BlockQuant q = block_params(mx);
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const size_t i = k * B + ((size_t)v * L + li) * 8;
-            u32x2 c;
-            c.x = quant_word(x[v].x, x[v].y, q);
-            c.y = quant_word(x[v].z, x[v].w, q);
-            if (valid && i + 8 <= n) {
-                st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
-            } else if (valid) {
-                for (int e = 0; e < 8 && i + e < n; ++e)
-                    codes[i + e] = (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
+            for (int v = 0; v < V; ++v) {
+                const size_t i = k * B + ((size_t)v * L + li) * 8;
+                u32x2 c;
+                c.x = quant_word(x[u][v].x, x[u][v].y, q);
+                c.y = quant_word(x[u][v].z, x[u][v].w, q);
+                if (valid && i + 8 <= n) {
+                    st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
+                } else if (valid) {
+                    for (int e = 0; e < 8 && i + e < n; ++e)
+                        codes[i + e] =
+                            (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
+                }
             }
+            if (valid && li == 0)
+                scales[k] = q.scale;
         }
-        if (valid && li == 0)
-            scales[k] = q.scale;
     }
 }
 
@@ -187,12 +207,12 @@ template <int B>
 void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales,
                 hipStream_t stream) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;
-    constexpr size_t kGroupsPerBlock = (kWave / L) * (kThreads / kWave);
+    constexpr size_t kGroupsPerBlock = (kWave / L) * (kQuantThreads / kWave) * ZPP_QUANT_UNROLL;
     const size_t nblocks = (n + B - 1) / B;
     const size_t need = (nblocks + kGroupsPerBlock - 1) / kGroupsPerBlock;
     const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
-    hipLaunchKernelGGL((quant_vec_kernel<B>), dim3(grid), dim3(kThreads), 0, stream, src, n,
-                       codes, scales);
+    hipLaunchKernelGGL((quant_vec_kernel<B, ZPP_QUANT_UNROLL>), dim3(grid), dim3(kQuantThreads), 0,
+                       stream, src, n, codes, scales);
 }
 
 }  // namespace

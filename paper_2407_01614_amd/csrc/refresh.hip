@@ -8,6 +8,9 @@
 #ifndef ZPP_REFRESH_UNROLL
 #define ZPP_REFRESH_UNROLL 4
 #endif
+#ifndef ZPP_REFRESH_THREADS
+#define ZPP_REFRESH_THREADS 256
+#endif
 #ifndef ZPP_REFRESH_MAX_GRID
 #define ZPP_REFRESH_MAX_GRID (1u << 20)
 #endif
@@ -15,11 +18,13 @@
 namespace zpp {
 namespace {
 
+constexpr int kRefreshThreads = ZPP_REFRESH_THREADS;
+
 template <int U>
-__global__ __launch_bounds__(kThreads) void refresh_vec_kernel(uint16_t *__restrict__ dst,
+__global__ __launch_bounds__(kRefreshThreads) void refresh_vec_kernel(uint16_t *__restrict__ dst,
                                                                const uint16_t *__restrict__ src,
                                                                size_t count) {
-    constexpr size_t kTile = (size_t)kThreads * 8 * U;  // 8 bf16 per 16-byte vector
+    constexpr size_t kTile = (size_t)kRefreshThreads * 8 * U;  // 8 bf16 per 16-byte vector
     const size_t ntiles = (count + kTile - 1) / kTile;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const size_t base = t * kTile + (size_t)threadIdx.x * 8;
@@ -27,14 +32,14 @@ __global__ __launch_bounds__(kThreads) void refresh_vec_kernel(uint16_t *__restr
             u32x4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                x[u] = ld_nt(reinterpret_cast<const u32x4 *>(src + base + (size_t)u * kThreads * 8));
+                x[u] = ld_nt(reinterpret_cast<const u32x4 *>(src + base + (size_t)u * kRefreshThreads * 8));
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                st_nt(reinterpret_cast<u32x4 *>(dst + base + (size_t)u * kThreads * 8), x[u]);
+                st_nt(reinterpret_cast<u32x4 *>(dst + base + (size_t)u * kRefreshThreads * 8), x[u]);
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const size_t i0 = base + (size_t)u * kThreads * 8;
+                const size_t i0 = base + (size_t)u * kRefreshThreads * 8;
                 if (i0 + 8 <= count) {
                     st_nt(reinterpret_cast<u32x4 *>(dst + i0),
                           ld_nt(reinterpret_cast<const u32x4 *>(src + i0)));
@@ -60,11 +65,12 @@ __global__ __launch_bounds__(kThreads) void refresh_scalar_kernel(uint16_t *__re
 hipError_t launch_refresh(uint16_t *dst, const uint16_t *src, size_t count, bool vector_path,
                           hipStream_t stream) {
     if (vector_path) {
-        constexpr size_t kTile = (size_t)kThreads * 8 * ZPP_REFRESH_UNROLL;
+        constexpr size_t kTile = (size_t)kRefreshThreads * 8 * ZPP_REFRESH_UNROLL;
         const size_t tiles = (count + kTile - 1) / kTile;
         const unsigned grid =
             (unsigned)(tiles < ZPP_REFRESH_MAX_GRID ? tiles : ZPP_REFRESH_MAX_GRID);
-        hipLaunchKernelGGL((refresh_vec_kernel<ZPP_REFRESH_UNROLL>), dim3(grid), dim3(kThreads),
+        hipLaunchKernelGGL((refresh_vec_kernel<ZPP_REFRESH_UNROLL>), dim3(grid),
+                           dim3(kRefreshThreads),
                            0, stream, dst, src, count);
     } else {
         const size_t blocks = (count + kThreads - 1) / kThreads;

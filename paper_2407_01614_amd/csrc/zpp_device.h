@@ -6,7 +6,10 @@
 
 namespace zpp {
 
-constexpr int kThreads = 256;  // 4 wave64 per workgroup
+#ifndef ZPP_THREADS
+#define ZPP_THREADS 256
+#endif
+constexpr int kThreads = ZPP_THREADS;  // workgroup size: 4 wave64 by default
 constexpr int kWave = 64;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -35,13 +38,25 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 
 // Streaming accesses: every byte is touched once, so loads and stores are
 // marked non-temporal.
+#ifndef ZPP_NT_LOAD
+#define ZPP_NT_LOAD 1
+#endif
+#ifndef ZPP_NT_STORE
+#define ZPP_NT_STORE 1
+#endif
 template <typename T>
 __device__ __forceinline__ T ld_nt(const T *p) {
-    return __builtin_nontemporal_load(p);
+    if constexpr (ZPP_NT_LOAD)
+        return __builtin_nontemporal_load(p);
+    else
+        return *p;
 }
 template <typename T>
 __device__ __forceinline__ void st_nt(T *p, T v) {
-    __builtin_nontemporal_store(v, p);
+    if constexpr (ZPP_NT_STORE)
+        __builtin_nontemporal_store(v, p);
+    else
+        *p = v;
 }
 
 }  // namespace zpp
