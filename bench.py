@@ -9,7 +9,11 @@ an event: the paper's fix).
 Prints ONE JSON line.  `value` is the algorithmic HBM bytes of all four
 kernels of a step divided by the measured time per step (GB/s), with every
 input resident in HBM.  Per-kernel durations come from a second run of K
-steps with HIP timing events on each kernel's own stream.  The roofline entry is for the dominant kernel (the
+steps with HIP timing events on each kernel's own stream.  Two further runs
+are reported beside it: the fused step + refresh + quantize kernel in place
+of the three separate ones, and the time per step with the gather ordered by
+a device event wait (the fix), by a host-side wait, or not at all (stock
+hpZ, racy: timing only).  The roofline entry is for the dominant kernel (the
 Adam step).  The CPU baseline times the plain CPU oracle on a bounded sample
 of the same workload on this host.
 
@@ -63,6 +67,18 @@ def measured_traffic(path, workload, kernel, sources):
     if h.hexdigest()[:16] != entry.get("source_digest"):
         return None
     return round(entry["bytes_per_launch"])
+
+
+def kernel_table(kb, times):
+    out = {}
+    for k in kb:
+        ts = sorted(times[k])
+        mean = sum(ts) / len(ts)
+        gbps = kb[k] / (mean * 1e-3) / 1e9
+        out[k] = {"bytes": kb[k], "mean_us": round(mean * 1e3, 2),
+                  "median_us": round(ts[len(ts) // 2] * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
+                  "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    return out
 
 
 def cpu_baseline(wl, frac):
@@ -130,38 +146,41 @@ def main():
     pipe = PartitionPipeline(wl)
     pipe.load_synthetic()
 
-    for _ in range(args.warmup):
-        pipe.step()
-    pipe.wait()
-    # timed region: K steps exactly as the path runs them, no instrumentation
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        pipe.step()
-    pipe.wait()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
-    # then K more steps with a timing-event pair around every kernel, on the
-    # kernel's own stream, for the per-kernel durations
-    pipe.enable_timing()
-    for _ in range(args.steps):
-        pipe.step()
-    pipe.wait()
+    def run(fused, sync, timing):
+        """W warm-up steps, then K timed steps exactly as the path runs them
+        (no instrumentation); with `timing`, K more steps with a timing-event
+        pair around every kernel on that kernel's own stream."""
+        pipe.fused, pipe.sync, pipe.timing = fused, sync, None
+        for _ in range(args.warmup):
+            pipe.step()
+        pipe.wait()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            pipe.step()
+        pipe.wait()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        times = None
+        if timing:
+            pipe.enable_timing()
+            for _ in range(args.steps):
+                pipe.step()
+            pipe.wait()
+            times = pipe.kernel_times_ms()
+            pipe.timing = None
+        return ms, times, pipe.kernel_bytes()
 
-    kb = pipe.kernel_bytes()
-    times = pipe.kernel_times_ms()
+    ms_per_step, times, kb = run(False, "event", True)
+    fused_ms, fused_times, fused_kb = run(True, "event", True)
+    sync_ab = {}
+    for mode in ("event", "host", "none"):
+        sync_ab[mode] = round(run(False, mode, False)[0], 4)
     step_bytes = sum(kb.values())
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    kernels = {}
-    for k in kb:
-        ts = sorted(times[k])
-        mean = sum(ts) / len(ts)
-        med = ts[len(ts) // 2]
-        gbps = kb[k] / (mean * 1e-3) / 1e9
-        kernels[k] = {"bytes": kb[k], "mean_us": round(mean * 1e3, 2),
-                      "median_us": round(med * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
-                      "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    kernels = kernel_table(kb, times)
+    fused_kernels = kernel_table(fused_kb, fused_times)
+    fused_gbps = sum(fused_kb.values()) / (fused_ms * 1e-3) / 1e9
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
     sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
 
@@ -196,6 +215,10 @@ def main():
         "gather": {"GB/s": kernels["gather"]["GB/s"],
                    "frac_of_peak": kernels["gather"]["frac_of_peak"]},
         "kernels": kernels,
+        "fused_step_refresh_quant": {
+            "ms_per_step": round(fused_ms, 4), "GB/s": round(fused_gbps, 1),
+            "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
+        "sync_ab_ms_per_step": sync_ab,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }
     del pipe

@@ -8,6 +8,7 @@
 // issued before any arithmetic, and every access is non-temporal (nothing is
 // reused).  The grid is one-shot (one tile per workgroup): on this GPU a
 // persistent grid of a few thousand workgroups streams about 20% slower.
+#include "zpp_adam.h"
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
@@ -31,19 +32,6 @@ struct AdamArgs {
     size_t n;
     AdamConsts c;
 };
-
-template <bool ADAMW>
-__device__ __forceinline__ void adam_update(float &p, float &m, float &v, float g,
-                                            const AdamConsts &c) {
-    if (ADAMW)
-        p = p - c.lr_wd * p;
-    else
-        g = g + c.wd * p;
-    m = c.beta1 * m + c.one_minus_beta1 * g;
-    v = c.beta2 * v + c.one_minus_beta2 * (g * g);
-    const float denom = __builtin_sqrtf(v * c.inv_bc2) + c.eps;
-    p = p - c.step_size * (m / denom);
-}
 
 constexpr int kAdamThreads = ZPP_ADAM_THREADS;
 

@@ -1,0 +1,165 @@
+// Fused partition step: the Adam update of the rank's partition, its bf16
+// primary, the hpZ secondary copy and the qwZ int8 quantization of that copy,
+// in one pass over HBM (optimizer.step() of Algorithm 1 followed, for the
+// same weights, by the secondary copy of the forward loop and the qwZ
+// quantization that precedes the gather).
+//
+// Per element: 16 B read (p, m, v, g); 12 B + 2 B + 2 B + 1 B written (p, m,
+// v, primary, secondary, code) plus 4 B per block of scale: 33.016 B at block
+// 256, against 30 + 4 + 3.016 = 37.016 B for the three separate kernels,
+// which re-read the primary and the secondary from HBM.  The results are
+// those of the three separate steps, bit for bit, because the quantization
+// reads the same bf16 values the primary holds.
+//
+// One wave per chunk of C = max(B, 256) consecutive elements: lane l holds
+// the 4 elements [chunk + 256 w + 4 l, +4) for w < C / 256.  The bf16 of the
+// updated weights stays in registers (two per 4 elements) until the block's
+// absmax is known; a 256-block is exactly one wave, so its absmax is a
+// six-step cross-lane reduction.
+#include "zpp_adam.h"
+#include "zpp_device.h"
+#include "zpp_launch.h"
+#include "zpp_quant.h"
+
+#ifndef ZPP_FUSED_MAX_GRID
+#define ZPP_FUSED_MAX_GRID (1u << 30)
+#endif
+
+namespace zpp {
+namespace {
+
+struct FusedArgs {
+    float *p, *m, *v;
+    const float *g;
+    uint16_t *primary;
+    uint16_t *secondary;  // may be null: no bf16 secondary copy is kept
+    int8_t *codes;
+    float *scales;
+    size_t n;
+    AdamConsts c;
+};
+
+template <bool ADAMW, int B>
+__global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a) {
+    constexpr int C = B > 256 ? B : 256;  // elements per chunk (one wave)
+    constexpr int W = C / 256;            // float4 groups per lane
+    constexpr int L = B < 256 ? B / 4 : kWave;  // lanes per quant block
+    const int lane = threadIdx.x;
+    const size_t nchunks = (a.n + C - 1) / C;
+    for (size_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
+        const size_t base = ch * C;
+        const bool full = base + C <= a.n;
+        u32x2 pk[W];
+        u16x2 m2 = {0, 0};
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const size_t i = base + (size_t)w * 256 + (size_t)lane * 4;
+            if (full) {
+                f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
+                f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
+                f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
+                const f32x4 G = ld_nt(reinterpret_cast<const f32x4 *>(a.g + i));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float p = P[e], m = M[e], v = V[e];
+                    adam_update<ADAMW>(p, m, v, G[e], a.c);
+                    P[e] = p;
+                    M[e] = m;
+                    V[e] = v;
+                }
+                st_nt(reinterpret_cast<f32x4 *>(a.p + i), P);
+                st_nt(reinterpret_cast<f32x4 *>(a.m + i), M);
+                st_nt(reinterpret_cast<f32x4 *>(a.v + i), V);
+                pk[w] = u32x2{pack_bf16x2(P.x, P.y), pack_bf16x2(P.z, P.w)};
+                st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk[w]);
+                if (a.secondary)
+                    st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk[w]);
+            } else {
+                // the last, partial chunk: element by element; absent elements
+                // hold bf16 zero, which no absmax can see
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    h[e] = 0u;
+                    if (i + e < a.n) {
+                        float p = a.p[i + e], m = a.m[i + e], v = a.v[i + e];
+                        adam_update<ADAMW>(p, m, v, a.g[i + e], a.c);
+                        a.p[i + e] = p;
+                        a.m[i + e] = m;
+                        a.v[i + e] = v;
+                        h[e] = bf16_rne_bits(p);
+                        a.primary[i + e] = (uint16_t)h[e];
+                        if (a.secondary)
+                            a.secondary[i + e] = (uint16_t)h[e];
+                    }
+                }
+                pk[w] = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+            }
+            m2 = __builtin_elementwise_max(
+                m2, __builtin_elementwise_max(absbits2(pk[w].x), absbits2(pk[w].y)));
+        }
+        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+        for (int off = L / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const BlockQuant q = block_params(mx);
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            const size_t i = base + (size_t)w * 256 + (size_t)lane * 4;
+            const uint32_t c4 = quant_word(pk[w].x, pk[w].y, q);
+            if (full) {
+                st_nt(reinterpret_cast<uint32_t *>(a.codes + i), c4);
+            } else {
+                for (int e = 0; e < 4 && i + e < a.n; ++e)
+                    a.codes[i + e] = (int8_t)((c4 >> (8 * e)) & 0xFFu);
+            }
+        }
+        // the first lane of each quant block writes its scale
+        const size_t k = (base + (size_t)lane * 4) / B;
+        if (lane % L == 0 && k * B < a.n)
+            a.scales[k] = q.scale;
+    }
+}
+
+template <int B>
+void launch_fused_b(const FusedArgs &a, hipStream_t stream) {
+    constexpr size_t C = B > 256 ? B : 256;
+    const size_t chunks = (a.n + C - 1) / C;
+    const unsigned grid = (unsigned)(chunks < ZPP_FUSED_MAX_GRID ? chunks : ZPP_FUSED_MAX_GRID);
+    if (a.c.adamw)
+        hipLaunchKernelGGL((fused_kernel<true, B>), dim3(grid), dim3(kWave), 0, stream, a);
+    else
+        hipLaunchKernelGGL((fused_kernel<false, B>), dim3(grid), dim3(kWave), 0, stream, a);
+}
+
+}  // namespace
+
+hipError_t launch_fused(float *p, float *m, float *v, const float *g, uint16_t *primary,
+                        uint16_t *secondary, int8_t *codes, float *scales, size_t n,
+                        uint32_t block, const AdamConsts &c, bool vector_path,
+                        hipStream_t stream) {
+    if (!vector_path) {
+        // any alignment: the three separate scalar kernels, one after another
+        // on the stream, compute the same values
+        hipError_t e = launch_adam(p, m, v, g, primary, n, c, false, stream);
+        if (e == hipSuccess && secondary)
+            e = launch_refresh(secondary, primary, n, false, stream);
+        if (e == hipSuccess)
+            e = launch_quantize(primary, n, block, codes, scales, false, stream);
+        return e;
+    }
+    const FusedArgs a{p, m, v, g, primary, secondary, codes, scales, n, c};
+    switch (block) {
+    case 64: launch_fused_b<64>(a, stream); break;
+    case 128: launch_fused_b<128>(a, stream); break;
+    case 256: launch_fused_b<256>(a, stream); break;
+    case 512: launch_fused_b<512>(a, stream); break;
+    case 1024: launch_fused_b<1024>(a, stream); break;
+    case 2048: launch_fused_b<2048>(a, stream); break;
+    case 4096: launch_fused_b<4096>(a, stream); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace zpp

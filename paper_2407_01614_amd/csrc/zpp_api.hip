@@ -33,6 +33,45 @@ bool valid_block(uint32_t block) {
 // overflow a size_t.
 constexpr size_t kMaxElems = SIZE_MAX / 16;
 
+bool any_overlap(const void *const *ptrs, const size_t *bytes, int k) {
+    for (int x = 0; x < k; ++x)
+        for (int y = x + 1; y < k; ++y)
+            if (overlaps(ptrs[x], bytes[x], ptrs[y], bytes[y]))
+                return true;
+    return false;
+}
+
+zpp_status check_hparams(const zpp_adam_hparams *hp) {
+    if (!hp)
+        return ZPP_EINVAL;
+    if (!isfinite(hp->lr) || !isfinite(hp->beta1) || !isfinite(hp->beta2) ||
+        !isfinite(hp->eps) || !isfinite(hp->weight_decay))
+        return ZPP_EINVAL;
+    if (hp->beta1 < 0.0f || hp->beta1 >= 1.0f || hp->beta2 < 0.0f || hp->beta2 >= 1.0f ||
+        hp->eps < 0.0f || hp->step < 1)
+        return ZPP_EINVAL;
+    return ZPP_OK;
+}
+
+// Step-dependent constants, folded on the host in double and rounded once.
+zpp::AdamConsts adam_consts(const zpp_adam_hparams &hp) {
+    zpp::AdamConsts c;
+    const double b1 = hp.beta1, b2 = hp.beta2, lr = hp.lr, wd = hp.weight_decay;
+    const double bc1 = 1.0 - pow(b1, (double)hp.step);
+    const double bc2 = 1.0 - pow(b2, (double)hp.step);
+    c.lr_wd = (float)(lr * wd);
+    c.wd = hp.weight_decay;
+    c.beta1 = hp.beta1;
+    c.one_minus_beta1 = (float)(1.0 - b1);
+    c.beta2 = hp.beta2;
+    c.one_minus_beta2 = (float)(1.0 - b2);
+    c.step_size = (float)(lr / bc1);
+    c.inv_bc2 = (float)(1.0 / bc2);
+    c.eps = hp.eps;
+    c.adamw = hp.adamw ? 1 : 0;
+    return c;
+}
+
 zpp_status wait_on(hipStream_t stream, hipEvent_t ev) {
     if (!ev)
         return ZPP_OK;
@@ -52,16 +91,11 @@ zpp_status record(hipStream_t stream, hipEvent_t ev) {
 extern "C" {
 
 ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float *exp_avg_sq,
-                                   const float *grad, uint16_t *primary_bf16, size_t n,
-                                   const zpp_adam_hparams *hp, hipStream_t stream) {
-    if (!hp)
-        return ZPP_EINVAL;
-    if (!isfinite(hp->lr) || !isfinite(hp->beta1) || !isfinite(hp->beta2) ||
-        !isfinite(hp->eps) || !isfinite(hp->weight_decay))
-        return ZPP_EINVAL;
-    if (hp->beta1 < 0.0f || hp->beta1 >= 1.0f || hp->beta2 < 0.0f || hp->beta2 >= 1.0f ||
-        hp->eps < 0.0f || hp->step < 1)
-        return ZPP_EINVAL;
+                                           const float *grad, uint16_t *primary_bf16, size_t n,
+                                           const zpp_adam_hparams *hp, hipStream_t stream) {
+    zpp_status st = check_hparams(hp);
+    if (st != ZPP_OK)
+        return st;
     if (n == 0)
         return ZPP_OK;
     if (n > kMaxElems)
@@ -73,30 +107,57 @@ ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float 
         return ZPP_EALIGN;
     const void *ptrs[5] = {master, exp_avg, exp_avg_sq, grad, primary_bf16};
     const size_t bytes[5] = {4 * n, 4 * n, 4 * n, 4 * n, 2 * n};
-    for (int x = 0; x < 5; ++x)
-        for (int y = x + 1; y < 5; ++y)
-            if (overlaps(ptrs[x], bytes[x], ptrs[y], bytes[y]))
-                return ZPP_EOVERLAP;
-
-    zpp::AdamConsts c;
-    const double b1 = hp->beta1, b2 = hp->beta2, lr = hp->lr, wd = hp->weight_decay;
-    const double bc1 = 1.0 - pow(b1, (double)hp->step);
-    const double bc2 = 1.0 - pow(b2, (double)hp->step);
-    c.lr_wd = (float)(lr * wd);
-    c.wd = hp->weight_decay;
-    c.beta1 = hp->beta1;
-    c.one_minus_beta1 = (float)(1.0 - b1);
-    c.beta2 = hp->beta2;
-    c.one_minus_beta2 = (float)(1.0 - b2);
-    c.step_size = (float)(lr / bc1);
-    c.inv_bc2 = (float)(1.0 / bc2);
-    c.eps = hp->eps;
-    c.adamw = hp->adamw ? 1 : 0;
+    if (any_overlap(ptrs, bytes, 5))
+        return ZPP_EOVERLAP;
     const bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
                      aligned(grad, 16) && aligned(primary_bf16, 16);
-    const hipError_t e =
-        zpp::launch_adam(master, exp_avg, exp_avg_sq, grad, primary_bf16, n, c, vec, stream);
+    const hipError_t e = zpp::launch_adam(master, exp_avg, exp_avg_sq, grad, primary_bf16, n,
+                                          adam_consts(*hp), vec, stream);
     return e == hipSuccess ? ZPP_OK : hip_fail(e);
+}
+
+ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
+                                                  float *exp_avg_sq, const float *grad,
+                                                  uint16_t *primary_bf16,
+                                                  uint16_t *secondary_bf16, int8_t *codes,
+                                                  float *scales, size_t n, uint32_t block,
+                                                  const zpp_adam_hparams *hp,
+                                                  hipStream_t stream, hipEvent_t wait_before,
+                                                  hipEvent_t done_after) {
+    zpp_status st = check_hparams(hp);
+    if (st != ZPP_OK)
+        return st;
+    if (!valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    const size_t nblocks = (n + block - 1) / block;
+    if (n) {
+        if (!master || !exp_avg || !exp_avg_sq || !grad || !primary_bf16 || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(master, 4) || !aligned(exp_avg, 4) || !aligned(exp_avg_sq, 4) ||
+            !aligned(grad, 4) || !aligned(primary_bf16, 2) || !aligned(secondary_bf16, 2) ||
+            !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const void *ptrs[8] = {master, exp_avg, exp_avg_sq, grad, primary_bf16, codes, scales,
+                               secondary_bf16};
+        const size_t bytes[8] = {4 * n, 4 * n, 4 * n, 4 * n, 2 * n, n, 4 * nblocks,
+                                 secondary_bf16 ? 2 * n : 0};
+        if (any_overlap(ptrs, bytes, 8))
+            return ZPP_EOVERLAP;
+    }
+    st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (n) {
+        const bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
+                         aligned(grad, 16) && aligned(primary_bf16, 8) &&
+                         aligned(secondary_bf16, 8) && aligned(codes, 4);
+        const hipError_t e =
+            zpp::launch_fused(master, exp_avg, exp_avg_sq, grad, primary_bf16, secondary_bf16,
+                              codes, scales, n, block, adam_consts(*hp), vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
 }
 
 ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16, size_t count,

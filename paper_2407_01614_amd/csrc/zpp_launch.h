@@ -28,6 +28,13 @@ hipError_t launch_refresh(uint16_t *dst, const uint16_t *src, size_t count, bool
 hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
                            float *scales, bool vector_path, hipStream_t stream);
 
+// Adam step + bf16 primary + optional bf16 secondary + int8 codes/scales of
+// the primary, in one pass (vector_path) or as the three scalar kernels.
+hipError_t launch_fused(float *p, float *m, float *v, const float *g, uint16_t *primary,
+                        uint16_t *secondary, int8_t *codes, float *scales, size_t n,
+                        uint32_t block, const AdamConsts &c, bool vector_path,
+                        hipStream_t stream);
+
 constexpr uint32_t kMaxShards = 64;
 
 struct GatherShards {

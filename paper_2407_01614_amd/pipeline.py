@@ -22,13 +22,27 @@ import torch
 
 from . import synth
 from . import zpp
-from .workloads import BYTES_ADAM, BYTES_REFRESH, bytes_gather, bytes_quant
+from .workloads import BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_gather, bytes_quant
+
+
+SYNC_MODES = ("event", "host", "none")
 
 
 class PartitionPipeline:
-    def __init__(self, wl, device="cuda"):
+    """`fused`: one pass for step + refresh + quantize instead of three
+    kernels.  `sync`: how the gather is ordered after the quantization --
+    "event" (the paper's fix, as a device-side stream wait), "host" (the host
+    blocks on the event before it enqueues the gather: the fix as a host-side
+    wait) or "none" (stock hpZ: no edge at all; the gather may read codes that
+    are not written yet, so only its timing means anything)."""
+
+    def __init__(self, wl, device="cuda", fused=False, sync="event"):
+        if sync not in SYNC_MODES:
+            raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         self.wl = wl
         self.dev = device
+        self.fused = fused
+        self.sync = sync
         n, s, B = wl.n, wl.shard_elems, wl.block
         if s > n:
             raise ValueError("the local gather shard (%d) must fit in the rank partition (%d)"
@@ -103,7 +117,8 @@ class PartitionPipeline:
     def enable_timing(self):
         """Record a HIP timing-event pair around every kernel, on the stream
         that kernel runs on."""
-        self.timing = {k: [] for k in ("adam", "refresh", "quant", "gather")}
+        names = ("fused", "gather") if self.fused else ("adam", "refresh", "quant", "gather")
+        self.timing = {k: [] for k in names}
 
     def _timed(self, name, stream, fn):
         if self.timing is None:
@@ -122,20 +137,31 @@ class PartitionPipeline:
         t = self.step_count
         if t > 1:
             zpp.stream_wait(self.compute, self.ev_gather)
-        self._timed("adam", self.compute, lambda: zpp.adam_partition_step(
-            self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
-            stream=self.compute, **wl.adam))
-        self.ev_primary.record(self.compute)
-        zpp.stream_wait(self.copy, self.ev_primary)
-        self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
-            self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary))
-        self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
-            self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
-            done_after=self.ev_quant))
-        zpp.stream_wait(self.comm, self.ev_quant)
+        if self.fused:
+            self._timed("fused", self.compute, lambda: zpp.adam_step_refresh_quantize(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
+                self.secondary, self.codes, self.scales, step=t, block=B, stream=self.compute,
+                done_after=self.ev_quant, **wl.adam))
+        else:
+            self._timed("adam", self.compute, lambda: zpp.adam_partition_step(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
+                stream=self.compute, **wl.adam))
+            self.ev_primary.record(self.compute)
+            zpp.stream_wait(self.copy, self.ev_primary)
+            self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
+                self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary))
+            self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
+                self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
+                done_after=self.ev_quant))
+        waits = []
+        if self.sync == "event":
+            zpp.stream_wait(self.comm, self.ev_quant)
+            waits = [self.ev_quant]
+        elif self.sync == "host":
+            self.ev_quant.synchronize()
         self._timed("gather", self.comm, lambda: zpp.dequant_gather_layer(
             [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
-            wl.layer_elems, self.out, block=B, stream=self.comm, wait_events=[self.ev_quant],
+            wl.layer_elems, self.out, block=B, stream=self.comm, wait_events=waits,
             done_after=self.ev_gather))
 
     def wait(self):
@@ -147,12 +173,14 @@ class PartitionPipeline:
     # ------------------------------------------------------------------
     def kernel_bytes(self):
         wl = self.wl
+        gather = float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems, wl.block))
+        if self.fused:
+            return {"fused": float(bytes_fused(wl.n, wl.block)), "gather": gather}
         return {
             "adam": BYTES_ADAM * wl.n,
             "refresh": BYTES_REFRESH * wl.n,
             "quant": float(bytes_quant(wl.n, wl.block)),
-            "gather": float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems,
-                                         wl.block)),
+            "gather": gather,
         }
 
     def kernel_times_ms(self):

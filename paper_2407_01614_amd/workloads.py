@@ -108,3 +108,9 @@ def bytes_gather(shard_elems, num_shards, layer_elems, block=BLOCK):
         valid = max(0, min(shard_elems, layer_elems - j * shard_elems))
         blocks += (valid + block - 1) // block
     return read_codes + 4 * blocks + 2 * layer_elems
+
+
+def bytes_fused(n, block=BLOCK):
+    # Adam's 30 B, the secondary copy written (2 B), the codes and scales
+    # written (1 B + 4 B per block); the primary is not read back
+    return 32 * n + n + 4 * ((n + block - 1) // block)

@@ -38,6 +38,9 @@ class AdamHParams(ctypes.Structure):
 
 _lib.zpp_adam_partition_step.restype = ctypes.c_int
 _lib.zpp_adam_partition_step.argtypes = [_P, _P, _P, _P, _P, _sz, ctypes.POINTER(AdamHParams), _P]
+_lib.zpp_adam_step_refresh_quantize.restype = ctypes.c_int
+_lib.zpp_adam_step_refresh_quantize.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _sz, _u32,
+                                                ctypes.POINTER(AdamHParams), _P, _P, _P]
 _lib.zpp_refresh_secondary.restype = ctypes.c_int
 _lib.zpp_refresh_secondary.argtypes = [_P, _P, _sz, _P, _P, _P]
 _lib.zpp_quantize_blockwise_i8.restype = ctypes.c_int
@@ -49,8 +52,9 @@ _lib.zpp_status_string.argtypes = [ctypes.c_int]
 _lib.zpp_last_hip_error.restype = ctypes.c_int
 _lib.zpp_last_hip_error.argtypes = []
 
-EXPORTS = ("zpp_adam_partition_step", "zpp_refresh_secondary", "zpp_quantize_blockwise_i8",
-           "zpp_dequant_gather_layer", "zpp_status_string", "zpp_last_hip_error")
+EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
+           "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_status_string",
+           "zpp_last_hip_error")
 
 
 class ZppError(RuntimeError):
@@ -201,6 +205,35 @@ def adam_partition_step(master, exp_avg, exp_avg_sq, grad, primary_bf16, *, lr, 
                                       primary_bf16.data_ptr(), n, ctypes.byref(hp),
                                       stream_handle(stream))
     _check(st, "zpp_adam_partition_step")
+
+
+def adam_step_refresh_quantize(master, exp_avg, exp_avg_sq, grad, primary_bf16, secondary_bf16,
+                               codes, scales, *, lr, beta1, beta2, eps, weight_decay, step,
+                               adamw=True, block=256, n=None, stream=None, wait_before=None,
+                               done_after=None):
+    """zpp_adam_step_refresh_quantize: the partition step, the secondary copy
+    (``secondary_bf16`` may be None) and its int8 quantization in one pass."""
+    for t, name in ((master, "master"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq"),
+                    (grad, "grad"), (scales, "scales")):
+        _dev(t, _F32, name)
+    _dev(primary_bf16, _BF16, "primary_bf16")
+    if secondary_bf16 is not None:
+        _dev(secondary_bf16, _BF16, "secondary_bf16")
+    _dev(codes, _I8, "codes")
+    if n is None:
+        n = master.numel()
+    bufs = [master, exp_avg, exp_avg_sq, grad, primary_bf16, codes]
+    if secondary_bf16 is not None:
+        bufs.append(secondary_bf16)
+    if any(t.numel() < n for t in bufs) or scales.numel() < num_blocks(n, block):
+        raise ValueError("a buffer is too small for n = %d" % n)
+    hp = AdamHParams(lr, beta1, beta2, eps, weight_decay, 1 if adamw else 0, int(step))
+    st = _lib.zpp_adam_step_refresh_quantize(
+        master.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), grad.data_ptr(),
+        primary_bf16.data_ptr(), secondary_bf16.data_ptr() if secondary_bf16 is not None else None,
+        codes.data_ptr(), scales.data_ptr(), n, block, ctypes.byref(hp), stream_handle(stream),
+        _event_handle(wait_before), _event_handle(done_after))
+    _check(st, "zpp_adam_step_refresh_quantize")
 
 
 def refresh_secondary(secondary_bf16, src_bf16, count=None, *, stream=None, wait_before=None,

@@ -33,8 +33,9 @@ def declared_functions():
 
 def test_header_declares_the_four_calls():
     names = declared_functions()
-    for fn in ("zpp_adam_partition_step", "zpp_refresh_secondary", "zpp_quantize_blockwise_i8",
-               "zpp_dequant_gather_layer", "zpp_status_string", "zpp_last_hip_error"):
+    for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
+               "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
+               "zpp_status_string", "zpp_last_hip_error"):
         assert fn in names
 
 
@@ -104,6 +105,34 @@ def test_adam_validation(zpp):
                 dict(lr=float("nan")), dict(weight_decay=float("inf"))):
         assert adam(zpp, h=hp(zpp, **bad)) == zpp.ZPP_EINVAL, bad
     assert adam(zpp, n=(1 << 64) - 1) == zpp.ZPP_EINVAL
+
+
+F = 0x7F0050000000
+G = 0x7F0060000000
+H = 0x7F0070000000
+
+
+def fused(zpp, ptrs=(A, B, C, D, E, F, G, H), n=1024, block=256, h=None):
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_adam_step_refresh_quantize(*ptrs, n, block, ctypes.byref(h), None, None,
+                                                  None)
+
+
+def test_fused_validation(zpp):
+    assert fused(zpp, n=0) == zpp.ZPP_OK
+    assert fused(zpp, n=0, block=100) == zpp.ZPP_EINVAL
+    assert fused(zpp, h=hp(zpp, step=0)) == zpp.ZPP_EINVAL
+    for blk in (0, 32, 96, 8192):
+        assert fused(zpp, block=blk) == zpp.ZPP_EINVAL
+    assert fused(zpp, ptrs=(A, B, C, D, None, F, G, H)) == zpp.ZPP_EINVAL
+    assert fused(zpp, ptrs=(A, B, C, D, E, F, None, H)) == zpp.ZPP_EINVAL
+    assert fused(zpp, ptrs=(A, B, C, D, E, F, G, None)) == zpp.ZPP_EINVAL
+    assert fused(zpp, ptrs=(A, B, C, D, E + 1, F, G, H)) == zpp.ZPP_EALIGN
+    assert fused(zpp, ptrs=(A, B, C, D, E, F + 1, G, H)) == zpp.ZPP_EALIGN
+    assert fused(zpp, ptrs=(A, B, C, D, E, F, G, H + 2)) == zpp.ZPP_EALIGN
+    assert fused(zpp, ptrs=(A, B, C, D, E, E + 100, G, H)) == zpp.ZPP_EOVERLAP
+    assert fused(zpp, ptrs=(A, B, C, D, E, F, A + 8, H)) == zpp.ZPP_EOVERLAP
+    assert fused(zpp, ptrs=(A, B, C, D, E, F, G, G + 1020)) == zpp.ZPP_EOVERLAP
 
 
 def test_refresh_validation(zpp):

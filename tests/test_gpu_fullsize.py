@@ -164,3 +164,47 @@ def test_fullsize_pipeline_properties(zpp):
     assert not bool(((pipe.out & 0x7FFF) > 0x7F80).any())
     del pipe
     torch.cuda.empty_cache()
+
+
+def test_fullsize_fused_step_refresh_quantize(zpp):
+    """The fused kernel on the whole Llama-2-13B partition: sampled whole
+    quantization blocks (and the short last block) against the oracle's Adam
+    followed by its quantizer on its own primary."""
+    n, B = WL.n, WL.block
+    nb = (n + B - 1) // B
+    hp = f32hp(WL.adam)
+    p = synth.device_normal_f32(n, synth.WEIGHT_STD, WL.cfg_id, synth.KIND_MASTER)
+    g = synth.device_normal_f32(n, synth.GRAD_STD, WL.cfg_id, synth.KIND_GRAD, it=1)
+    m = torch.zeros(n, device="cuda")
+    v = torch.zeros(n, device="cuda")
+    prim = torch.empty(n, dtype=torch.int16, device="cuda")
+    sec = torch.empty(n, dtype=torch.int16, device="cuda")
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    scales = torch.empty(nb, dtype=torch.float32, device="cuda")
+    kb = block_sample(nb, NBLOCKS, 4)
+    elems = np.concatenate([(kb[:, None] * B + np.arange(B)[None, :]).ravel(),
+                            np.arange((nb - 1) * B, n)])
+    eidx = torch.from_numpy(elems).cuda()
+    ph, gh = host(p, eidx, np.float32), host(g, eidx, np.float32)
+    torch.cuda.synchronize()
+    zpp.adam_step_refresh_quantize(p, m, v, g, prim, sec, codes, scales, step=1, block=B, **hp)
+    torch.cuda.synchronize()
+    got = tuple(host(t, eidx, d) for t, d in ((p, np.float32), (m, np.float32), (v, np.float32),
+                                              (prim, np.uint16)))
+    z = np.zeros_like(ph)
+    rp, rm, rv, rb = oracle.adam_step(ph, z, z, gh, step=1, **hp)
+    assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "fused")
+    assert torch.equal(sec, prim)
+    gb = got[3]
+    gc = host(codes, eidx, np.int8)
+    full = kb.size * B
+    rc, rs = oracle.quantize_blockwise_i8(rb[:full], B)
+    same = (gb[:full].reshape(-1, B) == rb[:full].reshape(-1, B)).all(axis=1)
+    assert same.mean() > 0.99
+    assert_bits_equal(gc[:full].reshape(-1, B)[same], rc.reshape(-1, B)[same], "sampled codes")
+    gs = host(scales, torch.from_numpy(kb).cuda(), np.float32)
+    assert_bits_equal(gs[same], rs[same], "sampled scales")
+    tc, ts = oracle.quantize_blockwise_i8(rb[full:], B)
+    if np.array_equal(gb[full:], rb[full:]):
+        assert_bits_equal(gc[full:], tc, "tail codes")
+        assert_bits_equal(scales[nb - 1:].cpu().numpy(), ts, "tail scale")

@@ -353,3 +353,98 @@ def test_gather_empty_layer_records_event(zpp):
     zpp.dequant_gather_layer([c], [sc], 256, 0, out, done_after=ev)
     ev.synchronize()
     assert ev.query()
+
+
+# ===========================================================================
+# Fused step + refresh + quantize
+# ===========================================================================
+def run_fused_gpu(zpp, p, m, v, g, hp, step, block, secondary=True, pad=0):
+    tp, tm, tv, tg = (to_dev(x, pad=pad) for x in (p, m, v, g))
+    n = p.size
+    prim = empty_dev(n, np.uint16, pad=pad, fill=0x5555)
+    sec = empty_dev(n, np.uint16, pad=pad, fill=0x7FC0) if secondary else None
+    codes = empty_dev(n, np.int8, pad=pad, fill=99)
+    scales = empty_dev((n + block - 1) // block, np.float32, fill=-1.0)
+    zpp.adam_step_refresh_quantize(tp, tm, tv, tg, prim, sec, codes, scales, step=step,
+                                   block=block, **hp)
+    torch.cuda.synchronize()
+    return (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
+            to_host(prim, np.uint16), to_host(sec, np.uint16) if secondary else None,
+            to_host(codes, np.int8), to_host(scales, np.float32))
+
+
+def assert_fused_matches_oracle(got, p, m, v, g, hp, step, block, what):
+    gp, gm, gv, gb, gs, gc, gsc = got
+    rp, rm, rv, rb = oracle.adam_step(p, m, v, g, step=step, **hp)
+    assert_adam_close((gp, gm, gv, gb), (rp, rm, rv, rb), hp["lr"], what, prev=(p, m, v), g=g,
+                      hp=hp)
+    if gs is not None:
+        assert_bits_equal(gs, gb, what + " secondary = primary")
+    rc, rs = oracle.quantize_blockwise_i8(rb, block)
+    n = p.size
+    nb = (n + block - 1) // block
+    same = np.array([np.array_equal(gb[k * block:(k + 1) * block], rb[k * block:(k + 1) * block])
+                     for k in range(nb)])
+    assert same.mean() > 0.95, what
+    for k in np.nonzero(same)[0]:
+        assert_bits_equal(gc[k * block:(k + 1) * block], rc[k * block:(k + 1) * block],
+                          "%s codes block %d" % (what, k))
+    assert_bits_equal(gsc[same], rs[same], what + " scales")
+
+
+@pytest.mark.parametrize("block", [64, 128, 256, 512, 4096])
+@pytest.mark.parametrize("n", [1, 255, 256, 4099, 256 * 40 + 80, 65536 + 64 + 3])
+def test_fused_vs_oracle(zpp, block, n):
+    hp = f32hp(HP_TINY)
+    p = synth.master_weights(n, 70, n)
+    g = synth.gradients(n, 70, n)
+    m, v = synth.moments(n, 70, n)
+    got = run_fused_gpu(zpp, p, m, v, g, hp, 2, block)
+    assert_fused_matches_oracle(got, p, m, v, g, hp, 2, block, "n=%d block=%d" % (n, block))
+
+
+@pytest.mark.parametrize("secondary", [True, False], ids=["with-secondary", "no-secondary"])
+@pytest.mark.parametrize("pad", [0, 1], ids=["fused", "scalar"])
+def test_fused_equals_separate_calls(zpp, secondary, pad):
+    """The fused entry gives, bit for bit, what the three separate calls give
+    on the same inputs (both on the GPU), on both of its paths."""
+    hp = f32hp(HP_LOUD)
+    n, block = 256 * 300 + 17, 256
+    p = synth.master_weights(n, 71)
+    g = synth.gradients(n, 71)
+    m, v = synth.moments(n, 71)
+    got = run_fused_gpu(zpp, p, m, v, g, hp, 5, block, secondary=secondary, pad=pad)
+    tp, tm, tv, tg = (to_dev(x) for x in (p, m, v, g))
+    prim = empty_dev(n, np.uint16)
+    sec = empty_dev(n, np.uint16)
+    codes = empty_dev(n, np.int8)
+    scales = empty_dev((n + block - 1) // block, np.float32)
+    zpp.adam_partition_step(tp, tm, tv, tg, prim, step=5, **hp)
+    zpp.refresh_secondary(sec, prim)
+    zpp.quantize_blockwise_i8(sec, codes, scales, block=block)
+    torch.cuda.synchronize()
+    sep = (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
+           to_host(prim, np.uint16), to_host(sec, np.uint16), to_host(codes, np.int8),
+           to_host(scales, np.float32))
+    for i, (a, b) in enumerate(zip(got, sep)):
+        if a is not None:
+            assert_bits_equal(a, b, "output %d" % i)
+    assert_fused_matches_oracle(got, p, m, v, g, hp, 5, block, "fused")
+
+
+def test_fused_special_values(zpp):
+    """Non-finite gradients make a NaN weight; its block gets a NaN scale and
+    zero codes, as the quantizer does for a NaN secondary."""
+    hp = f32hp(HP_TINY)
+    n, block = 256 * 8, 256
+    p = synth.master_weights(n, 72)
+    g = synth.gradients(n, 72)
+    g[3 * 256 + 5] = np.nan
+    g[6 * 256] = np.inf
+    p[5 * 256:6 * 256] = 0.0
+    g[5 * 256:6 * 256] = 0.0
+    z = np.zeros(n, np.float32)
+    got = run_fused_gpu(zpp, p, z, z, g, hp, 1, block)
+    assert_fused_matches_oracle(got, p, z, z, g, hp, 1, block, "special")
+    sc = got[6]
+    assert np.isnan(sc[3]) and np.isnan(sc[6]) and sc[5] == 0.0

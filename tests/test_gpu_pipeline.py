@@ -237,3 +237,37 @@ def test_iterations_with_buffer_reuse(zpp):
                              to_host(scales, np.float32), rc, rs, B, "last iteration")
     last = to_host(snaps[-1], np.uint16)[:s].reshape(-1, B)
     assert_bits_equal(last[same], r_out[:s].reshape(-1, B)[same], "last gathered layer")
+
+
+def test_pipeline_modes_agree(zpp):
+    """Separate kernels or the fused one, ordered by a device event or by a
+    host wait: from the same inputs, three iterations end in bit-identical
+    state, codes and gathered layer."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small", cfg_id=9, n=1 << 20, layer_elems=8 * (1 << 17) - 1000,
+                  secondary_world=8, world=8)
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    g0 = synth.gradients(wl.n, wl.cfg_id)
+    peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
+                                          wl.block) for j in range(wl.secondary_world - 1)]
+    results = {}
+    for fused in (False, True):
+        for sync in ("event", "host"):
+            pipe = PartitionPipeline(wl, fused=fused, sync=sync)
+            pipe.load(p0, g0, [q[0] for q in peers], [q[1] for q in peers])
+            for _ in range(3):
+                pipe.step()
+            pipe.wait()
+            results[(fused, sync)] = [t.cpu().numpy().copy() for t in
+                                      (pipe.master, pipe.exp_avg, pipe.exp_avg_sq, pipe.primary,
+                                       pipe.secondary, pipe.codes, pipe.scales, pipe.out)]
+    ref = results[(False, "event")]
+    for key, res in results.items():
+        for i, (a, b) in enumerate(zip(res, ref)):
+            assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "%s output %d" % (key, i))
+    # the peers' part of the gathered layer against the oracle
+    s, B = wl.shard_elems, wl.block
+    expect = oracle.dequant_gather_layer([q[0] for q in peers], [q[1] for q in peers], s, B,
+                                         wl.layer_elems - s)
+    assert_bits_equal(ref[7].view(np.uint16)[s:], expect, "peer shards")
