@@ -53,6 +53,9 @@ class Oracle:
         lib.orc_quantize_blockwise_i8.argtypes = [P, sz, u32, P, P]
         lib.orc_dequant_blockwise_i8.argtypes = [P, P, sz, u32, P]
         lib.orc_dequant_gather_layer.argtypes = [P, P, u32, sz, u32, sz, P]
+        lib.orc_quantize_blockwise_i4.argtypes = [P, sz, u32, P, P]
+        lib.orc_unpack_i4.argtypes = [P, sz, P]
+        lib.orc_dequant_reduce_i4.argtypes = [P, P, u32, sz, u32, f32, P]
         self.lib = lib
         self.path = lib_path
 
@@ -137,6 +140,41 @@ class Oracle:
         return out
 
 
+    # -- qgZ: int4 gradient quantization and the dequantize-and-reduce ------
+    def quantize_blockwise_i4(self, x_f32, block=256):
+        """fp32 values -> (packed int4 codes uint8[ceil(n/2)], scales)."""
+        x = _req(x_f32, np.float32)
+        codes = np.empty((x.size + 1) // 2, np.uint8)
+        scales = np.empty(num_blocks(x.size, block), np.float32)
+        self.lib.orc_quantize_blockwise_i4(_ptr(x), x.size, block, _ptr(codes), _ptr(scales))
+        return codes, scales
+
+    def unpack_i4(self, codes, n):
+        codes = _req(codes, np.uint8)
+        if codes.size < (n + 1) // 2:
+            raise ValueError("too few packed codes")
+        out = np.empty(n, np.int8)
+        self.lib.orc_unpack_i4(_ptr(codes), n, _ptr(out))
+        return out
+
+    def dequant_reduce_i4(self, src_codes, src_scales, n, block, scale_out):
+        """Sum over the sources, in order, of the dequantized partition, then
+        times scale_out."""
+        k = len(src_codes)
+        if k != len(src_scales) or k == 0:
+            raise ValueError("need one scales array per codes array")
+        codes = [_req(c, np.uint8) for c in src_codes]
+        scales = [_req(s, np.float32) for s in src_scales]
+        for c, s in zip(codes, scales):
+            if c.size < (n + 1) // 2 or s.size < num_blocks(n, block):
+                raise ValueError("source buffer too small")
+        cptrs = (ctypes.c_void_p * k)(*[c.ctypes.data for c in codes])
+        sptrs = (ctypes.c_void_p * k)(*[s.ctypes.data for s in scales])
+        out = np.empty(n, np.float32)
+        self.lib.orc_dequant_reduce_i4(cptrs, sptrs, k, n, block, scale_out, _ptr(out))
+        return out
+
+
 _default = None
 
 
@@ -177,6 +215,18 @@ def dequant_blockwise_i8(codes, scales, block=256):
 def dequant_gather_layer(shard_codes, shard_scales, shard_elems, block, layer_elems):
     return default().dequant_gather_layer(shard_codes, shard_scales, shard_elems, block,
                                           layer_elems)
+
+
+def quantize_blockwise_i4(x_f32, block=256):
+    return default().quantize_blockwise_i4(x_f32, block)
+
+
+def unpack_i4(codes, n):
+    return default().unpack_i4(codes, n)
+
+
+def dequant_reduce_i4(src_codes, src_scales, n, block, scale_out):
+    return default().dequant_reduce_i4(src_codes, src_scales, n, block, scale_out)
 
 
 # --------------------------------------------------------------------------

@@ -223,3 +223,100 @@ void orc_dequant_gather_layer(const int8_t *const *shard_codes, const float *con
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* qgZ: gradients are quantized before the exchange that replaces the      */
+/* ReduceScatter (Background section; Algorithm 1, backward loop, where an */
+/* INT4 all-to-all takes the ReduceScatter's place).  The paper gives no   */
+/* format; this build uses symmetric absmax int4 over blocks of `block`    */
+/* consecutive binary32 gradient values of one destination partition, one */
+/* binary32 scale per block, codes in [-7, 7], all decisions in binary32:  */
+/*   block holds a non-finite value -> scale = NaN (0x7FC00000), codes 0;  */
+/*   absmax a == 0                  -> scale = 0, codes 0;                 */
+/*   otherwise scale = RN(a / 7), inv = RN(7 / a), code = rint(x * inv)    */
+/*   (ties to even), clamped to [-7, 7]; when a < 2^-100 both x and a are  */
+/*   first multiplied by 2^64 (exact).                                     */
+/* Codes are packed two per byte, element 2i in the low nibble and 2i+1 in */
+/* the high nibble, as 4-bit two's complement; an odd tail leaves the last */
+/* high nibble 0.                                                          */
+/* ------------------------------------------------------------------------ */
+void orc_quantize_blockwise_i4(const float *x, size_t n, uint32_t block, uint8_t *codes,
+                               float *scales)
+{
+    if (block == 0)
+        return;
+    for (size_t b = 0; b < (n + 1) / 2; b++)
+        codes[b] = 0;
+    const size_t nblocks = (n + block - 1) / block;
+    for (size_t k = 0; k < nblocks; k++) {
+        const size_t lo = k * (size_t)block;
+        const size_t hi = (lo + block < n) ? lo + block : n;
+        int nonfinite = 0;
+        float a = 0.0f;
+        for (size_t i = lo; i < hi; i++) {
+            if (!isfinite(x[i]))
+                nonfinite = 1;
+            else if (fabsf(x[i]) > a)
+                a = fabsf(x[i]);
+        }
+        if (nonfinite) {
+            float qnan;
+            memcpy(&qnan, &ORC_SCALE_NAN_BITS, sizeof qnan);
+            scales[k] = qnan;
+            continue; /* codes stay 0 */
+        }
+        if (a == 0.0f) {
+            scales[k] = 0.0f;
+            continue;
+        }
+        scales[k] = a / 7.0f;
+        float pre = 1.0f;
+        if (a < 0x1p-100f)
+            pre = 0x1p64f;
+        const float inv = 7.0f / (a * pre);
+        for (size_t i = lo; i < hi; i++) {
+            float q = rintf((x[i] * pre) * inv);
+            if (q > 7.0f)
+                q = 7.0f;
+            if (q < -7.0f)
+                q = -7.0f;
+            const uint8_t nib = (uint8_t)((int)q & 0xF);
+            if (i % 2 == 0)
+                codes[i / 2] |= nib;
+            else
+                codes[i / 2] |= (uint8_t)(nib << 4);
+        }
+    }
+}
+
+/* The signed value of 4-bit code i of a packed array. */
+static int orc_i4_code(const uint8_t *codes, size_t i)
+{
+    const int nib = (i % 2 == 0) ? (codes[i / 2] & 0xF) : (codes[i / 2] >> 4);
+    return nib >= 8 ? nib - 16 : nib;
+}
+
+void orc_unpack_i4(const uint8_t *codes, size_t n, int8_t *out)
+{
+    for (size_t i = 0; i < n; i++)
+        out[i] = (int8_t)orc_i4_code(codes, i);
+}
+
+/* The receiving side of the qgZ exchange for one destination partition:
+ * num_src quantized copies of the same n-element partition (one from each
+ * sending rank, in rank order) are dequantized and summed,
+ *     acc = 0;  acc = fma(code_q[i], scale_q[i / block], acc) for q = 0..num_src-1
+ *     out[i] = acc * scale_out
+ * each fma a single rounding, the final product one more; scale_out is 1
+ * for a sum or 1/P for the data-parallel mean. */
+void orc_dequant_reduce_i4(const uint8_t *const *src_codes, const float *const *src_scales,
+                           uint32_t num_src, size_t n, uint32_t block, float scale_out,
+                           float *out)
+{
+    for (size_t i = 0; i < n; i++) {
+        float acc = 0.0f;
+        for (uint32_t q = 0; q < num_src; q++)
+            acc = fmaf((float)orc_i4_code(src_codes[q], i), src_scales[q][i / block], acc);
+        out[i] = acc * scale_out;
+    }
+}

@@ -24,6 +24,9 @@ QUANT = [pins.check_quant_integer_blocks, pins.check_quant_ties_to_even,
 GATHER = [pins.check_dequant_vs_library, pins.check_gather_markers,
           pins.check_gather_is_concatenation, pins.check_round_trip]
 
+I4 = [pins.check_i4_packing, pins.check_i4_integer_blocks, pins.check_i4_ties_and_specials,
+      pins.check_i4_nearest_code, pins.check_i4_dequant_reduce]
+
 # (name, text in the committed source, planted replacement, checks that must catch it)
 MUTANTS = [
     ("bf16-truncates", "        round_up = 1;\n    else if", "        round_up = 0;\n    else if", BF16),
@@ -53,6 +56,15 @@ MUTANTS = [
     ("gather-block-index", "shard_scales[j][i / block]", "shard_scales[j][i / block / 2]", GATHER),
     ("gather-reversed-shards", "(size_t)j * shard_elems + i", "(size_t)(num_shards - 1 - j) * shard_elems + i",
      GATHER),
+    ("i4-nibbles-swapped", "codes[i / 2] |= nib;\n            else", "codes[i / 2] |= (uint8_t)(nib << 4);\n            else", I4),
+    ("i4-floor", "float q = rintf((x[i] * pre) * inv);", "float q = floorf((x[i] * pre) * inv);", I4),
+    ("i4-scale-8", "scales[k] = a / 7.0f;", "scales[k] = a / 8.0f;", I4),
+    ("i4-sign-lost", "return nib >= 8 ? nib - 16 : nib;", "return nib;", I4),
+    ("i4-mul-then-add", "acc = fmaf((float)orc_i4_code(src_codes[q], i), src_scales[q][i / block], acc);",
+     "acc = (float)orc_i4_code(src_codes[q], i) * src_scales[q][i / block] + acc;", I4),
+    ("i4-no-output-scale", "out[i] = acc * scale_out;", "out[i] = acc;", I4),
+    ("i4-nonfinite-ignored", "if (!isfinite(x[i]))\n                nonfinite = 1;",
+     "if (!isfinite(x[i]))\n                nonfinite = 0;", I4),
     ("refresh-drops-last", "for (size_t i = 0; i < count; i++)", "for (size_t i = 0; i + 1 < count; i++)",
      [pins.check_refresh]),
 ]
@@ -86,6 +98,6 @@ def test_pins_catch_mutant(mutant, tmp_path):
 def test_unmutated_build_passes_all_checks(tmp_path):
     lib = obuild.build_oracle(out=str(tmp_path / "lib_clean.so"))
     orc = oracle.Oracle(lib)
-    for check in sorted(set(BF16 + ADAM + QUANT + GATHER), key=lambda c: c.__name__):
+    for check in sorted(set(BF16 + ADAM + QUANT + GATHER + I4), key=lambda c: c.__name__):
         check(orc)
     assert os.path.exists(lib)

@@ -544,3 +544,140 @@ def test_partition_sizes_golden(row):
         assert (b, e - b) == (size, size)
         assert size % block == extra
         assert oracle.num_blocks(size, block) == blocks
+
+
+# ===========================================================================
+# qgZ: int4 gradient quantization and the dequantize-and-reduce
+# ===========================================================================
+def check_i4_packing(orc):
+    """Hand-worked bytes: codes (1, -1) -> 0xF1, (7, -7) -> 0x97, (0, 2) ->
+    0x20, (2, -2) -> 0xE2 (element 2i in the low nibble, two's complement);
+    an odd tail leaves the high nibble 0."""
+    x = np.array([1, -1, 7, -7, 0.5, 1.5, 2.5, -2.5, 3.0], np.float32)
+    codes, scales = orc.quantize_blockwise_i4(x, 64)
+    assert scales.tolist() == [1.0]
+    assert codes.tolist() == [0xF1, 0x97, 0x20, 0xE2, 0x03]
+    assert orc.unpack_i4(codes, 9).tolist() == [1, -1, 7, -7, 0, 2, 2, -2, 3]
+
+
+def test_i4_packing_by_hand():
+    check_i4_packing(oracle.default())
+
+
+def i4_block(rng, block):
+    q = rng.integers(-7, 8, size=block).astype(np.int8)
+    q[rng.integers(0, block)] = rng.choice([-7, 7])
+    return q
+
+
+def check_i4_integer_blocks(orc):
+    rng = np.random.default_rng(15)
+    for block in (64, 256, 1024):
+        exps = list(range(-149, 121, 9)) + [-126, -101, -100, 0, 120]
+        q = np.concatenate([i4_block(rng, block) for _ in exps])
+        x = np.concatenate([q[i * block:(i + 1) * block].astype(np.float64) * 2.0 ** e
+                            for i, e in enumerate(exps)]).astype(np.float32)
+        codes, scales = orc.quantize_blockwise_i4(x, block)
+        assert np.array_equal(orc.unpack_i4(codes, x.size), q), block
+        assert np.array_equal(scales, np.array([2.0 ** e for e in exps], np.float32)), block
+
+
+def test_i4_integer_blocks():
+    check_i4_integer_blocks(oracle.default())
+
+
+def check_i4_ties_and_specials(orc):
+    vals = [7.0, 0.5, 1.5, 2.5, 3.5, -0.5, -1.5, 6.5, -6.5]
+    x = np.zeros(64 * 5 + 3, np.float32)
+    x[:len(vals)] = vals
+    x[64:128] = 0.0                       # zero block
+    x[128:192] = np.linspace(-1, 1, 64)
+    x[130] = np.inf                       # non-finite block
+    x[192:256] = np.linspace(-3, 3, 64)
+    x[200] = np.nan
+    x[256:320] = np.linspace(-0.5, 0.25, 64)
+    x[320:] = [1e-3, -4e-3, 2e-3]         # short tail block
+    codes, scales = orc.quantize_blockwise_i4(x, 64)
+    c = orc.unpack_i4(codes, x.size)
+    assert c[:len(vals)].tolist() == [7, 0, 2, 2, 4, 0, -2, 6, -6]
+    assert scales[1] == 0.0 and not c[64:128].any()
+    assert scales.view(np.uint32)[2] == 0x7FC00000 and not c[128:192].any()
+    assert scales.view(np.uint32)[3] == 0x7FC00000 and not c[192:256].any()
+    assert scales[5] == np.float32(4e-3) / np.float32(7) and c[320:].tolist() == [2, -7, 4]
+    n2 = orc.quantize_blockwise_i4(-x, 64)
+    assert np.array_equal(orc.unpack_i4(n2[0], x.size), -c)
+
+
+def test_i4_ties_and_specials():
+    check_i4_ties_and_specials(oracle.default())
+
+
+def check_i4_nearest_code(orc):
+    rng = np.random.default_rng(16)
+    block = 64
+    x = (rng.standard_normal(block * 30) * 1e-3).astype(np.float32)
+    codes, scales = orc.quantize_blockwise_i4(x, block)
+    c = orc.unpack_i4(codes, x.size).astype(int)
+    slack = Fraction(1, 1 << 15)
+    for k in range(30):
+        blk = x[k * block:(k + 1) * block]
+        a = np.abs(blk).max()
+        sc = exact(scales[k])
+        qx = exact(a) / 7
+        up = exact(np.nextafter(scales[k], np.float32(np.inf)))
+        dn = exact(np.nextafter(scales[k], np.float32(0)))
+        assert abs(sc - qx) <= abs(up - qx) and abs(sc - qx) <= abs(dn - qx)
+        cb = c[k * block:(k + 1) * block]
+        assert np.abs(cb[np.abs(blk) == a]).min() == 7
+        for xi, ci in zip(blk, cb):
+            assert abs(exact(xi) - ci * sc) <= sc * (Fraction(1, 2) + slack)
+            for other in (ci - 1, ci + 1):
+                if -7 <= other <= 7:
+                    assert abs(exact(xi) - other * sc) >= sc * (Fraction(1, 2) - slack)
+
+
+def test_i4_nearest_code_exact():
+    check_i4_nearest_code(oracle.default())
+
+
+def f32_round_exact(r):
+    """The binary32 value nearest the rational r (ties to even), by exact
+    comparison with the neighbours of a candidate."""
+    cand = np.float32(float(r))
+    best = None
+    for c in (np.nextafter(cand, np.float32(-np.inf)), cand, np.nextafter(cand, np.float32(np.inf))):
+        d = abs(exact(c) - r)
+        if best is None or d < best[0] or (d == best[0] and (c.view(np.uint32) & 1) == 0):
+            best = (d, c)
+    return best[1]
+
+
+def check_i4_dequant_reduce(orc):
+    rng = np.random.default_rng(17)
+    n, block, P = 64 * 12 + 5, 64, 4
+    srcs = [(rng.standard_normal(n) * 10.0 ** rng.uniform(-5, -2, n)).astype(np.float32)
+            for _ in range(P)]
+    q = [orc.quantize_blockwise_i4(s, block) for s in srcs]
+    codes = [orc.unpack_i4(c, n).astype(int) for c, _ in q]
+    # brute force in exact rationals: acc = RN(code * s + acc) per source, then RN(acc * f)
+    f = np.float32(0.25)
+    out = orc.dequant_reduce_i4([c for c, _ in q], [s for _, s in q], n, block, float(f))
+    for i in range(0, n, 7):
+        acc = np.float32(0.0)
+        for j in range(P):
+            acc = f32_round_exact(codes[j][i] * exact(q[j][1][i // block]) + exact(acc))
+        want = f32_round_exact(exact(acc) * exact(f))
+        assert out[i].view(np.uint32) == want.view(np.uint32), i
+    # one source, unit output scale: the dequantized partition (a float32 product)
+    one = orc.dequant_reduce_i4([q[0][0]], [q[0][1]], n, block, 1.0)
+    prod = codes[0].astype(np.float32) * np.repeat(q[0][1], block)[:n]
+    assert np.array_equal(one.view(np.uint32), prod.view(np.uint32))
+    # integer sums are exact whatever the order: P copies of an integer block
+    ints = np.concatenate([i4_block(rng, block) for _ in range(4)]).astype(np.float32)
+    ci, si = orc.quantize_blockwise_i4(ints, block)
+    tot = orc.dequant_reduce_i4([ci] * 8, [si] * 8, ints.size, block, 0.125)
+    assert np.array_equal(tot, ints)
+
+
+def test_i4_dequant_reduce_brute_force():
+    check_i4_dequant_reduce(oracle.default())
