@@ -188,6 +188,48 @@ ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
                                     const hipEvent_t *wait_events, uint32_t num_wait,
                                     hipEvent_t done_after);
 
+/* qgZ, sending side: quantize a rank's fp32 gradient of one destination
+ * partition before the exchange that replaces the ReduceScatter (Background
+ * section: gradients are quantized before ReduceScatter; Algorithm 1,
+ * backward loop: an INT4 all-to-all takes its place).  Symmetric absmax int4
+ * over consecutive blocks of `block` values (the last block may be short),
+ * one fp32 scale per block, decisions in fp32:
+ *   block holds an Inf or NaN  -> scale = NaN (0x7FC00000), codes 0
+ *   a = max |x| == 0           -> scale = 0, codes 0
+ *   otherwise                  -> scale = a / 7, inv = 7 / a (correctly
+ *       rounded), code = rint(x * inv) (ties to even) in [-7, 7]; when
+ *       a < 2^-100, x and a are first multiplied by 2^64.
+ * Packing: two codes per byte, element 2i in the low nibble, 2i+1 in the high
+ * nibble, 4-bit two's complement; an odd n leaves the last high nibble 0.
+ * src: float[n].  codes: uint8_t[ceil(n/2)] out.  scales:
+ * float[ceil(n/block)] out.  block: a power of two in [64, 4096].
+ * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
+ * No two ranges may overlap (ZPP_EOVERLAP).  Alignment: src and scales 4
+ * bytes (ZPP_EALIGN); 16-byte src and 4-byte codes select the vector kernel. */
+ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_t block,
+                                             uint8_t *codes, float *scales, hipStream_t stream,
+                                             hipEvent_t wait_before, hipEvent_t done_after);
+
+/* qgZ, receiving side: the num_src quantized copies of this rank's n-element
+ * gradient partition (one from each sending rank, in rank order) are
+ * dequantized and reduced into the fp32 gradient the partition step reads:
+ *     acc = 0;  for q in 0..num_src-1: acc = fma(code_q[i], scale_q[i/block], acc)
+ *     out[i] = acc * scale_out          (1 for a sum, 1/P for the mean)
+ * each fma one rounding, the final product another; the order is fixed.
+ * src_codes, src_scales: HOST arrays of num_src DEVICE pointers
+ * (uint8_t[ceil(n/2)] and float[ceil(n/block)] each), read during the call
+ * only; num_src in [1, ZPP_MAX_SHARDS].  out: float[n].  scale_out finite.
+ * Order on `stream`: wait for every event of wait_events[0..num_wait) (the
+ * exchange that delivered the sources), reduce, record `done_after`.
+ * out must not overlap any source range (ZPP_EOVERLAP).  Alignment: out and
+ * scales 4 bytes (ZPP_EALIGN); 16-byte out and 4-byte codes select the vector
+ * kernel. */
+ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
+                                         const float *const *src_scales, uint32_t num_src,
+                                         size_t n, uint32_t block, float scale_out, float *out,
+                                         hipStream_t stream, const hipEvent_t *wait_events,
+                                         uint32_t num_wait, hipEvent_t done_after);
+
 /* Static, NUL-terminated description of a status code. */
 ZPP_API const char *zpp_status_string(zpp_status s);
 

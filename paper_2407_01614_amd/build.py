@@ -12,7 +12,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzpp.so")
 
-SOURCES = ["zpp_api.hip", "adam.hip", "refresh.hip", "quant.hip", "gather.hip", "fused.hip"]
+SOURCES = ["zpp_api.hip", "adam.hip", "refresh.hip", "quant.hip", "gather.hip", "fused.hip",
+           "qgz.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

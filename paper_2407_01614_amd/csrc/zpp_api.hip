@@ -267,6 +267,85 @@ ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
     return record(stream, done_after);
 }
 
+ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_t block,
+                                             uint8_t *codes, float *scales, hipStream_t stream,
+                                             hipEvent_t wait_before, hipEvent_t done_after) {
+    if (!valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    const size_t nblocks = (n + block - 1) / block;
+    const size_t nbytes = (n + 1) / 2;
+    if (n) {
+        if (!src || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(src, 4) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const void *ptrs[3] = {src, codes, scales};
+        const size_t bytes[3] = {4 * n, nbytes, 4 * nblocks};
+        if (any_overlap(ptrs, bytes, 3))
+            return ZPP_EOVERLAP;
+    }
+    zpp_status st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (n) {
+        const bool vec = aligned(src, 16) && aligned(codes, 4);
+        const hipError_t e = zpp::launch_quantize_i4(src, n, block, codes, scales, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
+                                         const float *const *src_scales, uint32_t num_src,
+                                         size_t n, uint32_t block, float scale_out, float *out,
+                                         hipStream_t stream, const hipEvent_t *wait_events,
+                                         uint32_t num_wait, hipEvent_t done_after) {
+    if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    if (!isfinite(scale_out))
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!src_codes || !src_scales)
+        return ZPP_EINVAL;
+    const size_t nblocks = (n + block - 1) / block;
+    const size_t nbytes = (n + 1) / 2;
+    bool vec = aligned(out, 16);
+    for (uint32_t q = 0; q < num_src; ++q) {
+        if (!src_codes[q] || !src_scales[q])
+            return ZPP_EINVAL;
+        if (!aligned(src_scales[q], 4))
+            return ZPP_EALIGN;
+        vec = vec && aligned(src_codes[q], 4);
+    }
+    if (n) {
+        if (!out)
+            return ZPP_EINVAL;
+        if (!aligned(out, 4))
+            return ZPP_EALIGN;
+        for (uint32_t q = 0; q < num_src; ++q)
+            if (overlaps(out, 4 * n, src_codes[q], nbytes) ||
+                overlaps(out, 4 * n, src_scales[q], 4 * nblocks))
+                return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        const zpp_status st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (n) {
+        const hipError_t e = zpp::launch_dequant_reduce_i4(src_codes, src_scales, num_src, n,
+                                                           block, scale_out, out, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
 ZPP_API const char *zpp_status_string(zpp_status s) {
     switch (s) {
     case ZPP_OK: return "ok";

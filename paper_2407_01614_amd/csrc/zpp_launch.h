@@ -46,4 +46,14 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
                          uint32_t block, size_t layer_elems, uint16_t *out, bool vector_path,
                          hipStream_t stream);
 
+// qgZ: int4 quantization of fp32 gradients, and the dequantize-and-reduce
+// of num_src quantized copies of one partition.
+hipError_t launch_quantize_i4(const float *src, size_t n, uint32_t block, uint8_t *codes,
+                              float *scales, bool vector_path, hipStream_t stream);
+
+hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
+                                    const float *const *src_scales, uint32_t num_src, size_t n,
+                                    uint32_t block, float scale_out, float *out,
+                                    bool vector_path, hipStream_t stream);
+
 }  // namespace zpp

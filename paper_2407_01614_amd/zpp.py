@@ -47,14 +47,19 @@ _lib.zpp_quantize_blockwise_i8.restype = ctypes.c_int
 _lib.zpp_quantize_blockwise_i8.argtypes = [_P, _sz, _u32, _P, _P, _P, _P, _P]
 _lib.zpp_dequant_gather_layer.restype = ctypes.c_int
 _lib.zpp_dequant_gather_layer.argtypes = [_P, _P, _u32, _sz, _u32, _sz, _P, _P, _P, _u32, _P]
+_lib.zpp_quantize_blockwise_i4.restype = ctypes.c_int
+_lib.zpp_quantize_blockwise_i4.argtypes = [_P, _sz, _u32, _P, _P, _P, _P, _P]
+_lib.zpp_dequant_reduce_i4.restype = ctypes.c_int
+_lib.zpp_dequant_reduce_i4.argtypes = [_P, _P, _u32, _sz, _u32, ctypes.c_float, _P, _P, _P, _u32,
+                                       _P]
 _lib.zpp_status_string.restype = ctypes.c_char_p
 _lib.zpp_status_string.argtypes = [ctypes.c_int]
 _lib.zpp_last_hip_error.restype = ctypes.c_int
 _lib.zpp_last_hip_error.argtypes = []
 
 EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
-           "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_status_string",
-           "zpp_last_hip_error")
+           "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
+           "zpp_dequant_reduce_i4", "zpp_status_string", "zpp_last_hip_error")
 
 
 class ZppError(RuntimeError):
@@ -183,6 +188,7 @@ def _dev(t, dtypes, name):
 _F32 = (torch.float32,)
 _BF16 = (torch.bfloat16, torch.int16, torch.uint16)
 _I8 = (torch.int8,)
+_U8 = (torch.uint8, torch.int8)
 
 
 # --------------------------------------------------------------------------
@@ -296,6 +302,46 @@ def dequant_gather_layer(shard_codes, shard_scales, shard_elems, layer_elems, ou
                                        out_bf16.data_ptr(), stream_handle(stream), warr,
                                        len(waits), _event_handle(done_after))
     _check(st, "zpp_dequant_gather_layer")
+
+
+def quantize_blockwise_i4(src, codes, scales, *, block=256, n=None, stream=None,
+                          wait_before=None, done_after=None):
+    """zpp_quantize_blockwise_i4 of the first ``n`` fp32 values of src."""
+    _dev(src, _F32, "src")
+    _dev(codes, _U8, "codes")
+    _dev(scales, _F32, "scales")
+    if n is None:
+        n = src.numel()
+    if src.numel() < n or codes.numel() < (n + 1) // 2 or scales.numel() < num_blocks(n, block):
+        raise ValueError("a buffer is too small for n = %d" % n)
+    st = _lib.zpp_quantize_blockwise_i4(src.data_ptr(), n, block, codes.data_ptr(),
+                                        scales.data_ptr(), stream_handle(stream),
+                                        _event_handle(wait_before), _event_handle(done_after))
+    _check(st, "zpp_quantize_blockwise_i4")
+
+
+def dequant_reduce_i4(src_codes, src_scales, n, out, *, block=256, scale_out=1.0, stream=None,
+                      wait_events=(), done_after=None):
+    """zpp_dequant_reduce_i4 over len(src_codes) sources into out[:n]."""
+    k = len(src_codes)
+    if k != len(src_scales) or not 1 <= k <= MAX_SHARDS:
+        raise ValueError("1..%d sources, one scales tensor each" % MAX_SHARDS)
+    for q in range(k):
+        _dev(src_codes[q], _U8, "src_codes[%d]" % q)
+        _dev(src_scales[q], _F32, "src_scales[%d]" % q)
+        if src_codes[q].numel() < (n + 1) // 2 or src_scales[q].numel() < num_blocks(n, block):
+            raise ValueError("source %d buffers too small" % q)
+    _dev(out, _F32, "out")
+    if out.numel() < n:
+        raise ValueError("out holds fewer than n elements")
+    cptrs = (_P * k)(*[c.data_ptr() for c in src_codes])
+    sptrs = (_P * k)(*[x.data_ptr() for x in src_scales])
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    st = _lib.zpp_dequant_reduce_i4(cptrs, sptrs, k, n, block, scale_out, out.data_ptr(),
+                                    stream_handle(stream), warr, len(waits),
+                                    _event_handle(done_after))
+    _check(st, "zpp_dequant_reduce_i4")
 
 
 # --------------------------------------------------------------------------

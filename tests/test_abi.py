@@ -35,7 +35,8 @@ def test_header_declares_the_four_calls():
     names = declared_functions()
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
                "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
-               "zpp_status_string", "zpp_last_hip_error"):
+               "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_status_string",
+               "zpp_last_hip_error"):
         assert fn in names
 
 
@@ -191,6 +192,43 @@ def test_gather_validation(zpp):
     assert gather(zpp, cs, ss, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
     # an empty layer is a valid no-op (no events given: no HIP call)
     assert gather(zpp, cs, ss, N=0, out=None) == zpp.ZPP_OK
+
+
+def test_quant_i4_validation(zpp):
+    q = zpp.raw.zpp_quantize_blockwise_i4
+    assert q(None, 0, 256, None, None, None, None, None) == zpp.ZPP_OK
+    for blk in (0, 2, 100, 8192):
+        assert q(A, 1024, blk, B, C, None, None, None) == zpp.ZPP_EINVAL
+    assert q(A, 1024, 256, None, C, None, None, None) == zpp.ZPP_EINVAL
+    assert q(A + 2, 1024, 256, B, C, None, None, None) == zpp.ZPP_EALIGN
+    assert q(A, 1024, 256, B, C + 1, None, None, None) == zpp.ZPP_EALIGN
+    assert q(A, 1024, 256, A + 4000, C, None, None, None) == zpp.ZPP_EOVERLAP
+    assert q(A, 1024, 256, B, B + 508, None, None, None) == zpp.ZPP_EOVERLAP
+
+
+def reduce_i4(zpp, codes, scales, n=1024, block=256, scale_out=1.0, out=E, waits=None, nwait=0):
+    P = ctypes.c_void_p
+    k = len(codes)
+    carr = (P * k)(*codes)
+    sarr = (P * k)(*scales)
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    return zpp.raw.zpp_dequant_reduce_i4(carr, sarr, k, n, block, scale_out, out, None, warr,
+                                         nwait, None)
+
+
+def test_dequant_reduce_i4_validation(zpp):
+    cs, ss = [A, B], [C, D]
+    assert reduce_i4(zpp, cs, ss, n=0, out=None) == zpp.ZPP_OK
+    assert reduce_i4(zpp, cs, ss, block=96) == zpp.ZPP_EINVAL
+    assert reduce_i4(zpp, cs, ss, scale_out=float("inf")) == zpp.ZPP_EINVAL
+    assert reduce_i4(zpp, [A, None], ss) == zpp.ZPP_EINVAL
+    assert reduce_i4(zpp, cs, [C, D + 1]) == zpp.ZPP_EALIGN
+    assert reduce_i4(zpp, cs, ss, out=E + 2) == zpp.ZPP_EALIGN
+    assert reduce_i4(zpp, cs, ss, out=None) == zpp.ZPP_EINVAL
+    assert reduce_i4(zpp, cs, ss, out=A - 100) == zpp.ZPP_EOVERLAP
+    assert reduce_i4(zpp, cs, ss, out=D + 8) == zpp.ZPP_EOVERLAP
+    assert reduce_i4(zpp, cs, ss, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
+    assert reduce_i4(zpp, [A] * 65, [C] * 65) == zpp.ZPP_EINVAL
 
 
 def test_no_oracle_in_product_path():
