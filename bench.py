@@ -81,6 +81,45 @@ def kernel_table(kb, times):
     return out
 
 
+def qgz_measure(pipe, wl, reps, num_src=8):
+    """The qgZ gradient side at this workload's partition: one sending rank's
+    int4 quantization of n fp32 gradient values, and the mean of `num_src`
+    int4 copies back into fp32 (the gradient the partition step reads); each
+    timed with events on its stream over `reps` launches."""
+    import torch
+    from paper_2407_01614_amd import zpp
+    from paper_2407_01614_amd.pipeline import GradientExchange
+    from paper_2407_01614_amd.workloads import bytes_quant_i4, bytes_reduce_i4
+    ex = GradientExchange(wl.n, num_src, wl.block)
+    stream = pipe.compute
+    for q in range(num_src):
+        ex.quantize(q, pipe.grad, stream=stream)
+    out = torch.empty(wl.n, dtype=torch.float32, device="cuda")
+    res = {}
+    for name, fn, nbytes in (
+            ("quant_i4", lambda: ex.quantize(0, pipe.grad, stream=stream),
+             bytes_quant_i4(wl.n, wl.block)),
+            ("dequant_reduce_i4", lambda: ex.reduce(out, stream=stream),
+             bytes_reduce_i4(wl.n, num_src, wl.block))):
+        fn()
+        evs = []
+        for _ in range(reps):
+            a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        ts = sorted(a.elapsed_ms(b) for a, b in evs)
+        mean = sum(ts) / len(ts)
+        gbps = nbytes / (mean * 1e-3) / 1e9
+        res[name] = {"bytes": nbytes, "mean_us": round(mean * 1e3, 2),
+                     "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    res["sources"] = num_src
+    del ex, out
+    return res
+
+
 def cpu_baseline(wl, frac):
     """Time the CPU oracle (as it stands, one thread) on a `frac` sample of the
     workload: Adam on frac*n, refresh and quantization of frac*n, gather of a
@@ -176,6 +215,7 @@ def main():
     sync_ab = {}
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False)[0], 4)
+    qgz = qgz_measure(pipe, wl, args.steps)
     step_bytes = sum(kb.values())
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = kernel_table(kb, times)
@@ -219,6 +259,7 @@ def main():
             "ms_per_step": round(fused_ms, 4), "GB/s": round(fused_gbps, 1),
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
         "sync_ab_ms_per_step": sync_ab,
+        "qgz_gradient_side": qgz,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }
     del pipe

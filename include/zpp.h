@@ -205,7 +205,7 @@ ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
  * float[ceil(n/block)] out.  block: a power of two in [64, 4096].
  * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
  * No two ranges may overlap (ZPP_EOVERLAP).  Alignment: src and scales 4
- * bytes (ZPP_EALIGN); 16-byte src and 4-byte codes select the vector kernel. */
+ * bytes (ZPP_EALIGN); 16-byte src and 2-byte codes select the vector kernel. */
 ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_t block,
                                              uint8_t *codes, float *scales, hipStream_t stream,
                                              hipEvent_t wait_before, hipEvent_t done_after);
@@ -222,7 +222,7 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_
  * Order on `stream`: wait for every event of wait_events[0..num_wait) (the
  * exchange that delivered the sources), reduce, record `done_after`.
  * out must not overlap any source range (ZPP_EOVERLAP).  Alignment: out and
- * scales 4 bytes (ZPP_EALIGN); 16-byte out and 4-byte codes select the vector
+ * scales 4 bytes (ZPP_EALIGN); 16-byte out and 2-byte codes select the vector
  * kernel. */
 ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
                                          const float *const *src_scales, uint32_t num_src,

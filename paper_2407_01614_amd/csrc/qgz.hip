@@ -4,23 +4,31 @@
 // rank, the dequantize-and-reduce of the P quantized copies of its partition
 // into the fp32 gradient the optimizer step consumes.
 //
-// Quantize: 4 B read, 0.5 B + 4/B B written per element.  A lane holds 8
-// consecutive values (two 16-byte loads); the absmax is an integer max of the
-// |x| bit patterns (bits >= 0x7F800000 mean Inf or NaN), reduced over the
-// B/8 lanes of a block with xor shuffles.  Codes come from the same
-// round-to-nearest-even trick as the int8 quantizer (the low bits of
-// x*inv + 1.5*2^23), and 8 codes are packed into one 32-bit store.
+// Quantize: 4 B read, 0.5 B + 4/B B written per element.  The absmax is an
+// integer max of the |x| bit patterns (bits >= 0x7F800000 mean Inf or NaN),
+// reduced over the lanes of a block with xor shuffles.  Codes come from the
+// same round-to-nearest-even trick as the int8 quantizer (the low bits of
+// x*inv + 1.5*2^23), packed four to a 16-bit store.
 //
 // Dequant-reduce: P * (0.5 B + 4/B B) read, 4 B written per element.  The
 // sources' pointers travel by value in the kernel arguments; a lane
-// accumulates 8 elements over the sources in order, one fma each, loading
-// four sources ahead.
+// accumulates its elements over the sources in order, one fma each.
+//
+// Both kernels keep every wave's loads and stores contiguous: on this GPU,
+// non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
+// lane at a 32- or 64-byte stride) run two to three times slower.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
 
 #ifndef ZPP_QGZ_THREADS
 #define ZPP_QGZ_THREADS 256
+#endif
+#ifndef ZPP_QGZ_QUANT_UNROLL
+#define ZPP_QGZ_QUANT_UNROLL 4
+#endif
+#ifndef ZPP_QGZ_REDUCE_GROUPS
+#define ZPP_QGZ_REDUCE_GROUPS 2
 #endif
 #ifndef ZPP_QGZ_MAX_GRID
 #define ZPP_QGZ_MAX_GRID (1u << 30)
@@ -55,23 +63,21 @@ __device__ __forceinline__ I4Quant i4_params(uint32_t absbits) {
     return q;
 }
 
-// 8 values -> 8 int4 codes packed little-endian in one word.  No clamp is
+// 4 values -> 4 int4 codes packed little-endian in 16 bits.  No clamp is
 // needed: |x * inv| rounds to at most 7 (1 + 2^-24)^2 < 7.5.
-__device__ __forceinline__ uint32_t i4_word(const f32x4 &lo, const f32x4 &hi, const I4Quant &q) {
+__device__ __forceinline__ uint32_t i4_half(const f32x4 &x, const I4Quant &q) {
 #pragma clang fp contract(off)
-    float x[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-    uint32_t b[8];
+    uint32_t b[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < 4; ++e) {
         const float xe = q.tiny ? x[e] * q.pre : x[e];
         b[e] = code_bits(xe * q.inv);
     }
-    // low bytes of each group of four, then their low nibbles side by side
-    const uint32_t w0 = pack_low_bytes(b[0], b[1], b[2], b[3]) & 0x0F0F0F0Fu;
-    const uint32_t w1 = pack_low_bytes(b[4], b[5], b[6], b[7]) & 0x0F0F0F0Fu;
-    const uint32_t t0 = w0 | (w0 >> 4);  // bytes 0 and 2 hold (c0|c1<<4), (c2|c3<<4)
-    const uint32_t t1 = w1 | (w1 >> 4);
-    const uint32_t packed = __builtin_amdgcn_perm(t1, t0, 0x06040200u);
+    // low bytes side by side, then low nibbles: bytes 0 and 2 of t hold
+    // (c0 | c1 << 4) and (c2 | c3 << 4)
+    const uint32_t w = pack_low_bytes(b[0], b[1], b[2], b[3]) & 0x0F0F0F0Fu;
+    const uint32_t t = w | (w >> 4);
+    const uint32_t packed = __builtin_amdgcn_perm(0u, t, 0x0c0c0200u);
     return q.zero ? 0u : packed;
 }
 
@@ -80,59 +86,70 @@ __device__ __forceinline__ uint32_t abs_bits_max4(const f32x4 &v) {
                max(__float_as_uint(v.z) & 0x7FFFFFFFu, __float_as_uint(v.w) & 0x7FFFFFFFu));
 }
 
-template <int B>
+// A lane holds groups of 4 consecutive values; group t of lane l in a wave's
+// tile starts at 256 t + 4 l, so every load instruction of a wave reads 1 KiB
+// and every code store writes 128 contiguous bytes.  A block of B values
+// spans L = min(B/4, 64) lanes and G = max(1, B/256) groups per lane; a
+// wave covers C = max(B, 256) values per tile and keeps U tiles in flight.
+template <int B, int U>
 __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(const float *__restrict__ src,
                                                                size_t n, uint8_t *__restrict__ codes,
                                                                float *__restrict__ scales) {
-    constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;  // lanes per block
-    constexpr int V = (B / 8 > kWave) ? B / (8 * kWave) : 1;
-    constexpr int kGroupsPerWave = kWave / L;
-    constexpr int kGroupsPerBlock = kGroupsPerWave * (kQgzThreads / kWave);
-    const size_t nblocks = (n + B - 1) / B;
+    constexpr int C = B > 256 ? B : 256;
+    constexpr int G = C / 256;
+    constexpr int L = B < 256 ? B / 4 : kWave;
+    constexpr int kWaves = kQgzThreads / kWave;
+    const size_t ntiles = (n + C - 1) / C;
     const size_t nbytes = (n + 1) / 2;
     const int lane = threadIdx.x & (kWave - 1);
-    const int gl = lane / L, li = lane % L;
     const int wave = threadIdx.x / kWave;
-    for (size_t g0 = (size_t)blockIdx.x * kGroupsPerBlock; g0 < nblocks;
-         g0 += (size_t)gridDim.x * kGroupsPerBlock) {
-        const size_t k = g0 + (size_t)wave * kGroupsPerWave + gl;
-        const bool valid = k < nblocks;
-        f32x4 x[V][2];
-        uint32_t mx = 0;
+    for (size_t t0 = ((size_t)blockIdx.x * kWaves + wave) * U; t0 < ntiles;
+         t0 += (size_t)gridDim.x * kWaves * U) {
+        f32x4 x[U][G];
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const size_t i = k * B + ((size_t)v * L + li) * 8;
-            if (valid && i + 8 <= n) {
-                x[v][0] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
-                x[v][1] = ld_nt(reinterpret_cast<const f32x4 *>(src + i + 4));
-            } else {
-                float h[8];
+        for (int u = 0; u < U; ++u) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    h[e] = (valid && i + e < n) ? src[i + e] : 0.0f;
-                x[v][0] = f32x4{h[0], h[1], h[2], h[3]};
-                x[v][1] = f32x4{h[4], h[5], h[6], h[7]};
-            }
-            mx = max(mx, max(abs_bits_max4(x[v][0]), abs_bits_max4(x[v][1])));
-        }
+            for (int g = 0; g < G; ++g) {
+                const size_t i = (t0 + u) * C + (size_t)g * 256 + (size_t)lane * 4;
+                if (t0 + u < ntiles && i + 4 <= n) {
+                    x[u][g] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
+                } else {
+                    float h[4];
 #pragma unroll
-        for (int off = L / 2; off >= 1; off >>= 1)
-            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-        const I4Quant q = i4_params(mx);
-#pragma unroll
-        for (int v = 0; v < V; ++v) {
-            const size_t i = k * B + ((size_t)v * L + li) * 8;
-            const uint32_t w = i4_word(x[v][0], x[v][1], q);
-            const size_t byte0 = i / 2;
-            if (valid && byte0 + 4 <= nbytes) {
-                st_nt(reinterpret_cast<uint32_t *>(codes + byte0), w);
-            } else if (valid) {
-                for (int e = 0; e < 4 && byte0 + e < nbytes; ++e)
-                    codes[byte0 + e] = (uint8_t)(w >> (8 * e));
+                    for (int e = 0; e < 4; ++e)
+                        h[e] = (t0 + u < ntiles && i + e < n) ? src[i + e] : 0.0f;
+                    x[u][g] = f32x4{h[0], h[1], h[2], h[3]};
+                }
             }
         }
-        if (valid && li == 0)
-            scales[k] = q.scale;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t tile = t0 + u;
+            uint32_t mx = 0;
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                mx = max(mx, abs_bits_max4(x[u][g]));
+#pragma unroll
+            for (int off = L / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+            const I4Quant q = i4_params(mx);
+            if (tile < ntiles) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const size_t i = tile * C + (size_t)g * 256 + (size_t)lane * 4;
+                    const uint32_t h = i4_half(x[u][g], q);
+                    const size_t byte0 = i / 2;
+                    if (byte0 + 2 <= nbytes) {
+                        st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
+                    } else if (byte0 < nbytes) {
+                        codes[byte0] = (uint8_t)h;
+                    }
+                }
+                const size_t k = (tile * C + (size_t)lane * 4) / B;
+                if (lane % L == 0 && k * B < n)
+                    scales[k] = q.scale;
+            }
+        }
     }
 }
 
@@ -159,8 +176,8 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(const floa
         for (size_t i = lo + 2 * lane; i < hi; i += 2 * kWave) {
             const float x0 = src[i];
             const float x1 = (i + 1 < hi) ? src[i + 1] : 0.0f;
-            const uint32_t w = i4_word(f32x4{x0, x1, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}, q);
-            codes[i / 2] = (uint8_t)(w & 0xFFu);
+            const uint32_t h = i4_half(f32x4{x0, x1, 0.0f, 0.0f}, q);
+            codes[i / 2] = (uint8_t)(h & 0xFFu);
         }
         if (lane == 0)
             scales[k] = q.scale;
@@ -181,53 +198,78 @@ __device__ __forceinline__ float i4_code(uint32_t w, int e) {
     return (float)((int32_t)(w << (28 - 4 * e)) >> 28);
 }
 
+// A lane holds G groups of 4 consecutive elements; group t of lane l in a
+// wave's tile starts at 256 t + 4 l, so each source is read as 128-byte
+// contiguous wave loads (2 bytes per lane) and every store of the wave
+// writes 1 KiB contiguously.  Sources are taken eight at a time, all their
+// loads in flight before the fma passes, which keep the order q = 0, 1, ...
+template <int G>
 __global__ __launch_bounds__(kQgzThreads) void reduce_i4_kernel(ReduceArgs a) {
-    const size_t chunks = (a.n + 7) / 8;
-    for (size_t c = (size_t)blockIdx.x * kQgzThreads + threadIdx.x; c < chunks;
-         c += (size_t)gridDim.x * kQgzThreads) {
-        const size_t i = c * 8;
-        const bool full = i + 8 <= a.n;
-        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        const size_t kb = i >> a.block_shift;
-        for (uint32_t q0 = 0; q0 < a.num_src; q0 += 4) {
-            uint32_t w[4];
-            float s[4];
+    constexpr int kBatch = 8;
+    constexpr int kWaves = kQgzThreads / kWave;
+    constexpr size_t C = 256 * G;
+    const size_t ntiles = (a.n + C - 1) / C;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    for (size_t tile = (size_t)blockIdx.x * kWaves + wave; tile < ntiles;
+         tile += (size_t)gridDim.x * kWaves) {
+        const size_t base = tile * C + (size_t)lane * 4;
+        const bool full = tile * C + C <= a.n;
+        float acc[G][4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc[g][e] = 0.0f;
+        for (uint32_t q0 = 0; q0 < a.num_src; q0 += kBatch) {
+            uint32_t w[kBatch][G];
+            float s[kBatch][G];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
                 const uint32_t q = q0 + j;
-                if (q < a.num_src) {
-                    if (full) {
-                        w[j] = ld_nt(reinterpret_cast<const uint32_t *>(a.codes[q] + i / 2));
-                    } else {
-                        w[j] = 0;
-                        for (size_t e = i; e < a.n; e += 2)
-                            w[j] |= (uint32_t)a.codes[q][e / 2] << (4 * (e - i));
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const size_t i = base + (size_t)g * 256;
+                    w[j][g] = 0;
+                    s[j][g] = 0.0f;
+                    if (q < a.num_src) {
+                        if (full) {
+                            w[j][g] = ld_nt(reinterpret_cast<const uint16_t *>(a.codes[q] + i / 2));
+                        } else {
+                            if (i < a.n)
+                                w[j][g] = a.codes[q][i / 2];
+                            if (i + 2 < a.n)
+                                w[j][g] |= (uint32_t)a.codes[q][i / 2 + 1] << 8;
+                        }
+                        if (i < a.n)
+                            s[j][g] = a.scales[q][i >> a.block_shift];
                     }
-                    s[j] = a.scales[q][kb];
-                } else {
-                    w[j] = 0;
-                    s[j] = 0.0f;
                 }
             }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < kBatch; ++j) {
                 if (q0 + j < a.num_src) {
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        acc[e] = __builtin_fmaf(i4_code(w[j], e), s[j], acc[e]);
+                    for (int g = 0; g < G; ++g)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            acc[g][e] = __builtin_fmaf(i4_code(w[j][g], e), s[j][g], acc[g][e]);
                 }
             }
         }
-        if (full) {
-            st_nt(reinterpret_cast<f32x4 *>(a.out + i),
-                  f32x4{acc[0] * a.scale_out, acc[1] * a.scale_out, acc[2] * a.scale_out,
-                        acc[3] * a.scale_out});
-            st_nt(reinterpret_cast<f32x4 *>(a.out + i + 4),
-                  f32x4{acc[4] * a.scale_out, acc[5] * a.scale_out, acc[6] * a.scale_out,
-                        acc[7] * a.scale_out});
-        } else {
-            for (size_t e = i; e < a.n; ++e)
-                a.out[e] = acc[e - i] * a.scale_out;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const size_t i = base + (size_t)g * 256;
+            if (full) {
+                st_nt(reinterpret_cast<f32x4 *>(a.out + i),
+                      f32x4{acc[g][0] * a.scale_out, acc[g][1] * a.scale_out,
+                            acc[g][2] * a.scale_out, acc[g][3] * a.scale_out});
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (i + e < a.n)
+                        a.out[i + e] = acc[g][e] * a.scale_out;
+            }
         }
     }
 }
@@ -249,13 +291,13 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_scalar_kernel(ReduceArg
 template <int B>
 void launch_quant_i4_b(const float *src, size_t n, uint8_t *codes, float *scales,
                        hipStream_t stream) {
-    constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;
-    constexpr size_t kGroupsPerBlock = (kWave / L) * (kQgzThreads / kWave);
-    const size_t nblocks = (n + B - 1) / B;
-    const size_t need = (nblocks + kGroupsPerBlock - 1) / kGroupsPerBlock;
+    constexpr size_t C = B > 256 ? B : 256;
+    constexpr size_t kTilesPerBlock = (kQgzThreads / kWave) * ZPP_QGZ_QUANT_UNROLL;
+    const size_t ntiles = (n + C - 1) / C;
+    const size_t need = (ntiles + kTilesPerBlock - 1) / kTilesPerBlock;
     const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
-    hipLaunchKernelGGL((quant_i4_kernel<B>), dim3(grid), dim3(kQgzThreads), 0, stream, src, n,
-                       codes, scales);
+    hipLaunchKernelGGL((quant_i4_kernel<B, ZPP_QGZ_QUANT_UNROLL>), dim3(grid), dim3(kQgzThreads),
+                       0, stream, src, n, codes, scales);
 }
 
 }  // namespace
@@ -298,10 +340,13 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
     a.scale_out = scale_out;
     a.out = out;
     if (vector_path) {
-        const size_t chunks = (n + 7) / 8;
-        const size_t need = (chunks + kQgzThreads - 1) / kQgzThreads;
+        constexpr size_t C = 256 * ZPP_QGZ_REDUCE_GROUPS;
+        const size_t ntiles = (n + C - 1) / C;
+        const size_t waves = kQgzThreads / kWave;
+        const size_t need = (ntiles + waves - 1) / waves;
         const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
-        hipLaunchKernelGGL(reduce_i4_kernel, dim3(grid), dim3(kQgzThreads), 0, stream, a);
+        hipLaunchKernelGGL((reduce_i4_kernel<ZPP_QGZ_REDUCE_GROUPS>), dim3(grid),
+                           dim3(kQgzThreads), 0, stream, a);
     } else {
         const size_t need = (n + kQgzThreads - 1) / kQgzThreads;
         const unsigned grid = (unsigned)(need < (1u << 20) ? need : (1u << 20));

@@ -288,7 +288,7 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_
     if (st != ZPP_OK)
         return st;
     if (n) {
-        const bool vec = aligned(src, 16) && aligned(codes, 4);
+        const bool vec = aligned(src, 16) && aligned(codes, 2);
         const hipError_t e = zpp::launch_quantize_i4(src, n, block, codes, scales, vec, stream);
         if (e != hipSuccess)
             return hip_fail(e);
@@ -320,7 +320,7 @@ ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
             return ZPP_EINVAL;
         if (!aligned(src_scales[q], 4))
             return ZPP_EALIGN;
-        vec = vec && aligned(src_codes[q], 4);
+        vec = vec && aligned(src_codes[q], 2);
     }
     if (n) {
         if (!out)

@@ -186,3 +186,28 @@ class PartitionPipeline:
     def kernel_times_ms(self):
         """Per-kernel list of event-measured durations (ms); call after wait()."""
         return {k: [a.elapsed_ms(b) for a, b in v] for k, v in self.timing.items()}
+
+
+class GradientExchange:
+    """The qgZ gradient side of one rank's partition, on one GPU: each of the
+    `num_src` sending ranks quantizes its gradient of this rank's partition to
+    int4 (sources other than this rank are simulated in this GPU's memory),
+    and the rank reduces the copies into the fp32 mean gradient that the
+    partition step reads."""
+
+    def __init__(self, n, num_src, block=256, device="cuda"):
+        self.n, self.num_src, self.block = n, num_src, block
+        nb = (n + block - 1) // block
+        self.codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device=device)
+                      for _ in range(num_src)]
+        self.scales = [torch.empty(nb, dtype=torch.float32, device=device)
+                       for _ in range(num_src)]
+
+    def quantize(self, q, grad, stream=None, done_after=None):
+        zpp.quantize_blockwise_i4(grad, self.codes[q], self.scales[q], block=self.block,
+                                  n=self.n, stream=stream, done_after=done_after)
+
+    def reduce(self, out, stream=None, wait_events=(), done_after=None):
+        zpp.dequant_reduce_i4(self.codes, self.scales, self.n, out, block=self.block,
+                              scale_out=1.0 / self.num_src, stream=stream,
+                              wait_events=wait_events, done_after=done_after)

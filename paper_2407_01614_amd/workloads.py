@@ -114,3 +114,13 @@ def bytes_fused(n, block=BLOCK):
     # Adam's 30 B, the secondary copy written (2 B), the codes and scales
     # written (1 B + 4 B per block); the primary is not read back
     return 32 * n + n + 4 * ((n + block - 1) // block)
+
+
+def bytes_quant_i4(n, block=BLOCK):
+    # read fp32 (4 B), write packed int4 (0.5 B) and one fp32 scale per block
+    return 4 * n + (n + 1) // 2 + 4 * ((n + block - 1) // block)
+
+
+def bytes_reduce_i4(n, num_src, block=BLOCK):
+    # read every source's packed codes and scales, write the fp32 result
+    return num_src * ((n + 1) // 2 + 4 * ((n + block - 1) // block)) + 4 * n
