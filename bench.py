@@ -224,7 +224,8 @@ def main():
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
     sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
 
-    traffic = measured_traffic(args.traffic, wl.name, "adam", ["adam.hip", "zpp_device.h"])
+    traffic = measured_traffic(args.traffic, wl.name, "adam",
+                               ["adam.hip", "zpp_adam.h", "zpp_device.h"])
 
     adam_mean_s = kernels["adam"]["mean_us"] * 1e-6
     achieved = kb["adam"] / adam_mean_s / 1e9
