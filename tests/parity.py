@@ -5,12 +5,13 @@ Tolerances:
   * refresh, int8 codes, fp32 scales, gathered bf16: bit for bit (one correct
     result exists for identical inputs);
   * Adam fp32 master / moments: max relative error 1e-5, with the relative
-    error of element i taken as |a - r| / max(|r|, tau): tau = lr for the
-    master weights (a weight that lands within one update of zero after the
-    decay and the update cancel has no meaningful relative error); for the
-    first moment tau is the size of the two terms the update sums (see
-    assert_adam_close); for the second moment (a sum of non-negative terms)
-    tau = 1e-6 * max|v| only guards exact zeros;
+    error of element i taken as |a - r| / max(|r|, tau): tau = lr per step
+    since the common state for the master weights (a weight that lands within
+    the updates' reach of zero has no meaningful relative error); for the
+    first moment tau is the size of the terms its updates summed, discounted
+    by beta1 per step (see assert_adam_close, MomentTolerance); for the second
+    moment (a sum of non-negative terms) tau = 1e-6 * max|v| only guards
+    exact zeros;
   * Adam bf16 primary: the exact rounding of the kernel's own fp32 master,
     and within 1 bf16 ulp of the oracle's (the fp32 results may differ in the
     last bits, which can move a value across a bf16 rounding boundary) where
@@ -36,41 +37,65 @@ def assert_same_nan(a, r, what):
     return ~na
 
 
-def assert_adam_close(got, ref, lr, what="", prev=None, g=None, hp=None, adamw=True):
-    """got/ref: (p, m, v, bf16) tuples of numpy arrays.
+def first_moment_scale(prev, g, hp, adamw=True):
+    """beta1*|m| + (1-beta1)*|g'| of one step (g' = g + wd*p in the L2 form):
+    the size of the two terms the first-moment update sums."""
+    b1 = float(hp["beta1"])
+    gabs = np.abs(np.asarray(g, np.float64))
+    if not adamw:
+        gabs = gabs + float(hp["weight_decay"]) * np.abs(np.asarray(prev[0], np.float64))
+    return b1 * np.abs(np.asarray(prev[1], np.float64)) + (1.0 - b1) * gabs
 
-    When the step's inputs are given (prev = (p, m, v) before the step, the
-    gradient g and the hyperparameters), the first moment's relative error is
-    taken against the size of the two terms it sums,
-    beta1*|m| + (1-beta1)*|g'| (g' = g + wd*p for the L2 form): where those
-    terms cancel, the result's own magnitude carries no fp32 precision.
-    Without them (zero first moment before the step, so m = (1-beta1)*g
-    involves no sum) tau = 1e-6 * max|m| guards values at zero."""
+
+class MomentTolerance:
+    """Running tolerance of the first moment over several steps taken from a
+    common starting state: an error made at step k decays by beta1 per later
+    step, so the tolerance is the beta1-discounted sum of the per-step term
+    sizes, S_t = beta1 * S_(t-1) + first_moment_scale_t."""
+
+    def __init__(self):
+        self.s = None
+
+    def step(self, prev, g, hp, adamw=True):
+        cur = first_moment_scale(prev, g, hp, adamw)
+        self.s = cur if self.s is None else float(hp["beta1"]) * self.s + cur
+        return self.s
+
+
+def assert_adam_close(got, ref, lr, what="", prev=None, g=None, hp=None, adamw=True, steps=1,
+                      m_tau=None):
+    """got/ref: (p, m, v, bf16) tuples of numpy arrays, `steps` steps after
+    the kernel and the oracle last shared their state.
+
+    Master weights: tau = steps * lr (a weight within the distance the
+    updates can move it of zero carries no meaningful relative error, and the
+    rounding of every step since the common state adds to the absolute one).
+    First moment: tau = m_tau if given (see MomentTolerance), else, when the
+    step's inputs are given (prev = (p, m, v) before the step, gradient g,
+    hyperparameters), the size of the two terms it sums; without them (zero
+    first moment before the step: m = (1-beta1)*g involves no sum)
+    tau = 1e-6 * max|m| guards values at zero.  Second moment (a sum of
+    non-negative terms): tau = 1e-6 * max|v|."""
     gp, gm, gv, gb = got
     rp, rm, rv, rb = ref
+    tau_p = lr * steps
     ok = assert_same_nan(gp, rp, what + " master")
-    e = rel_err(gp[ok], rp[ok], lr)
+    e = rel_err(gp[ok], rp[ok], tau_p)
     assert e.size == 0 or e.max() <= REL_TOL, "%s master rel err %.3g" % (what, e.max())
     tiny = np.finfo(np.float32).tiny
-    if prev is not None:
-        b1 = float(hp["beta1"])
-        gabs = np.abs(np.asarray(g, np.float64))
-        if not adamw:
-            gabs = gabs + float(hp["weight_decay"]) * np.abs(np.asarray(prev[0], np.float64))
-        m_scale = b1 * np.abs(np.asarray(prev[1], np.float64)) + (1.0 - b1) * gabs
-    else:
-        m_scale = None
+    if m_tau is None and prev is not None:
+        m_tau = first_moment_scale(prev, g, hp, adamw)
     for a, r, name in ((gm, rm, "exp_avg"), (gv, rv, "exp_avg_sq")):
         ok = assert_same_nan(a, r, what + " " + name)
         if not ok.any():
             continue
-        if name == "exp_avg" and m_scale is not None:
-            tau = np.maximum(m_scale[ok], tiny)
+        if name == "exp_avg" and m_tau is not None:
+            tau = np.maximum(np.asarray(m_tau)[ok], tiny)
         else:
             tau = max(1e-6 * float(np.abs(r[ok]).max()), tiny)
         e = rel_err(a[ok], r[ok], tau)
         assert e.max() <= REL_TOL, "%s %s rel err %.3g" % (what, name, e.max())
-    assert_bf16_primary(gb, gp, rb, rp, lr, what + " bf16")
+    assert_bf16_primary(gb, gp, rb, rp, tau_p, what + " bf16")
 
 
 def bf16_value(h):

@@ -12,7 +12,8 @@ import torch
 import oracle
 from paper_2407_01614_amd import synth
 from paper_2407_01614_amd.workloads import WORKLOADS, secondary_elems
-from parity import (assert_adam_close, assert_bits_equal, empty_dev, to_dev, to_host)
+from parity import (MomentTolerance, assert_adam_close, assert_bits_equal, empty_dev, to_dev,
+                    to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -69,16 +70,16 @@ def test_adam_multistep(zpp, adamw, hp):
     rp, rm, rv = p, m, v
     tp, tm, tv = (to_dev(x) for x in (p, m, v))
     out = empty_dev(n, np.uint16)
+    mt = MomentTolerance()
     for t in range(1, 8):
         g = synth.gradients(n, 40, it=t) * np.float32(5.0)
         zpp.adam_partition_step(tp, tm, tv, to_dev(g), out, step=t, adamw=adamw, **hp)
-        prev = (rp, rm, rv)
+        tau_m = mt.step((rp, rm, rv), g, hp, adamw)
         rp, rm, rv, rb = oracle.adam_step(rp, rm, rv, g, step=t, adamw=adamw, **hp)
         torch.cuda.synchronize()
         got = (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
                to_host(out, np.uint16))
-        assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "step %d" % t, prev=prev, g=g,
-                          hp=hp, adamw=adamw)
+        assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "step %d" % t, steps=t, m_tau=tau_m)
 
 
 @pytest.mark.parametrize("n", [1, 3, 4, 5, 1023, 2047, 2048, 2049, 3 * 2048 + 7, 100003])
