@@ -8,12 +8,13 @@ an event: the paper's fix).
 
 Prints ONE JSON line.  `value` is the algorithmic HBM bytes of all four
 kernels of a step divided by the measured time per step (GB/s), with every
-input resident in HBM.  Per-kernel durations come from a second run of K
+input resident in HBM; steps are ordered only by their data dependencies, so
+one step's gather overlaps the next step's Adam.  Per-kernel durations come from a second run of K
 steps with HIP timing events on each kernel's own stream.  Two further runs
 are reported beside it: the fused step + refresh + quantize kernel in place
 of the three separate ones, and the time per step with the gather ordered by
 a device event wait (the fix), by a host-side wait, or not at all (stock
-hpZ, racy: timing only).  The roofline entry is for the dominant kernel (the
+hpZ, racy: timing only), each with steps run one after another.  The roofline entry is for the dominant kernel (the
 Adam step).  The CPU baseline times the plain CPU oracle on a bounded sample
 of the same workload on this host.
 
@@ -185,11 +186,12 @@ def main():
     pipe = PartitionPipeline(wl)
     pipe.load_synthetic()
 
-    def run(fused, sync, timing):
+    def run(fused, sync, timing, overlap=True):
         """W warm-up steps, then K timed steps exactly as the path runs them
         (no instrumentation); with `timing`, K more steps with a timing-event
-        pair around every kernel on that kernel's own stream."""
-        pipe.fused, pipe.sync, pipe.timing = fused, sync, None
+        pair around every kernel on that kernel's own stream (the pipeline
+        then runs each kernel alone)."""
+        pipe.fused, pipe.sync, pipe.overlap, pipe.timing = fused, sync, overlap, None
         for _ in range(args.warmup):
             pipe.step()
         pipe.wait()
@@ -211,10 +213,11 @@ def main():
         return ms, times, pipe.kernel_bytes()
 
     ms_per_step, times, kb = run(False, "event", True)
+    serial_ms = run(False, "event", False, overlap=False)[0]
     fused_ms, fused_times, fused_kb = run(True, "event", True)
     sync_ab = {}
     for mode in ("event", "host", "none"):
-        sync_ab[mode] = round(run(False, mode, False)[0], 4)
+        sync_ab[mode] = round(run(False, mode, False, overlap=False)[0], 4)
     qgz = qgz_measure(pipe, wl, args.steps)
     step_bytes = sum(kb.values())
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -237,6 +240,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_without_overlap": round(serial_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -93,8 +93,8 @@ typedef struct {
  * be aligned to their element size (ZPP_EALIGN); 16-byte alignment of all
  * five selects the vector kernel.  hp must be non-NULL. */
 ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float *exp_avg_sq,
-                                   const float *grad, uint16_t *primary_bf16, size_t n,
-                                   const zpp_adam_hparams *hp, hipStream_t stream);
+                                           const float *grad, uint16_t *primary_bf16, size_t n,
+                                           const zpp_adam_hparams *hp, hipStream_t stream);
 
 /* Secondary refresh: the copy into the hpZ secondary partition
  * L_{i,second} of |L_i|/P' elements (Eq. 1) of the weights that belong to
@@ -105,9 +105,9 @@ ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float 
  * of this copy must wait on (the paper's fix).
  * The two ranges must not overlap (ZPP_EOVERLAP); pointers 2-byte aligned
  * (ZPP_EALIGN). */
-ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16, size_t count,
-                                 hipStream_t stream, hipEvent_t wait_before,
-                                 hipEvent_t done_after);
+ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16,
+                                         size_t count, hipStream_t stream, hipEvent_t wait_before,
+                                         hipEvent_t done_after);
 
 /* qwZ quantization of a weight shard before it is gathered (Background
  * section: weights are quantized before AllGather).  Symmetric absmax int8
@@ -124,8 +124,8 @@ ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_
  * No two of the three ranges may overlap (ZPP_EOVERLAP).  Alignment: src 2,
  * scales 4 (ZPP_EALIGN); src 16 and codes 8 bytes select the vector kernel. */
 ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n, uint32_t block,
-                                     int8_t *codes, float *scales, hipStream_t stream,
-                                     hipEvent_t wait_before, hipEvent_t done_after);
+                                             int8_t *codes, float *scales, hipStream_t stream,
+                                             hipEvent_t wait_before, hipEvent_t done_after);
 
 /* Fused partition step: zpp_adam_partition_step, then the secondary refresh
  * and the qwZ quantization of the new bf16 weights, in one pass over HBM
@@ -146,14 +146,12 @@ ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n,
  * bytes (ZPP_EALIGN); 16-byte fp32 arrays, 8-byte bf16 arrays and 4-byte
  * codes select the single-pass kernel, otherwise the three scalar kernels run
  * one after another. */
-ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
-                                                  float *exp_avg_sq, const float *grad,
-                                                  uint16_t *primary_bf16,
+ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg, float *exp_avg_sq,
+                                                  const float *grad, uint16_t *primary_bf16,
                                                   uint16_t *secondary_bf16, int8_t *codes,
                                                   float *scales, size_t n, uint32_t block,
-                                                  const zpp_adam_hparams *hp,
-                                                  hipStream_t stream, hipEvent_t wait_before,
-                                                  hipEvent_t done_after);
+                                                  const zpp_adam_hparams *hp, hipStream_t stream,
+                                                  hipEvent_t wait_before, hipEvent_t done_after);
 
 /* Maximum number of shards one gather accepts (the secondary group P'). */
 #define ZPP_MAX_SHARDS 64u
@@ -182,11 +180,11 @@ ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
  * scales 4 (ZPP_EALIGN); shard_elems % 16 == 0 with 16-byte aligned codes
  * and out selects the vector kernel. */
 ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
-                                    const float *const *shard_scales, uint32_t num_shards,
-                                    size_t shard_elems, uint32_t block, size_t layer_elems,
-                                    uint16_t *out_bf16, hipStream_t stream,
-                                    const hipEvent_t *wait_events, uint32_t num_wait,
-                                    hipEvent_t done_after);
+                                            const float *const *shard_scales, uint32_t num_shards,
+                                            size_t shard_elems, uint32_t block, size_t layer_elems,
+                                            uint16_t *out_bf16, hipStream_t stream,
+                                            const hipEvent_t *wait_events, uint32_t num_wait,
+                                            hipEvent_t done_after);
 
 /* qgZ, sending side: quantize a rank's fp32 gradient of one destination
  * partition before the exchange that replaces the ReduceScatter (Background
@@ -225,8 +223,8 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_
  * scales 4 bytes (ZPP_EALIGN); 16-byte out and 2-byte codes select the vector
  * kernel. */
 ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
-                                         const float *const *src_scales, uint32_t num_src,
-                                         size_t n, uint32_t block, float scale_out, float *out,
+                                         const float *const *src_scales, uint32_t num_src, size_t n,
+                                         uint32_t block, float scale_out, float *out,
                                          hipStream_t stream, const hipEvent_t *wait_events,
                                          uint32_t num_wait, hipEvent_t done_after);
 

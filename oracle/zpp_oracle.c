@@ -22,7 +22,7 @@
 
 /* ------------------------------------------------------------------------ */
 /* bf16 <-> fp32.  The paper fixes no precision; the primary and secondary   */
-/* weight copies are bf16 and the master weights fp32 in this build.         */
+/* weight copies are taken as bf16 and the master weights as fp32.           */
 /* ------------------------------------------------------------------------ */
 
 /* Round a binary32 value to bfloat16 (8-bit significand) with IEEE
@@ -126,20 +126,20 @@ void orc_refresh(uint16_t *dst, const uint16_t *src, size_t count)
         dst[i] = src[i];
 }
 
-/* ------------------------------------------------------------------------ */
-/* qwZ: weights are quantized before the AllGather (Background section).     */
-/* The paper gives no format; this build uses symmetric absmax int8 over     */
-/* blocks of `block` consecutive elements of one shard, one binary32 scale   */
-/* per block, codes in [-127, 127].  All decisions are taken in binary32,    */
-/* the precision the kernels use:                                           */
-/*   block holds a non-finite value -> scale = NaN (0x7FC00000), codes 0;    */
-/*   absmax a == 0                  -> scale = 0, codes 0;                   */
-/*   otherwise scale = RN(a / 127) and inv = RN(127 / a), and code =         */
-/*   rint(x * inv) (ties to even), clamped to [-127, 127].  When a < 2^-100  */
-/*   both x and a are first multiplied by 2^64 (exact) so that 127 / a       */
-/*   cannot overflow; the codes then stay invariant under scaling of the     */
-/*   block by any power of two.  The last block of a shard may be short.     */
-/* ------------------------------------------------------------------------ */
+/*
+ * qwZ: weights are quantized before the AllGather (Background section).  The
+ * paper gives no format; the one taken here is symmetric absmax int8 over
+ * blocks of `block` consecutive elements of one shard, one binary32 scale per
+ * block, codes in [-127, 127].  All decisions are taken in binary32, the
+ * precision the kernels use:
+ *   block holds a non-finite value -> scale = NaN (0x7FC00000), codes 0;
+ *   absmax a == 0                  -> scale = 0, codes 0;
+ *   otherwise scale = RN(a / 127) and inv = RN(127 / a), and code =
+ *   rint(x * inv) (ties to even), clamped to [-127, 127].  When a < 2^-100
+ *   both x and a are first multiplied by 2^64 (exact) so that 127 / a cannot
+ *   overflow; the codes then stay invariant under scaling of the block by any
+ *   power of two.  The last block of a shard may be short.
+ */
 static const uint32_t ORC_SCALE_NAN_BITS = 0x7FC00000u;
 
 void orc_quantize_blockwise_i8(const uint16_t *x, size_t n, uint32_t block, int8_t *codes,
@@ -224,22 +224,22 @@ void orc_dequant_gather_layer(const int8_t *const *shard_codes, const float *con
     }
 }
 
-/* ------------------------------------------------------------------------ */
-/* qgZ: gradients are quantized before the exchange that replaces the      */
-/* ReduceScatter (Background section; Algorithm 1, backward loop, where an */
-/* INT4 all-to-all takes the ReduceScatter's place).  The paper gives no   */
-/* format; this build uses symmetric absmax int4 over blocks of `block`    */
-/* consecutive binary32 gradient values of one destination partition, one */
-/* binary32 scale per block, codes in [-7, 7], all decisions in binary32:  */
-/*   block holds a non-finite value -> scale = NaN (0x7FC00000), codes 0;  */
-/*   absmax a == 0                  -> scale = 0, codes 0;                 */
-/*   otherwise scale = RN(a / 7), inv = RN(7 / a), code = rint(x * inv)    */
-/*   (ties to even), clamped to [-7, 7]; when a < 2^-100 both x and a are  */
-/*   first multiplied by 2^64 (exact).                                     */
-/* Codes are packed two per byte, element 2i in the low nibble and 2i+1 in */
-/* the high nibble, as 4-bit two's complement; an odd tail leaves the last */
-/* high nibble 0.                                                          */
-/* ------------------------------------------------------------------------ */
+/*
+ * qgZ: gradients are quantized before the exchange that replaces the
+ * ReduceScatter (Background section; Algorithm 1, backward loop, where an
+ * INT4 all-to-all takes the ReduceScatter's place).  The paper gives no
+ * format; the one taken here is symmetric absmax int4 over blocks of `block`
+ * consecutive binary32 gradient values of one destination partition, one
+ * binary32 scale per block, codes in [-7, 7], all decisions in binary32:
+ *   block holds a non-finite value -> scale = NaN (0x7FC00000), codes 0;
+ *   absmax a == 0                  -> scale = 0, codes 0;
+ *   otherwise scale = RN(a / 7), inv = RN(7 / a), code = rint(x * inv)
+ *   (ties to even), clamped to [-7, 7]; when a < 2^-100 both x and a are
+ *   first multiplied by 2^64 (exact).
+ * Codes are packed two per byte, element 2i in the low nibble and 2i+1 in the
+ * high nibble, as 4-bit two's complement; an odd tail leaves the last high
+ * nibble 0.
+ */
 void orc_quantize_blockwise_i4(const float *x, size_t n, uint32_t block, uint8_t *codes,
                                float *scales)
 {

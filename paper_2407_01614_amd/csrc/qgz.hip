@@ -92,9 +92,9 @@ __device__ __forceinline__ uint32_t abs_bits_max4(const f32x4 &v) {
 // spans L = min(B/4, 64) lanes and G = max(1, B/256) groups per lane; a
 // wave covers C = max(B, 256) values per tile and keeps U tiles in flight.
 template <int B, int U>
-__global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(const float *__restrict__ src,
-                                                               size_t n, uint8_t *__restrict__ codes,
-                                                               float *__restrict__ scales) {
+__global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
+    const float *__restrict__ src, size_t n, uint8_t *__restrict__ codes,
+    float *__restrict__ scales) {
     constexpr int C = B > 256 ? B : 256;
     constexpr int G = C / 256;
     constexpr int L = B < 256 ? B / 4 : kWave;
@@ -155,10 +155,9 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(const float *__re
 
 // Any alignment: one wave per block, lanes stride through it; each code
 // byte is written by the lane that owns its even element.
-__global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(const float *__restrict__ src,
-                                                                      size_t n, uint32_t block,
-                                                                      uint8_t *__restrict__ codes,
-                                                                      float *__restrict__ scales) {
+__global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(
+    const float *__restrict__ src, size_t n, uint32_t block, uint8_t *__restrict__ codes,
+    float *__restrict__ scales) {
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
     const size_t wave0 = (size_t)blockIdx.x * (kQgzThreads / kWave) + threadIdx.x / kWave;

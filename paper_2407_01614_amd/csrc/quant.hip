@@ -30,9 +30,9 @@ namespace {
 constexpr int kQuantThreads = ZPP_QUANT_THREADS;
 
 template <int B, int U>
-__global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(const uint16_t *__restrict__ src,
-                                                             size_t n, int8_t *__restrict__ codes,
-                                                             float *__restrict__ scales) {
+__global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
+    const uint16_t *__restrict__ src, size_t n, int8_t *__restrict__ codes,
+    float *__restrict__ scales) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;  // lanes per quant block
     constexpr int V = (B / 8 > kWave) ? B / (8 * kWave) : 1;
     constexpr int kGroupsPerWave = kWave / L;
@@ -105,10 +105,9 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(const uint16_t
 
 // Any alignment, any power-of-two block: one wave per quant block, lanes
 // stride through it element by element.
-__global__ __launch_bounds__(kThreads) void quant_scalar_kernel(const uint16_t *__restrict__ src,
-                                                                size_t n, uint32_t block,
-                                                                int8_t *__restrict__ codes,
-                                                                float *__restrict__ scales) {
+__global__ __launch_bounds__(kThreads) void quant_scalar_kernel(
+    const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
+    float *__restrict__ scales) {
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
     const size_t wave0 = (size_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;

@@ -21,9 +21,8 @@ namespace {
 constexpr int kRefreshThreads = ZPP_REFRESH_THREADS;
 
 template <int U>
-__global__ __launch_bounds__(kRefreshThreads) void refresh_vec_kernel(uint16_t *__restrict__ dst,
-                                                               const uint16_t *__restrict__ src,
-                                                               size_t count) {
+__global__ __launch_bounds__(kRefreshThreads) void refresh_vec_kernel(
+    uint16_t *__restrict__ dst, const uint16_t *__restrict__ src, size_t count) {
     constexpr size_t kTile = (size_t)kRefreshThreads * 8 * U;  // 8 bf16 per 16-byte vector
     const size_t ntiles = (count + kTile - 1) / kTile;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -32,10 +31,12 @@ __global__ __launch_bounds__(kRefreshThreads) void refresh_vec_kernel(uint16_t *
             u32x4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                x[u] = ld_nt(reinterpret_cast<const u32x4 *>(src + base + (size_t)u * kRefreshThreads * 8));
+                x[u] = ld_nt(reinterpret_cast<const u32x4 *>(src + base +
+                                                             (size_t)u * kRefreshThreads * 8));
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                st_nt(reinterpret_cast<u32x4 *>(dst + base + (size_t)u * kRefreshThreads * 8), x[u]);
+                st_nt(reinterpret_cast<u32x4 *>(dst + base + (size_t)u * kRefreshThreads * 8),
+                      x[u]);
         } else {
 #pragma unroll
             for (int u = 0; u < U; ++u) {

@@ -116,14 +116,12 @@ ZPP_API zpp_status zpp_adam_partition_step(float *master, float *exp_avg, float 
     return e == hipSuccess ? ZPP_OK : hip_fail(e);
 }
 
-ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
-                                                  float *exp_avg_sq, const float *grad,
-                                                  uint16_t *primary_bf16,
+ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg, float *exp_avg_sq,
+                                                  const float *grad, uint16_t *primary_bf16,
                                                   uint16_t *secondary_bf16, int8_t *codes,
                                                   float *scales, size_t n, uint32_t block,
-                                                  const zpp_adam_hparams *hp,
-                                                  hipStream_t stream, hipEvent_t wait_before,
-                                                  hipEvent_t done_after) {
+                                                  const zpp_adam_hparams *hp, hipStream_t stream,
+                                                  hipEvent_t wait_before, hipEvent_t done_after) {
     zpp_status st = check_hparams(hp);
     if (st != ZPP_OK)
         return st;
@@ -160,9 +158,9 @@ ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
     return record(stream, done_after);
 }
 
-ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16, size_t count,
-                                 hipStream_t stream, hipEvent_t wait_before,
-                                 hipEvent_t done_after) {
+ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_t *src_bf16,
+                                         size_t count, hipStream_t stream, hipEvent_t wait_before,
+                                         hipEvent_t done_after) {
     if (count > kMaxElems)
         return ZPP_EINVAL;
     if (count) {
@@ -186,8 +184,8 @@ ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_
 }
 
 ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n, uint32_t block,
-                                     int8_t *codes, float *scales, hipStream_t stream,
-                                     hipEvent_t wait_before, hipEvent_t done_after) {
+                                             int8_t *codes, float *scales, hipStream_t stream,
+                                             hipEvent_t wait_before, hipEvent_t done_after) {
     if (!valid_block(block) || n > kMaxElems)
         return ZPP_EINVAL;
     const size_t nblocks = (n + block - 1) / block;
@@ -213,11 +211,11 @@ ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n,
 }
 
 ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
-                                    const float *const *shard_scales, uint32_t num_shards,
-                                    size_t shard_elems, uint32_t block, size_t layer_elems,
-                                    uint16_t *out_bf16, hipStream_t stream,
-                                    const hipEvent_t *wait_events, uint32_t num_wait,
-                                    hipEvent_t done_after) {
+                                            const float *const *shard_scales, uint32_t num_shards,
+                                            size_t shard_elems, uint32_t block, size_t layer_elems,
+                                            uint16_t *out_bf16, hipStream_t stream,
+                                            const hipEvent_t *wait_events, uint32_t num_wait,
+                                            hipEvent_t done_after) {
     if (num_shards == 0 || num_shards > ZPP_MAX_SHARDS || !valid_block(block))
         return ZPP_EINVAL;
     if (shard_elems == 0 || shard_elems > kMaxElems / num_shards)
@@ -297,8 +295,8 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4(const float *src, size_t n, uint32_
 }
 
 ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
-                                         const float *const *src_scales, uint32_t num_src,
-                                         size_t n, uint32_t block, float scale_out, float *out,
+                                         const float *const *src_scales, uint32_t num_src, size_t n,
+                                         uint32_t block, float scale_out, float *out,
                                          hipStream_t stream, const hipEvent_t *wait_events,
                                          uint32_t num_wait, hipEvent_t done_after) {
     if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(block) || n > kMaxElems)

@@ -10,9 +10,9 @@ Per iteration (Algorithm 1 seen from one rank, one GPU):
 Local rank 0's shard of the gathered layer is the first s codes of this
 rank's own freshly quantized secondary; the other P' - 1 shards stand for the
 peers of the secondary group and live in this GPU's memory.  The gather waits
-on the quantize's event (the ordering fix); the next iteration's optimizer
-step waits for the gather, which closes the write-after-read edges on the
-primary, the secondary and the codes.
+on the quantize's event (the ordering fix); across iterations the
+write-after-read edges on the primary and the codes are events too, so one
+iteration's gather overlaps the next iteration's optimizer step.
 
 Buffers are laid out flat in HBM, one allocation per array, 256-byte
 aligned (torch's allocator), so every kernel takes its 16-byte vector path.
@@ -36,13 +36,14 @@ class PartitionPipeline:
     wait) or "none" (stock hpZ: no edge at all; the gather may read codes that
     are not written yet, so only its timing means anything)."""
 
-    def __init__(self, wl, device="cuda", fused=False, sync="event"):
+    def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True):
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         self.wl = wl
         self.dev = device
         self.fused = fused
         self.sync = sync
+        self.overlap = overlap
         n, s, B = wl.n, wl.shard_elems, wl.block
         if s > n:
             raise ValueError("the local gather shard (%d) must fit in the rank partition (%d)"
@@ -64,6 +65,7 @@ class PartitionPipeline:
         self.copy = torch.cuda.Stream(device)
         self.comm = torch.cuda.Stream(device)
         self.ev_primary = zpp.Event()
+        self.ev_refresh = zpp.Event()
         self.ev_quant = zpp.Event()
         self.ev_gather = zpp.Event()
         self.step_count = 0
@@ -131,12 +133,27 @@ class PartitionPipeline:
         self.timing[name].append((a, b))
 
     def step(self):
+        """Enqueue one iteration.  Edges: the step reads the gradient and
+        writes the primary; the refresh reads the primary (after the step) and
+        writes the secondary; the quantization reads the secondary and writes
+        codes and scales; the gather reads the codes (after the quantization:
+        the fix) and writes the layer.  Across iterations only the
+        write-after-read edges are needed: the next step waits for this
+        refresh (the primary), the next quantization for this gather (the
+        codes), so the gather of one iteration may overlap the next step.
+        With `overlap` off, or while timing kernels, the next step waits for
+        the whole iteration instead, so each kernel runs alone."""
         wl = self.wl
         n, s, B = wl.n, wl.shard_elems, wl.block
         self.step_count += 1
         t = self.step_count
+        serial = not self.overlap or self.timing is not None
         if t > 1:
-            zpp.stream_wait(self.compute, self.ev_gather)
+            if serial or self.fused:
+                # the fused kernel writes the codes, which the last gather reads
+                zpp.stream_wait(self.compute, self.ev_gather)
+            else:
+                zpp.stream_wait(self.compute, self.ev_refresh)
         if self.fused:
             self._timed("fused", self.compute, lambda: zpp.adam_step_refresh_quantize(
                 self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
@@ -149,7 +166,10 @@ class PartitionPipeline:
             self.ev_primary.record(self.compute)
             zpp.stream_wait(self.copy, self.ev_primary)
             self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
-                self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary))
+                self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary,
+                done_after=self.ev_refresh))
+            if t > 1:
+                zpp.stream_wait(self.copy, self.ev_gather)
             self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
                 self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
                 done_after=self.ev_quant))
