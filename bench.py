@@ -219,6 +219,19 @@ def main():
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False, overlap=False)[0], 4)
     qgz = qgz_measure(pipe, wl, args.steps)
+    # the whole iteration seen by the rank: qgZ receive (8 int4 sources ->
+    # mean gradient) feeding the step
+    from paper_2407_01614_amd import synth as _synth
+    from paper_2407_01614_amd.pipeline import GradientExchange
+    pipe.exchange = GradientExchange(wl.n, 8, wl.block)
+    for q in range(8):
+        g = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id, _synth.KIND_GRAD, rank=q)
+        pipe.exchange.quantize(q, g)
+        del g
+    torch.cuda.synchronize()
+    qgz_ms, qgz_times, qgz_kb = run(False, "event", True)
+    pipe.exchange = None
+    qgz_gbps = sum(qgz_kb.values()) / (qgz_ms * 1e-3) / 1e9
     step_bytes = sum(kb.values())
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = kernel_table(kb, times)
@@ -265,6 +278,10 @@ def main():
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
         "sync_ab_ms_per_step": sync_ab,
         "qgz_gradient_side": qgz,
+        "step_with_qgz_receive": {
+            "ms_per_step": round(qgz_ms, 4), "GB/s": round(qgz_gbps, 1),
+            "frac_of_peak": round(qgz_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(qgz_kb, qgz_times)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }
     del pipe

@@ -22,7 +22,8 @@ import torch
 
 from . import synth
 from . import zpp
-from .workloads import BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_gather, bytes_quant
+from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_gather, bytes_quant,
+                        bytes_reduce_i4)
 
 
 SYNC_MODES = ("event", "host", "none")
@@ -36,7 +37,8 @@ class PartitionPipeline:
     wait) or "none" (stock hpZ: no edge at all; the gather may read codes that
     are not written yet, so only its timing means anything)."""
 
-    def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True):
+    def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
+                 qgz_sources=0):
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         self.wl = wl
@@ -44,6 +46,10 @@ class PartitionPipeline:
         self.fused = fused
         self.sync = sync
         self.overlap = overlap
+        # with qgz_sources > 0 every step starts with the qgZ receive: the mean
+        # of that many int4 copies of this partition's gradient becomes `grad`
+        self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device)
+                         if qgz_sources else None)
         n, s, B = wl.n, wl.shard_elems, wl.block
         if s > n:
             raise ValueError("the local gather shard (%d) must fit in the rank partition (%d)"
@@ -120,6 +126,8 @@ class PartitionPipeline:
         """Record a HIP timing-event pair around every kernel, on the stream
         that kernel runs on."""
         names = ("fused", "gather") if self.fused else ("adam", "refresh", "quant", "gather")
+        if self.exchange is not None:
+            names = ("reduce_i4",) + names
         self.timing = {k: [] for k in names}
 
     def _timed(self, name, stream, fn):
@@ -154,6 +162,9 @@ class PartitionPipeline:
                 zpp.stream_wait(self.compute, self.ev_gather)
             else:
                 zpp.stream_wait(self.compute, self.ev_refresh)
+        if self.exchange is not None:
+            self._timed("reduce_i4", self.compute,
+                        lambda: self.exchange.reduce(self.grad, stream=self.compute))
         if self.fused:
             self._timed("fused", self.compute, lambda: zpp.adam_step_refresh_quantize(
                 self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
@@ -194,14 +205,19 @@ class PartitionPipeline:
     def kernel_bytes(self):
         wl = self.wl
         gather = float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems, wl.block))
+        out = {}
+        if self.exchange is not None:
+            out["reduce_i4"] = float(bytes_reduce_i4(wl.n, self.exchange.num_src, wl.block))
         if self.fused:
-            return {"fused": float(bytes_fused(wl.n, wl.block)), "gather": gather}
-        return {
+            out.update({"fused": float(bytes_fused(wl.n, wl.block)), "gather": gather})
+            return out
+        out.update({
             "adam": BYTES_ADAM * wl.n,
             "refresh": BYTES_REFRESH * wl.n,
             "quant": float(bytes_quant(wl.n, wl.block)),
             "gather": gather,
-        }
+        })
+        return out
 
     def kernel_times_ms(self):
         """Per-kernel list of event-measured durations (ms); call after wait()."""

@@ -273,3 +273,43 @@ def test_pipeline_modes_agree(zpp):
     expect = oracle.dequant_gather_layer([q[0] for q in peers], [q[1] for q in peers], s, B,
                                          wl.layer_elems - s)
     assert_bits_equal(ref[7].view(np.uint16)[s:], expect, "peer shards")
+
+
+def test_pipeline_with_qgz_receive(zpp):
+    """The qgZ receive at the start of each step: the mean of 8 int4 copies of
+    the partition's gradient (quantized by the oracle, as the senders would)
+    becomes the gradient of the Adam step.  The reduced gradient is bit-equal
+    to the oracle's, and two steps follow the oracle's Adam on it."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small-qgz", cfg_id=12, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
+                  secondary_world=4, world=4)
+    P = 8
+    srcs = [synth.gradients(wl.n, wl.cfg_id, q) for q in range(P)]
+    quants = [oracle.quantize_blockwise_i4(x, wl.block) for x in srcs]
+    pipe = PartitionPipeline(wl, qgz_sources=P)
+    peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
+                                          wl.block) for j in range(wl.secondary_world - 1)]
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
+    for q, (c, sc) in enumerate(quants):
+        pipe.exchange.codes[q].copy_(torch.from_numpy(c))
+        pipe.exchange.scales[q].copy_(torch.from_numpy(sc))
+    torch.cuda.synchronize()
+    pipe.step()
+    pipe.step()
+    pipe.wait()
+    mean = float(np.float32(1.0 / P))
+    g = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], wl.n, wl.block,
+                                 mean)
+    assert_bits_equal(to_host(pipe.grad, np.float32), g, "reduced gradient")
+    hp = f32hp(wl.adam)
+    z = np.zeros(wl.n, np.float32)
+    mt = MomentTolerance()
+    mt.step((p0, z, z), g, hp)
+    r1 = oracle.adam_step(p0, z, z, g, step=1, **hp)
+    tau_m = mt.step(r1[:3], g, hp)
+    r2 = oracle.adam_step(r1[0], r1[1], r1[2], g, step=2, **hp)
+    got = (to_host(pipe.master, np.float32), to_host(pipe.exp_avg, np.float32),
+           to_host(pipe.exp_avg_sq, np.float32), to_host(pipe.primary, np.uint16))
+    assert_adam_close(got, r2, hp["lr"], "after 2 steps", steps=2, m_tau=tau_m)
