@@ -1,0 +1,116 @@
+"""Sizes past 2^32 elements: 64-bit indexing and the grid-stride loops that
+take over once a one-shot grid would exceed its cap.  Checked on sampled
+outputs against the oracle and by properties on everything."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2407_01614_amd import synth
+from parity import assert_adam_close, assert_bits_equal
+
+pytestmark = pytest.mark.gpu
+
+BIG = (1 << 32) + 4099  # crosses 2^32 with a ragged tail
+
+
+@pytest.fixture(scope="module")
+def zpp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    free, _ = torch.cuda.mem_get_info()
+    if free < 120 * (1 << 30):
+        pytest.skip("needs about 100 GiB of free device memory")
+    from paper_2407_01614_amd import zpp as mod
+    return mod
+
+
+def sample_idx(n, seed, k=1 << 16):
+    g = np.random.default_rng(seed)
+    idx = np.unique(np.concatenate([g.integers(0, n, size=k), np.arange(1024),
+                                    np.arange((1 << 32) - 1024, (1 << 32) + 1024),
+                                    np.arange(n - 1024, n)]))
+    return torch.from_numpy(idx).cuda()
+
+
+def test_refresh_past_4g(zpp):
+    src = synth.device_bf16_weights(BIG, 100)
+    dst = torch.empty_like(src)
+    zpp.refresh_secondary(dst, src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    del src, dst
+    torch.cuda.empty_cache()
+
+
+def test_adam_past_4g(zpp):
+    n = BIG
+    hp = {k: float(np.float32(v)) for k, v in
+          dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1).items()}
+    p = synth.device_normal_f32(n, synth.WEIGHT_STD, 101, synth.KIND_MASTER)
+    g = synth.device_normal_f32(n, synth.GRAD_STD, 101, synth.KIND_GRAD)
+    m = torch.zeros(n, device="cuda")
+    v = torch.zeros(n, device="cuda")
+    out = torch.empty(n, dtype=torch.int16, device="cuda")
+    idx = sample_idx(n, 1)
+    ph = p.index_select(0, idx).cpu().numpy()
+    gh = g.index_select(0, idx).cpu().numpy()
+    zpp.adam_partition_step(p, m, v, g, out, step=1, **hp)
+    torch.cuda.synchronize()
+    got = tuple(t.index_select(0, idx).cpu().numpy().view(d) for t, d in
+                ((p, np.float32), (m, np.float32), (v, np.float32), (out, np.uint16)))
+    z = np.zeros_like(ph)
+    assert_adam_close(got, oracle.adam_step(ph, z, z, gh, step=1, **hp), hp["lr"], "past 2^32")
+    assert bool(torch.isfinite(p).all())
+    del p, g, m, v, out
+    torch.cuda.empty_cache()
+
+
+def test_quantize_past_4g(zpp):
+    n, B = BIG, 256
+    nb = (n + B - 1) // B
+    x = synth.device_bf16_weights(n, 102)
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    scales = torch.empty(nb, dtype=torch.float32, device="cuda")
+    zpp.quantize_blockwise_i8(x, codes, scales, block=B)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(3)
+    kb = np.unique(np.concatenate([g.integers(0, nb - 1, size=2048),
+                                   [(1 << 32) // B - 1, (1 << 32) // B, nb - 2]]))
+    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
+    rc, rs = oracle.quantize_blockwise_i8(x.index_select(0, eidx).cpu().numpy().view(np.uint16), B)
+    assert_bits_equal(codes.index_select(0, eidx).cpu().numpy(), rc, "codes")
+    assert_bits_equal(scales[torch.from_numpy(kb).cuda()].cpu().numpy(), rs, "scales")
+    tail = x[(nb - 1) * B:].cpu().numpy().view(np.uint16)
+    tc, ts = oracle.quantize_blockwise_i8(tail, B)
+    assert_bits_equal(codes[(nb - 1) * B:].cpu().numpy(), tc, "tail codes")
+    assert_bits_equal(scales[nb - 1:].cpu().numpy(), ts, "tail scale")
+    assert bool((scales > 0).all())
+    del x, codes, scales
+    torch.cuda.empty_cache()
+
+
+def test_gather_past_4g(zpp):
+    """A layer of more than 2^32 elements from 2 shards of 2^31 + 2^20."""
+    B, P2 = 256, 2
+    s = (1 << 31) + (1 << 20)
+    N = P2 * s - 777
+    codes = [synth.device_random_codes(s, 103, rank=j) for j in range(P2)]
+    scales = [synth.device_random_scales(s // B, 103, rank=j) for j in range(P2)]
+    out = torch.empty(N, dtype=torch.int16, device="cuda")
+    zpp.dequant_gather_layer(codes, scales, s, N, out, block=B)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(4)
+    per = s // B
+    kb = np.unique(np.concatenate([g.integers(0, 2 * per - 1, size=1024), [per - 1, per]]))
+    hc = np.concatenate([codes[k // per][(k % per) * B:(k % per + 1) * B].cpu().numpy() for k in kb])
+    hs = np.array([scales[k // per][k % per].item() for k in kb], np.float32)
+    ref = oracle.dequant_blockwise_i8(hc, hs, B)
+    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
+    assert_bits_equal(out.index_select(0, eidx).cpu().numpy().view(np.uint16), ref, "sampled")
+    # the end of the layer: the last 4 blocks of shard 1 reach past N
+    start = 2 * s - 4 * B
+    tail_ref = oracle.dequant_gather_layer([codes[1][-(4 * B):].cpu().numpy()],
+                                           [scales[1][-4:].cpu().numpy()], 4 * B, B, N - start)
+    assert_bits_equal(out[start:].cpu().numpy().view(np.uint16), tail_ref, "tail")
+    del codes, scales, out
+    torch.cuda.empty_cache()
