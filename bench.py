@@ -121,6 +121,34 @@ def qgz_measure(pipe, wl, reps, num_src=8):
     return res
 
 
+def copy_reference(reps=20):
+    """Two plain copies of 1 GiB on this GPU, for scale: the runtime's
+    device-to-device memcpy, and this library's refresh kernel (a bf16 copy)."""
+    import torch
+    from paper_2407_01614_amd import zpp
+    n = 1 << 29  # bf16 elements: 1 GiB
+    src = torch.ones(n, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name, fn in (("hipMemcpyAsync_d2d", lambda: dst.copy_(src)),
+                     ("refresh_kernel", lambda: zpp.refresh_secondary(dst, src, stream=stream))):
+        fn()
+        evs = []
+        for _ in range(reps):
+            a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        mean = sum(a.elapsed_ms(b) for a, b in evs) / reps
+        res[name] = round(2.0 * 2 * n / (mean * 1e-3) / 1e9, 1)
+    del src, dst
+    res["unit"] = "GB/s (1 GiB read + 1 GiB written)"
+    return res
+
+
 def cpu_baseline(wl, frac):
     """Time the CPU oracle (as it stands, one thread) on a `frac` sample of the
     workload: Adam on frac*n, refresh and quantization of frac*n, gather of a
@@ -219,6 +247,7 @@ def main():
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False, overlap=False)[0], 4)
     qgz = qgz_measure(pipe, wl, args.steps)
+    copy_ref = copy_reference()
     # the whole iteration seen by the rank: qgZ receive (8 int4 sources ->
     # mean gradient) feeding the step
     from paper_2407_01614_amd import synth as _synth
@@ -277,6 +306,7 @@ def main():
             "ms_per_step": round(fused_ms, 4), "GB/s": round(fused_gbps, 1),
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
         "sync_ab_ms_per_step": sync_ab,
+        "copy_reference": copy_ref,
         "qgz_gradient_side": qgz,
         "step_with_qgz_receive": {
             "ms_per_step": round(qgz_ms, 4), "GB/s": round(qgz_gbps, 1),
