@@ -681,3 +681,20 @@ def check_i4_dequant_reduce(orc):
 
 def test_i4_dequant_reduce_brute_force():
     check_i4_dequant_reduce(oracle.default())
+
+
+@pytest.mark.parametrize("part", range(16))
+def test_bf16_rne_exhaustive_vs_library(part):
+    """Every float32 bit pattern (a sixteenth per case): the oracle's rounding
+    equals torch's CPU conversion on all non-NaN values, and every NaN gives
+    the canonical 0x7FC0."""
+    orc = oracle.default()
+    span = 1 << 28
+    for lo in range(part * span, (part + 1) * span, 1 << 25):
+        bits = np.arange(lo, lo + (1 << 25), dtype=np.uint32)
+        x = bits.view(np.float32)
+        got = orc.bf16_rne(x)
+        ref = torch_bf16_bits(x)
+        isnan = (bits & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+        assert np.array_equal(got[~isnan], ref[~isnan]), hex(lo)
+        assert np.all(got[isnan] == 0x7FC0), hex(lo)
