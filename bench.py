@@ -182,7 +182,17 @@ def cpu_baseline(wl, frac):
     secs = (t1 - t0) + (t2 - t1) + (t3 - t2) + (t5 - t4)
     nbytes = (BYTES_ADAM * n + BYTES_REFRESH * n + bytes_quant(n, B)
               + bytes_gather(s, wl.secondary_world, N, B))
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "host_cpu": cpu, "host_logical_cpus": os.cpu_count(),
             "sample": "%s at %.3g of full size: Adam+refresh+quant on %d elements, gather of a "
                       "%d-element layer from %d shards; %.2f s of CPU time"
                       % (wl.name, frac, n, N, wl.secondary_world, secs),
