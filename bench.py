@@ -149,12 +149,21 @@ def copy_reference(reps=20):
     return res
 
 
-def cpu_baseline(wl, frac):
-    """Time the CPU oracle (as it stands, one thread) on a `frac` sample of the
-    workload: Adam on frac*n, refresh and quantization of frac*n, gather of a
-    frac*N layer from P' shards.  Inputs come from the same seeded
-    generators; generation is not timed."""
+def _chunks(n, parts, align):
+    """[a, b) ranges covering [0, n), each boundary a multiple of `align`."""
+    step = max(align, -(-n // parts) // align * align)
+    return [(a, min(n, a + step)) for a in range(0, n, step)]
+
+
+def cpu_baseline(wl, frac, threads=1):
+    """Time the CPU oracle (as it stands) on a `frac` sample of the workload:
+    Adam on frac*n, refresh and quantization of frac*n, gather of a frac*N
+    layer from P' shards.  With threads > 1 each op's elements are split into
+    block-aligned ranges, and the same oracle calls run on the ranges from a
+    pool of that many threads (the calls release the GIL).  Inputs come from
+    the same seeded generators; generation is not timed."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
     import oracle
     from paper_2407_01614_amd import synth
     from paper_2407_01614_amd.workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_gather,
@@ -167,18 +176,34 @@ def cpu_baseline(wl, frac):
     g = synth.gradients(n, wl.cfg_id)
     z = np.zeros(n, np.float32)
     w = synth.bf16_weights(wl.secondary_world * s, wl.cfg_id)
+    ranges = _chunks(n, threads, B)
+    pool = ThreadPoolExecutor(threads) if threads > 1 else None
+
+    def run(fn, items):
+        return list(pool.map(fn, items)) if pool else [fn(x) for x in items]
+
     t0 = time.perf_counter()
-    _, _, _, prim = oracle.adam_step(p, z, z, g, step=1, **wl.adam)
+    prim = run(lambda r: oracle.adam_step(p[r[0]:r[1]], z[r[0]:r[1]], z[r[0]:r[1]],
+                                          g[r[0]:r[1]], step=1, **wl.adam)[3], ranges)
     t1 = time.perf_counter()
-    sec = oracle.refresh(prim)
+    sec = run(oracle.refresh, prim)
     t2 = time.perf_counter()
-    oracle.quantize_blockwise_i8(sec, B)
+    run(lambda x: oracle.quantize_blockwise_i8(x, B), sec)
     t3 = time.perf_counter()
     quants = [oracle.quantize_blockwise_i8(w[j * s:(j + 1) * s], B)
               for j in range(wl.secondary_world)]
     t4 = time.perf_counter()
-    oracle.dequant_gather_layer([q[0] for q in quants], [q[1] for q in quants], s, B, N)
+    # shard j holds layer elements [j s, (j+1) s); each piece of a shard is
+    # gathered into its own place of the layer
+    pieces = [(j, a, b) for j in range(wl.secondary_world)
+              for a, b in _chunks(s, max(1, threads // wl.secondary_world), B)
+              if j * s + a < N]
+    run(lambda t: oracle.dequant_gather_layer(
+        [quants[t[0]][0][t[1]:t[2]]], [quants[t[0]][1][t[1] // B:-(-t[2] // B)]],
+        t[2] - t[1], B, min(t[2] - t[1], N - t[0] * s - t[1])), pieces)
     t5 = time.perf_counter()
+    if pool:
+        pool.shutdown()
     secs = (t1 - t0) + (t2 - t1) + (t3 - t2) + (t5 - t4)
     nbytes = (BYTES_ADAM * n + BYTES_REFRESH * n + bytes_quant(n, B)
               + bytes_gather(s, wl.secondary_world, N, B))
@@ -191,13 +216,22 @@ def cpu_baseline(wl, frac):
                     break
     except OSError:
         pass
-    return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "host_cpu": cpu, "host_logical_cpus": os.cpu_count(),
+    return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "host_cpu": cpu, "host_logical_cpus": os.cpu_count(),
             "sample": "%s at %.3g of full size: Adam+refresh+quant on %d elements, gather of a "
-                      "%d-element layer from %d shards; %.2f s of CPU time"
-                      % (wl.name, frac, n, N, wl.secondary_world, secs),
+                      "%d-element layer from %d shards; %d thread(s), %.2f s of wall time"
+                      % (wl.name, frac, n, N, wl.secondary_world, threads, secs),
             "seconds": {"adam": round(t1 - t0, 3), "refresh": round(t2 - t1, 3),
                         "quant": round(t3 - t2, 3), "gather": round(t5 - t4, 3)}}
+
+
+def host_threads():
+    """Threads for the all-cores CPU baseline: the CPUs this process may run
+    on, at most 16 (the host share of one GPU)."""
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:
+        return max(1, min(16, os.cpu_count() or 1))
 
 
 def main():
@@ -224,12 +258,13 @@ def main():
     pipe = PartitionPipeline(wl)
     pipe.load_synthetic()
 
-    def run(fused, sync, timing, overlap=True):
+    def run(fused, sync, timing, overlap=True, streams=1):
         """W warm-up steps, then K timed steps exactly as the path runs them
         (no instrumentation); with `timing`, K more steps with a timing-event
         pair around every kernel on that kernel's own stream (the pipeline
         then runs each kernel alone)."""
         pipe.fused, pipe.sync, pipe.overlap, pipe.timing = fused, sync, overlap, None
+        pipe.streams = streams
         for _ in range(args.warmup):
             pipe.step()
         pipe.wait()
@@ -250,12 +285,14 @@ def main():
             pipe.timing = None
         return ms, times, pipe.kernel_bytes()
 
+    # the headline: the path in order on one stream (the stream order is the
+    # fix); then the same kernels on three streams ordered by events
     ms_per_step, times, kb = run(False, "event", True)
-    serial_ms = run(False, "event", False, overlap=False)[0]
+    three_ms = run(False, "event", False, overlap=True, streams=3)[0]
     fused_ms, fused_times, fused_kb = run(True, "event", True)
     sync_ab = {}
     for mode in ("event", "host", "none"):
-        sync_ab[mode] = round(run(False, mode, False, overlap=False)[0], 4)
+        sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
     qgz = qgz_measure(pipe, wl, args.steps)
     copy_ref = copy_reference()
     # the whole iteration seen by the rank: qgZ receive (8 int4 sources ->
@@ -292,7 +329,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
-        "ms_per_step_without_overlap": round(serial_ms, 4),
+        "ms_per_step_three_streams": {"overlap": round(three_ms, 4),
+                                      "without_overlap": sync_ab["event"]},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -328,8 +366,10 @@ def main():
     torch.cuda.empty_cache()
     if args.cpu_sample > 0:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)
+        line["cpu_baseline_all_cores"] = cpu_baseline(wl, args.cpu_sample, host_threads())
     else:
         line["cpu_baseline"] = None
+        line["cpu_baseline_all_cores"] = None
     print(json.dumps(line), flush=True)
 
 

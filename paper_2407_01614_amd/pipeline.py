@@ -1,4 +1,4 @@
-"""One simulated rank's partition path on three HIP streams.
+"""One simulated rank's partition path, on three HIP streams or on one.
 
 Per iteration (Algorithm 1 seen from one rank, one GPU):
   compute stream : optimizer step on the rank's partition -> bf16 primary
@@ -6,6 +6,15 @@ Per iteration (Algorithm 1 seen from one rank, one GPU):
                    quantize it (qwZ)
   comm stream    : backward gather of one layer from the P' node-local
                    secondary shards, dequantizing on the way
+
+With `streams=1` the same kernels run in that order on the compute stream
+alone: the order of the stream is then the fix (the gather cannot start
+before the quantization of the copy it reads has finished) and no event is
+needed.  On one GPU this is the faster arrangement, because every kernel is
+bound by HBM bandwidth, so overlapping two of them gains nothing, while each
+edge between streams costs the device some microseconds.  The three-stream
+form is the one a training step uses when the copy overlaps the forward
+pass's compute.
 
 Local rank 0's shard of the gathered layer is the first s codes of this
 rank's own freshly quantized secondary; the other P' - 1 shards stand for the
@@ -31,21 +40,26 @@ SYNC_MODES = ("event", "host", "none")
 
 class PartitionPipeline:
     """`fused`: one pass for step + refresh + quantize instead of three
-    kernels.  `sync`: how the gather is ordered after the quantization --
-    "event" (the paper's fix, as a device-side stream wait), "host" (the host
-    blocks on the event before it enqueues the gather: the fix as a host-side
-    wait) or "none" (stock hpZ: no edge at all; the gather may read codes that
-    are not written yet, so only its timing means anything)."""
+    kernels.  `sync`: how the gather is ordered after the quantization on
+    three streams -- "event" (the paper's fix, as a device-side stream wait),
+    "host" (the host blocks on the event before it enqueues the gather: the
+    fix as a host-side wait) or "none" (stock hpZ: no edge at all; the gather
+    may read codes that are not written yet, so only its timing means
+    anything).  `streams=1` runs every kernel on the compute stream in path
+    order; `sync` and `overlap` do not apply there."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
-                 qgz_sources=0):
+                 qgz_sources=0, streams=3):
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
+        if streams not in (1, 3):
+            raise ValueError("streams must be 1 or 3")
         self.wl = wl
         self.dev = device
         self.fused = fused
         self.sync = sync
         self.overlap = overlap
+        self.streams = streams
         # with qgz_sources > 0 every step starts with the qgZ receive: the mean
         # of that many int4 copies of this partition's gradient becomes `grad`
         self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device)
@@ -76,6 +90,7 @@ class PartitionPipeline:
         self.ev_gather = zpp.Event()
         self.step_count = 0
         self.timing = None
+        self._prev_streams = streams
 
     # ------------------------------------------------------------------
     # inputs
@@ -155,6 +170,11 @@ class PartitionPipeline:
         n, s, B = wl.n, wl.shard_elems, wl.block
         self.step_count += 1
         t = self.step_count
+        if self.streams == 1:
+            self._step_one_stream(t)
+            self._prev_streams = 1
+            return
+        self._prev_streams = 3
         serial = not self.overlap or self.timing is not None
         if t > 1:
             if serial or self.fused:
@@ -194,6 +214,38 @@ class PartitionPipeline:
             [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
             wl.layer_elems, self.out, block=B, stream=self.comm, wait_events=waits,
             done_after=self.ev_gather))
+
+    def _step_one_stream(self, t):
+        """The iteration in path order on the compute stream: each kernel
+        starts after the one before it, so the refresh reads the finished
+        primary and the gather reads finished codes, and the next iteration's
+        writes come after this one's reads."""
+        wl = self.wl
+        n, s, B = wl.n, wl.shard_elems, wl.block
+        cs = self.compute
+        if t > 1 and self._prev_streams == 3:
+            # the last iteration ran on three streams: join its copy and comm
+            # work (the quantization, then the gather) into this stream
+            zpp.stream_wait(cs, self.ev_quant)
+            zpp.stream_wait(cs, self.ev_gather)
+        if self.exchange is not None:
+            self._timed("reduce_i4", cs, lambda: self.exchange.reduce(self.grad, stream=cs))
+        if self.fused:
+            self._timed("fused", cs, lambda: zpp.adam_step_refresh_quantize(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
+                self.secondary, self.codes, self.scales, step=t, block=B, stream=cs,
+                **wl.adam))
+        else:
+            self._timed("adam", cs, lambda: zpp.adam_partition_step(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
+                stream=cs, **wl.adam))
+            self._timed("refresh", cs, lambda: zpp.refresh_secondary(
+                self.secondary, self.primary, n, stream=cs))
+            self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
+                self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
+        self._timed("gather", cs, lambda: zpp.dequant_gather_layer(
+            [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
+            wl.layer_elems, self.out, block=B, stream=cs, done_after=self.ev_gather))
 
     def wait(self):
         self.ev_gather.synchronize()
