@@ -146,11 +146,13 @@ def test_fullsize_gather(zpp, wl):
     assert not bool(((out & 0x7FFF) > 0x7F80).any()), "NaN in the gathered layer"
 
 
-def test_fullsize_pipeline_properties(zpp):
-    """The benchmark's own pipeline, two steps: the secondary is the primary
-    bit for bit, the local shard of the gathered layer round-trips the primary
-    within half a quantization step, and nothing is NaN."""
-    pipe = PartitionPipeline(WL)
+@pytest.mark.parametrize("streams", [1, 3])
+def test_fullsize_pipeline_properties(zpp, streams):
+    """The benchmark's own pipeline (one stream, as timed; and three streams
+    with event edges), two steps: the secondary is the primary bit for bit,
+    the local shard of the gathered layer round-trips the primary within half
+    a quantization step, and nothing is NaN."""
+    pipe = PartitionPipeline(WL, streams=streams)
     pipe.load_synthetic()
     pipe.step()
     pipe.step()
@@ -214,8 +216,8 @@ def test_fullsize_fused_step_refresh_quantize(zpp):
 
 @pytest.mark.parametrize("name", ["llama-2-7b", "falcon-40b"])
 def test_fullsize_other_workloads(zpp, name):
-    """The other rank-partition workloads, through the benchmark's pipeline:
-    Llama-2-7B for 2 iterations, Falcon-40B for its 10 iterations with fresh
+    """The other rank-partition workloads, through the benchmark's pipeline
+    (one stream, as timed): Llama-2-7B for 2 iterations, Falcon-40B for its 10 iterations with fresh
     gradients each time.  The oracle follows the sampled elements' Adam state
     through every iteration; the gathered layer is checked on sampled blocks
     against the oracle's dequantization of the codes the gather read (the
@@ -225,7 +227,7 @@ def test_fullsize_other_workloads(zpp, name):
     iters = wl.iterations if wl.iterations > 1 else 2
     hp = f32hp(wl.adam)
     n, B, s = wl.n, wl.block, wl.shard_elems
-    pipe = PartitionPipeline(wl)
+    pipe = PartitionPipeline(wl, streams=1)
     pipe.master.copy_(synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER))
     pipe.exp_avg.zero_()
     pipe.exp_avg_sq.zero_()
