@@ -60,6 +60,17 @@ def test_header_compiles_as_c():
     assert r.returncode == 0, r.stderr
 
 
+def test_c_driver_is_built_and_links():
+    """The C test driver (built with the library) resolves libzpp.so,
+    liboracle.so and the HIP runtime; the GPU test runs it."""
+    drv = os.path.join(ROOT, "tests", "c_abi_driver")
+    assert os.path.exists(drv), "tests/c_abi_driver is not built: run __graft_entry__.build()"
+    out = subprocess.run(["ldd", drv], capture_output=True, text=True, check=True).stdout
+    assert "not found" not in out, out
+    for lib in ("libzpp.so", "liboracle.so", "libamdhip64.so"):
+        assert lib in out, out
+
+
 def test_hparams_layout(zpp):
     assert ctypes.sizeof(zpp.AdamHParams) == 32
     assert zpp.AdamHParams.step.offset == 24
