@@ -157,6 +157,9 @@ def stream_handle(stream):
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, int):
         return stream
+    if stream.device.index != torch.cuda.current_device():
+        raise ValueError("stream of %s, not of the current device cuda:%d"
+                         % (stream.device, torch.cuda.current_device()))
     return stream.cuda_stream
 
 
@@ -178,6 +181,11 @@ def _dev(t, dtypes, name):
         raise TypeError("%s must be a torch.Tensor" % name)
     if not t.is_cuda:
         raise ValueError("%s must be on the GPU" % name)
+    if t.device.index != torch.cuda.current_device():
+        # the library launches on the current device; a pointer into another
+        # device's memory would be dereferenced there
+        raise ValueError("%s is on %s, not on the current device cuda:%d"
+                         % (name, t.device, torch.cuda.current_device()))
     if t.dtype not in dtypes:
         raise TypeError("%s: dtype %s not in %s" % (name, t.dtype, dtypes))
     if not t.is_contiguous():

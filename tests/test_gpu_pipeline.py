@@ -129,6 +129,29 @@ def test_tiny_pipeline_on_streams(zpp):
     assert_bits_equal(gout[same], ref_out.reshape(-1, B)[same], "gathered layer")
 
 
+def independent_streams(zpp, tries=8):
+    """Two streams that the device runs side by side.  A process has a few
+    hardware queues (4 by default) and two HIP streams can share one, in
+    which case the device runs their work in submission order and no race
+    can show.  A pair counts as independent when an event recorded on the
+    second stream completes while the first is held by a bounded spin."""
+    import time
+    for _ in range(tries):
+        a, b = torch.cuda.Stream(), torch.cuda.Stream()
+        with torch.cuda.stream(a):
+            torch.cuda._sleep(50_000_000)
+        ev = zpp.Event().record(b)
+        t0 = time.perf_counter()
+        while not ev.query() and time.perf_counter() - t0 < 0.005:
+            pass
+        free = ev.query()
+        busy = not zpp.Event().record(a).query()  # the spin still runs
+        torch.cuda.synchronize()
+        if free and busy:
+            return a, b
+    pytest.skip("no two streams of this process run side by side")
+
+
 def run_race(zpp, fixed, s=1 << 20, B=256, spin_cycles=100_000_000):
     """Refresh + quantize shard 0 on the copy stream behind a long device-side
     spin; gather on the comm stream, waiting on the quantize's event only when
@@ -140,7 +163,7 @@ def run_race(zpp, fixed, s=1 << 20, B=256, spin_cycles=100_000_000):
     sc, ss = oracle.quantize_blockwise_i8(src, B)
     expect = oracle.dequant_gather_layer([sc, pc], [ss, ps], s, B, 2 * s)
     tsrc, tpc, tps = to_dev(src), to_dev(pc), to_dev(ps)
-    copy, comm = torch.cuda.Stream(), torch.cuda.Stream()
+    copy, comm = independent_streams(zpp)
     sec = empty_dev(s, np.uint16, fill=0x7FC0)
     codes = empty_dev(s, np.int8, fill=0)
     scales = empty_dev(s // B, np.float32, fill=float("nan"))
