@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--workload", default="llama-2-13b")
     ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of the workload the CPU oracle is timed on (0 = skip)")
+    ap.add_argument("--cpu-steps", type=int, default=2,
+                    help="consecutive steps the CPU oracle is timed over")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters, if present")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -155,13 +157,15 @@ def _chunks(n, parts, align):
     return [(a, min(n, a + step)) for a in range(0, n, step)]
 
 
-def cpu_baseline(wl, frac, threads=1):
-    """Time the CPU oracle (as it stands) on a `frac` sample of the workload:
-    Adam on frac*n, refresh and quantization of frac*n, gather of a frac*N
-    layer from P' shards.  With threads > 1 each op's elements are split into
-    block-aligned ranges, and the same oracle calls run on the ranges from a
-    pool of that many threads (the calls release the GIL).  Inputs come from
-    the same seeded generators; generation is not timed."""
+def cpu_baseline(wl, frac, threads=1, steps=1):
+    """Time the CPU oracle (as it stands) on a `frac` sample of the workload
+    for `steps` consecutive steps: Adam on frac*n (step t = 1, 2, ..., each
+    from the state the previous one left), refresh and quantization of
+    frac*n, gather of a frac*N layer from P' shards.  With threads > 1 each
+    op's elements are split into block-aligned ranges, and the same oracle
+    calls run on the ranges from a pool of that many threads (the calls
+    release the GIL).  Inputs come from the same seeded generators;
+    generation is not timed."""
     import numpy as np
     from concurrent.futures import ThreadPoolExecutor
     import oracle
@@ -182,31 +186,36 @@ def cpu_baseline(wl, frac, threads=1):
     def run(fn, items):
         return list(pool.map(fn, items)) if pool else [fn(x) for x in items]
 
-    t0 = time.perf_counter()
-    prim = run(lambda r: oracle.adam_step(p[r[0]:r[1]], z[r[0]:r[1]], z[r[0]:r[1]],
-                                          g[r[0]:r[1]], step=1, **wl.adam)[3], ranges)
-    t1 = time.perf_counter()
-    sec = run(oracle.refresh, prim)
-    t2 = time.perf_counter()
-    run(lambda x: oracle.quantize_blockwise_i8(x, B), sec)
-    t3 = time.perf_counter()
+    secs_by = {"adam": 0.0, "refresh": 0.0, "quant": 0.0, "gather": 0.0}
+    state = [(p[a:b], z[a:b], z[a:b]) for a, b in ranges]
     quants = [oracle.quantize_blockwise_i8(w[j * s:(j + 1) * s], B)
               for j in range(wl.secondary_world)]
-    t4 = time.perf_counter()
     # shard j holds layer elements [j s, (j+1) s); each piece of a shard is
     # gathered into its own place of the layer
     pieces = [(j, a, b) for j in range(wl.secondary_world)
               for a, b in _chunks(s, max(1, threads // wl.secondary_world), B)
               if j * s + a < N]
-    run(lambda t: oracle.dequant_gather_layer(
-        [quants[t[0]][0][t[1]:t[2]]], [quants[t[0]][1][t[1] // B:-(-t[2] // B)]],
-        t[2] - t[1], B, min(t[2] - t[1], N - t[0] * s - t[1])), pieces)
-    t5 = time.perf_counter()
+    for t in range(1, steps + 1):
+        t0 = time.perf_counter()
+        res = run(lambda k: oracle.adam_step(*state[k], g[ranges[k][0]:ranges[k][1]], step=t,
+                                             **wl.adam), range(len(ranges)))
+        t1 = time.perf_counter()
+        state = [r[:3] for r in res]
+        sec = run(oracle.refresh, [r[3] for r in res])
+        t2 = time.perf_counter()
+        run(lambda x: oracle.quantize_blockwise_i8(x, B), sec)
+        t3 = time.perf_counter()
+        run(lambda q: oracle.dequant_gather_layer(
+            [quants[q[0]][0][q[1]:q[2]]], [quants[q[0]][1][q[1] // B:-(-q[2] // B)]],
+            q[2] - q[1], B, min(q[2] - q[1], N - q[0] * s - q[1])), pieces)
+        t4 = time.perf_counter()
+        for k, dt in zip(secs_by, (t1 - t0, t2 - t1, t3 - t2, t4 - t3)):
+            secs_by[k] += dt
     if pool:
         pool.shutdown()
-    secs = (t1 - t0) + (t2 - t1) + (t3 - t2) + (t5 - t4)
-    nbytes = (BYTES_ADAM * n + BYTES_REFRESH * n + bytes_quant(n, B)
-              + bytes_gather(s, wl.secondary_world, N, B))
+    secs = sum(secs_by.values())
+    nbytes = steps * (BYTES_ADAM * n + BYTES_REFRESH * n + bytes_quant(n, B)
+                      + bytes_gather(s, wl.secondary_world, N, B))
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -218,11 +227,10 @@ def cpu_baseline(wl, frac, threads=1):
         pass
     return {"value": round(nbytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
             "kind": "oracle", "host_cpu": cpu, "host_logical_cpus": os.cpu_count(),
-            "sample": "%s at %.3g of full size: Adam+refresh+quant on %d elements, gather of a "
-                      "%d-element layer from %d shards; %d thread(s), %.2f s of wall time"
-                      % (wl.name, frac, n, N, wl.secondary_world, threads, secs),
-            "seconds": {"adam": round(t1 - t0, 3), "refresh": round(t2 - t1, 3),
-                        "quant": round(t3 - t2, 3), "gather": round(t5 - t4, 3)}}
+            "sample": "%s at %.3g of full size, %d step(s): Adam+refresh+quant on %d elements, "
+                      "gather of a %d-element layer from %d shards; %d thread(s), %.2f s of "
+                      "wall time" % (wl.name, frac, steps, n, N, wl.secondary_world, threads, secs),
+            "seconds": {k: round(v, 3) for k, v in secs_by.items()}}
 
 
 def host_threads():
@@ -365,8 +373,9 @@ def main():
     del pipe
     torch.cuda.empty_cache()
     if args.cpu_sample > 0:
-        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)
-        line["cpu_baseline_all_cores"] = cpu_baseline(wl, args.cpu_sample, host_threads())
+        line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample, steps=args.cpu_steps)
+        line["cpu_baseline_all_cores"] = cpu_baseline(wl, args.cpu_sample, host_threads(),
+                                                      steps=args.cpu_steps)
     else:
         line["cpu_baseline"] = None
         line["cpu_baseline_all_cores"] = None

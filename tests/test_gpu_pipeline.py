@@ -7,6 +7,8 @@ Stream layout (one simulated rank, as in the benchmark):
 The next iteration's refresh waits on `gather_done` (the buffer it overwrites
 is still being read until then).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -20,6 +22,15 @@ from parity import (MomentTolerance, assert_adam_close, assert_bits_equal, empty
 pytestmark = pytest.mark.gpu
 
 TINY = WORKLOADS["tiny"]
+# The small workload's 1,048,576 elements are read as one rank's partition
+# (4 ranks, a 4,194,304-element layer, shards of 2,097,152); the other reading
+# takes them as the whole layer (partitions of 262,144, shards of 524,288).
+# Both divide evenly; both run.
+TINY_READINGS = {
+    "rank-partition": TINY,
+    "whole-layer": dataclasses.replace(TINY, name="tiny-whole-layer", n=TINY.n // TINY.world,
+                                       layer_elems=TINY.n),
+}
 
 
 @pytest.fixture(scope="module")
@@ -33,18 +44,18 @@ def f32hp(hp):
     return {k: float(np.float32(v)) for k, v in hp.items()}
 
 
-def oracle_tiny_pipeline(hp):
-    """The Tiny workload on the oracle: 4 ranks step their partitions, the
+def oracle_tiny_pipeline(hp, wl=TINY):
+    """The small workload on the oracle: 4 ranks step their partitions, the
     forward-gathered layer is their concatenation, local rank j of the
     secondary group (P' = 2) copies its slice, quantizes it, and the backward
     gather rebuilds the layer."""
-    n, P, P2, B = TINY.n, TINY.world, TINY.secondary_world, TINY.block
-    N = TINY.layer_elems
+    n, P, P2, B = wl.n, wl.world, wl.secondary_world, wl.block
+    N = wl.layer_elems
     ranks = []
     layer = np.empty(N, np.uint16)
     for r in range(P):
-        p = synth.master_weights(n, TINY.cfg_id, r)
-        g = synth.gradients(n, TINY.cfg_id, r)
+        p = synth.master_weights(n, wl.cfg_id, r)
+        g = synth.gradients(n, wl.cfg_id, r)
         z = np.zeros(n, np.float32)
         res = oracle.adam_step(p, z, z, g, step=1, **hp)
         ranks.append(res)
@@ -76,17 +87,20 @@ def assert_downstream(g_prim, r_prim, g_codes, g_scales, r_codes, r_scales, B, w
     return same
 
 
-def test_tiny_pipeline_on_streams(zpp):
-    hp = f32hp(TINY.adam)
-    n, P, P2, B, N = TINY.n, TINY.world, TINY.secondary_world, TINY.block, TINY.layer_elems
-    s = TINY.shard_elems
+@pytest.mark.parametrize("reading", sorted(TINY_READINGS))
+def test_tiny_pipeline_on_streams(zpp, reading):
+    wl = TINY_READINGS[reading]
+    hp = f32hp(wl.adam)
+    n, P, P2, B, N = wl.n, wl.world, wl.secondary_world, wl.block, wl.layer_elems
+    s = wl.shard_elems
+    assert P * n == N and P2 * s == N
     compute, copy, comm = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     layer = empty_dev(N, np.uint16, fill=0x7FC0)
     states, grads = [], []
     for r in range(P):
-        states.append((to_dev(synth.master_weights(n, TINY.cfg_id, r)),
+        states.append((to_dev(synth.master_weights(n, wl.cfg_id, r)),
                        torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")))
-        grads.append(to_dev(synth.gradients(n, TINY.cfg_id, r)))
+        grads.append(to_dev(synth.gradients(n, wl.cfg_id, r)))
     torch.cuda.synchronize()
     primary_ready = zpp.Event()
     for r in range(P):
@@ -110,7 +124,7 @@ def test_tiny_pipeline_on_streams(zpp):
     gather_done.synchronize()
     torch.cuda.synchronize()
 
-    ranks, ref_layer, ref_secs, ref_quants, ref_out = oracle_tiny_pipeline(hp)
+    ranks, ref_layer, ref_secs, ref_quants, ref_out = oracle_tiny_pipeline(hp, wl)
     for r in range(P):
         p, m, v = states[r]
         got = (to_host(p, np.float32), to_host(m, np.float32), to_host(v, np.float32),
