@@ -1,22 +1,25 @@
 """Benchmark of one rank's partition path on one MI355X.
 
 A step is one pass of the whole path over one rank's state: the Adam
-partition step (compute stream), the secondary refresh and its int8
-quantization (copy stream), and the dequant-gather of one layer from the P'
-node-local secondary shards (comm stream, ordered after the quantization by
-an event: the paper's fix).
+partition step, the secondary refresh, its int8 quantization, and the
+dequant-gather of the layers of the backward pass from the P' node-local
+secondary shards (one layer for the Llama-2 workloads; Falcon-40B's step
+gathers its 60 layers).  The headline runs these kernels in that order on one
+HIP stream, so the stream order is the ordering fix of the paper: the gather
+cannot start before the quantization of the copy it reads has finished.
 
-Prints ONE JSON line.  `value` is the algorithmic HBM bytes of all four
-kernels of a step divided by the measured time per step (GB/s), with every
-input resident in HBM; steps are ordered only by their data dependencies, so
-one step's gather overlaps the next step's Adam.  Per-kernel durations come from a second run of K
-steps with HIP timing events on each kernel's own stream.  Two further runs
-are reported beside it: the fused step + refresh + quantize kernel in place
-of the three separate ones, and the time per step with the gather ordered by
-a device event wait (the fix), by a host-side wait, or not at all (stock
-hpZ, racy: timing only), each with steps run one after another.  The roofline entry is for the dominant kernel (the
-Adam step).  The CPU baseline times the plain CPU oracle on a bounded sample
-of the same workload on this host.
+Prints ONE JSON line.  `value` is the algorithmic HBM bytes of all kernels of
+a step divided by the measured wall time per step (GB/s), with every input
+resident in HBM.  Per-kernel durations come from a second run of K steps with
+a HIP timing-event pair around every kernel on its stream; the roofline entry
+is the dominant kernel's (the Adam step).  Beside it: the same step on three
+streams ordered by events (with and without one step's gather overlapping the
+next step's Adam), the fused step + refresh + quantize kernel in place of the
+three separate ones, the time per step with the gather ordered by a device
+event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
+timing only), the qgZ gradient side, and the step preceded by the qgZ
+receive.  The CPU baseline times the plain CPU oracle on a bounded sample of
+the same workload on this host.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload llama-2-13b]
 """
@@ -291,13 +294,13 @@ def main():
             pipe.wait()
             times = pipe.kernel_times_ms()
             pipe.timing = None
-        return ms, times, pipe.kernel_bytes()
+        return ms, times, pipe.kernel_bytes(), pipe.step_bytes()
 
     # the headline: the path in order on one stream (the stream order is the
     # fix); then the same kernels on three streams ordered by events
-    ms_per_step, times, kb = run(False, "event", True)
+    ms_per_step, times, kb, step_bytes = run(False, "event", True)
     three_ms = run(False, "event", False, overlap=True, streams=3)[0]
-    fused_ms, fused_times, fused_kb = run(True, "event", True)
+    fused_ms, fused_times, fused_kb, fused_step_bytes = run(True, "event", True)
     sync_ab = {}
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
@@ -313,14 +316,13 @@ def main():
         pipe.exchange.quantize(q, g)
         del g
     torch.cuda.synchronize()
-    qgz_ms, qgz_times, qgz_kb = run(False, "event", True)
+    qgz_ms, qgz_times, qgz_kb, qgz_step_bytes = run(False, "event", True)
     pipe.exchange = None
-    qgz_gbps = sum(qgz_kb.values()) / (qgz_ms * 1e-3) / 1e9
-    step_bytes = sum(kb.values())
+    qgz_gbps = qgz_step_bytes / (qgz_ms * 1e-3) / 1e9
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = kernel_table(kb, times)
     fused_kernels = kernel_table(fused_kb, fused_times)
-    fused_gbps = sum(fused_kb.values()) / (fused_ms * 1e-3) / 1e9
+    fused_gbps = fused_step_bytes / (fused_ms * 1e-3) / 1e9
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
     sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
 
@@ -345,12 +347,16 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "%s rank shard: n=%d fp32 master/m/v/grad, bf16 primary and "
-                               "secondary, int8 blocks of %d; gather of a %d-element layer "
+                               "secondary, int8 blocks of %d; %s of a %d-element layer "
                                "from %d secondary shards of %d"
-                               % (wl.name, wl.n, wl.block, wl.layer_elems, wl.secondary_world,
-                                  wl.shard_elems),
+                               % (wl.name, wl.n, wl.block,
+                                  "gather" if wl.layers_gathered == 1 else
+                                  "%d gathers (over %d stored layers)"
+                                  % (wl.layers_gathered, wl.distinct_layers),
+                                  wl.layer_elems, wl.secondary_world, wl.shard_elems),
                    "n": wl.n, "layer_elems": wl.layer_elems, "secondary_world": wl.secondary_world,
-                   "shard_elems": wl.shard_elems, "block": wl.block},
+                   "shard_elems": wl.shard_elems, "block": wl.block,
+                   "layers_gathered_per_step": wl.layers_gathered},
         "roofline": {"bound": "hbm", "kernel": "adam_partition_step",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic},

@@ -16,12 +16,15 @@ edge between streams costs the device some microseconds.  The three-stream
 form is the one a training step uses when the copy overlaps the forward
 pass's compute.
 
-Local rank 0's shard of the gathered layer is the first s codes of this
-rank's own freshly quantized secondary; the other P' - 1 shards stand for the
-peers of the secondary group and live in this GPU's memory.  The gather waits
-on the quantize's event (the ordering fix); across iterations the
-write-after-read edges on the primary and the codes are events too, so one
-iteration's gather overlaps the next iteration's optimizer step.
+Local rank 0's shard of the gathered layer is s codes of this rank's own
+freshly quantized secondary; the other P' - 1 shards stand for the peers of
+the secondary group and live in this GPU's memory.  A step gathers
+`wl.layers_gathered` layers (the backward pass visits every layer once),
+cycling over `wl.distinct_layers` stored layers: layer k takes the local
+codes [k s, (k+1) s) and its own set of peer shards.  The gathers wait on the
+quantize's event (the ordering fix); across iterations the write-after-read
+edges on the primary and the codes are events too, so one iteration's gathers
+overlap the next iteration's optimizer step.
 
 Buffers are laid out flat in HBM, one allocation per array, 256-byte
 aligned (torch's allocator), so every kernel takes its 16-byte vector path.
@@ -65,9 +68,12 @@ class PartitionPipeline:
         self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device)
                          if qgz_sources else None)
         n, s, B = wl.n, wl.shard_elems, wl.block
-        if s > n:
-            raise ValueError("the local gather shard (%d) must fit in the rank partition (%d)"
-                             % (s, n))
+        K = wl.distinct_layers
+        if K < 1 or wl.layers_gathered < 1:
+            raise ValueError("a step gathers at least one layer, from at least one stored layer")
+        if K * s > n:
+            raise ValueError("the local gather shards (%d x %d) must fit in the rank partition (%d)"
+                             % (K, s, n))
         f32 = dict(dtype=torch.float32, device=device)
         self.master = torch.empty(n, **f32)
         self.exp_avg = torch.zeros(n, **f32)
@@ -78,8 +84,11 @@ class PartitionPipeline:
         self.codes = torch.empty(n, dtype=torch.int8, device=device)
         self.scales = torch.empty((n + B - 1) // B, **f32)
         P2 = wl.secondary_world
-        self.peer_codes = [torch.empty(s, dtype=torch.int8, device=device) for _ in range(P2 - 1)]
-        self.peer_scales = [torch.empty(s // B, **f32) for _ in range(P2 - 1)]
+        # layer_peers[k] = (codes, scales) of the P' - 1 peer shards of stored layer k
+        self.layer_peers = [
+            ([torch.empty(s, dtype=torch.int8, device=device) for _ in range(P2 - 1)],
+             [torch.empty(s // B, **f32) for _ in range(P2 - 1)]) for _ in range(K)]
+        self.peer_codes, self.peer_scales = self.layer_peers[0]
         self.out = torch.empty(wl.layer_elems, dtype=torch.int16, device=device)
         self.compute = torch.cuda.Stream(device)
         self.copy = torch.cuda.Stream(device)
@@ -97,28 +106,60 @@ class PartitionPipeline:
     # ------------------------------------------------------------------
     def load(self, master, grad, peer_codes=None, peer_scales=None):
         """Copy host arrays in: the fp32 master shard and its gradient; the
-        peers' quantized shards if given (else see `quantize_peers`)."""
+        peers' quantized shards of stored layer 0 if given (else see
+        `quantize_peers` and `load_layer_peers`)."""
         self.master.copy_(torch.from_numpy(master))
         self.grad.copy_(torch.from_numpy(grad))
         self.exp_avg.zero_()
         self.exp_avg_sq.zero_()
         if peer_codes is not None:
-            for t, a in zip(self.peer_codes, peer_codes):
-                t.copy_(torch.from_numpy(a))
-            for t, a in zip(self.peer_scales, peer_scales):
-                t.copy_(torch.from_numpy(a))
+            self.load_layer_peers(0, peer_codes, peer_scales)
         self.step_count = 0
         torch.cuda.synchronize(self.dev)
 
+    def load_layer_peers(self, k, peer_codes, peer_scales):
+        """Copy host arrays in: the P' - 1 peers' codes and scales of stored
+        layer k."""
+        codes, scales = self.layer_peers[k]
+        if len(peer_codes) != len(codes) or len(peer_scales) != len(scales):
+            raise ValueError("one codes and one scales array per peer (%d)" % len(codes))
+        for t, a in zip(codes, peer_codes):
+            t.copy_(torch.from_numpy(a))
+        for t, a in zip(scales, peer_scales):
+            t.copy_(torch.from_numpy(a))
+        torch.cuda.synchronize(self.dev)
+
     def quantize_peers(self, cfg):
-        """Fill the peer shards by quantizing synthetic bf16 weights with the
-        library's own quantizer (set-up work, not part of a step)."""
+        """Fill the peer shards of every stored layer by quantizing synthetic
+        bf16 weights with the library's own quantizer (set-up work, not part
+        of a step)."""
         s = self.wl.shard_elems
-        for j, (c, sc) in enumerate(zip(self.peer_codes, self.peer_scales)):
-            w = synth.device_bf16_weights(s, cfg, rank=j + 1, device=self.dev)
-            zpp.quantize_blockwise_i8(w, c, sc, block=self.wl.block)
-            torch.cuda.synchronize(self.dev)
-            del w
+        for k, (codes, scales) in enumerate(self.layer_peers):
+            for j, (c, sc) in enumerate(zip(codes, scales)):
+                w = synth.device_bf16_weights(s, cfg, rank=j + 1, it=k, device=self.dev)
+                zpp.quantize_blockwise_i8(w, c, sc, block=self.wl.block)
+                torch.cuda.synchronize(self.dev)
+                del w
+
+    def layer_shards(self, k):
+        """Codes and scales of the P' shards of stored layer k, local rank 0
+        first: this rank's quantized secondary [k s, (k+1) s), then the peers."""
+        s, B = self.wl.shard_elems, self.wl.block
+        codes, scales = self.layer_peers[k]
+        return ([self.codes[k * s:(k + 1) * s]] + codes,
+                [self.scales[k * s // B:(k + 1) * s // B]] + scales)
+
+    def _gathers(self, stream, waits=(), done_after=None):
+        """The backward pass's gathers of one step, in layer order on `stream`;
+        the first waits on `waits`, the last records `done_after`."""
+        wl = self.wl
+        G = wl.layers_gathered
+        for i in range(G):
+            codes, scales = self.layer_shards(i % wl.distinct_layers)
+            self._timed("gather", stream, lambda: zpp.dequant_gather_layer(
+                codes, scales, wl.shard_elems, wl.layer_elems, self.out, block=wl.block,
+                stream=stream, wait_events=waits if i == 0 else (),
+                done_after=done_after if i == G - 1 else None))
 
     def load_synthetic(self):
         """Seeded synthetic state drawn on the device: master ~ N(0, 0.02),
@@ -159,15 +200,16 @@ class PartitionPipeline:
         """Enqueue one iteration.  Edges: the step reads the gradient and
         writes the primary; the refresh reads the primary (after the step) and
         writes the secondary; the quantization reads the secondary and writes
-        codes and scales; the gather reads the codes (after the quantization:
-        the fix) and writes the layer.  Across iterations only the
+        codes and scales; the gathers read the codes (after the quantization:
+        the fix) and write the layers.  Across iterations only the
         write-after-read edges are needed: the next step waits for this
-        refresh (the primary), the next quantization for this gather (the
-        codes), so the gather of one iteration may overlap the next step.
+        refresh (the primary), the next quantization for this step's last
+        gather (the codes), so the gathers of one iteration may overlap the
+        next step.
         With `overlap` off, or while timing kernels, the next step waits for
         the whole iteration instead, so each kernel runs alone."""
         wl = self.wl
-        n, s, B = wl.n, wl.shard_elems, wl.block
+        n, B = wl.n, wl.block
         self.step_count += 1
         t = self.step_count
         if self.streams == 1:
@@ -210,10 +252,7 @@ class PartitionPipeline:
             waits = [self.ev_quant]
         elif self.sync == "host":
             self.ev_quant.synchronize()
-        self._timed("gather", self.comm, lambda: zpp.dequant_gather_layer(
-            [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
-            wl.layer_elems, self.out, block=B, stream=self.comm, wait_events=waits,
-            done_after=self.ev_gather))
+        self._gathers(self.comm, waits, self.ev_gather)
 
     def _step_one_stream(self, t):
         """The iteration in path order on the compute stream: each kernel
@@ -225,7 +264,7 @@ class PartitionPipeline:
         three-stream iteration stays ordered after this one, since its own
         edges start from the compute stream."""
         wl = self.wl
-        n, s, B = wl.n, wl.shard_elems, wl.block
+        n, B = wl.n, wl.block
         cs = self.compute
         if t > 1 and self._prev_streams == 3:
             # the last iteration ran on three streams: join its copy and comm
@@ -247,9 +286,7 @@ class PartitionPipeline:
                 self.secondary, self.primary, n, stream=cs))
             self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
                 self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
-        self._timed("gather", cs, lambda: zpp.dequant_gather_layer(
-            [self.codes[:s]] + self.peer_codes, [self.scales[:s // B]] + self.peer_scales, s,
-            wl.layer_elems, self.out, block=B, stream=cs))
+        self._gathers(cs)
 
     def wait(self):
         """Block the host until every stream of the pipeline is idle."""
@@ -258,7 +295,17 @@ class PartitionPipeline:
     # ------------------------------------------------------------------
     # accounting
     # ------------------------------------------------------------------
+    def launches_per_step(self):
+        """How many times each kernel runs in one step."""
+        return {k: (self.wl.layers_gathered if k == "gather" else 1) for k in self.kernel_bytes()}
+
+    def step_bytes(self):
+        """Algorithmic HBM bytes of one whole step."""
+        per = self.launches_per_step()
+        return sum(b * per[k] for k, b in self.kernel_bytes().items())
+
     def kernel_bytes(self):
+        """Algorithmic HBM bytes of one launch of each kernel of the step."""
         wl = self.wl
         gather = float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems, wl.block))
         out = {}

@@ -52,6 +52,10 @@ class Workload:
     eps: float = 1e-8
     weight_decay: float = 0.1
     iterations: int = 1
+    # the backward pass of one step gathers this many layers, one after the
+    # other, cycling over `distinct_layers` separately stored synthetic layers
+    layers_gathered: int = 1
+    distinct_layers: int = 1
     notes: str = ""
 
     @property
@@ -87,8 +91,9 @@ WORKLOADS = {
         notes="Llama-2-13B over 64 ranks; one 5120-hidden layer gathered from 8 shards"),
     "falcon-40b": Workload(
         name="falcon-40b", cfg_id=4, n=FALCON_40B_TOTAL // 128, layer_elems=FALCON_40B_LAYER,
-        secondary_world=8, world=128, iterations=10,
-        notes="Falcon-40B over 128 ranks, 10 iterations"),
+        secondary_world=8, world=128, iterations=10, layers_gathered=60, distinct_layers=2,
+        notes="Falcon-40B over 128 ranks, 10 iterations; each step gathers its 60 layers, "
+              "cycling over 2 stored layers"),
 }
 
 # Algorithmic HBM bytes per element of each kernel (no re-reads, no recompute)

@@ -217,8 +217,9 @@ def test_fullsize_fused_step_refresh_quantize(zpp):
 @pytest.mark.parametrize("name", ["llama-2-7b", "falcon-40b"])
 def test_fullsize_other_workloads(zpp, name):
     """The other rank-partition workloads, through the benchmark's pipeline
-    (one stream, as timed): Llama-2-7B for 2 iterations, Falcon-40B for its 10 iterations with fresh
-    gradients each time.  The oracle follows the sampled elements' Adam state
+    (one stream, as timed): Llama-2-7B for 2 iterations, Falcon-40B for its
+    10 iterations with fresh gradients each time and 60 layer gathers per
+    iteration over 2 stored layers.  The oracle follows the sampled elements' Adam state
     through every iteration; the gathered layer is checked on sampled blocks
     against the oracle's dequantization of the codes the gather read (the
     peers' codes, drawn by the seeded generator) and, for the local shard,
@@ -231,9 +232,10 @@ def test_fullsize_other_workloads(zpp, name):
     pipe.master.copy_(synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER))
     pipe.exp_avg.zero_()
     pipe.exp_avg_sq.zero_()
-    for j in range(wl.secondary_world - 1):
-        pipe.peer_codes[j].copy_(synth.device_random_codes(s, wl.cfg_id, rank=j + 1))
-        pipe.peer_scales[j].copy_(synth.device_random_scales(s // B, wl.cfg_id, rank=j + 1))
+    for k, (pcodes, pscales) in enumerate(pipe.layer_peers):
+        for j in range(wl.secondary_world - 1):
+            pcodes[j].copy_(synth.device_random_codes(s, wl.cfg_id, rank=64 * k + j + 1))
+            pscales[j].copy_(synth.device_random_scales(s // B, wl.cfg_id, rank=64 * k + j + 1))
     idx = sample_indices(n, 1 << 18, 5)
     p = host(pipe.master, idx, np.float32)
     m = np.zeros_like(p)
@@ -255,6 +257,10 @@ def test_fullsize_other_workloads(zpp, name):
         assert_adam_close(got, (p, m, v, b), hp["lr"], "%s iteration %d" % (name, t), steps=t,
                           m_tau=tau_m)
     assert torch.equal(pipe.secondary, pipe.primary)
+    # the layer gathered last in the step (of `layers_gathered`, cycling over
+    # the stored layers) is the one left in the output
+    k_last = (wl.layers_gathered - 1) % wl.distinct_layers
+    peer_codes, peer_scales = pipe.layer_peers[k_last]
     # peers' part of the gathered layer: sampled whole blocks of each peer
     rng = np.random.default_rng(6)
     N = wl.layer_elems
@@ -264,15 +270,16 @@ def test_fullsize_other_workloads(zpp, name):
         if valid <= 0:
             continue
         kb = np.unique(rng.integers(0, valid // B, size=64))
-        codes = np.concatenate([pipe.peer_codes[j - 1][k * B:(k + 1) * B].cpu().numpy() for k in kb])
-        scl = pipe.peer_scales[j - 1][torch.from_numpy(kb).cuda()].cpu().numpy()
+        codes = np.concatenate([peer_codes[j - 1][k * B:(k + 1) * B].cpu().numpy() for k in kb])
+        scl = peer_scales[j - 1][torch.from_numpy(kb).cuda()].cpu().numpy()
         ref = oracle.dequant_blockwise_i8(codes, scl, B)
         eidx = torch.from_numpy((lo + kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
         assert_bits_equal(host(pipe.out, eidx, np.uint16), ref, "%s peer %d" % (name, j))
     # local shard: round trip of the primary within half a quantization step
-    prim = (pipe.primary[:s].to(torch.int32) << 16).view(torch.float32).to(torch.float64)
+    lo = k_last * s
+    prim = (pipe.primary[lo:lo + s].to(torch.int32) << 16).view(torch.float32).to(torch.float64)
     of = (pipe.out[:s].to(torch.int32) << 16).view(torch.float32).to(torch.float64)
-    sc = pipe.scales[:s // B].to(torch.float64).repeat_interleave(B)
+    sc = pipe.scales[lo // B:(lo + s) // B].to(torch.float64).repeat_interleave(B)
     assert bool(((prim - of).abs() <= sc * (0.5 + 2.0 ** -15) + of.abs() * 2.0 ** -8).all())
     del pipe
     torch.cuda.empty_cache()

@@ -318,6 +318,50 @@ def test_pipeline_modes_agree(zpp):
     assert_bits_equal(ref[7].view(np.uint16)[s:], expect, "peer shards")
 
 
+@pytest.mark.parametrize("layers", [4, 5])
+def test_step_gathers_every_layer(zpp, layers):
+    """A step whose backward pass gathers `layers` layers, cycling over two
+    stored layers (local shard k at codes [k s, (k+1) s), its own peer
+    shards): every gather runs (one timed launch each), one stream and three
+    streams end bit-identical, and the layer gathered last equals the oracle's
+    gather of that stored layer's shards."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small-layers", cfg_id=13, n=1 << 20, layer_elems=4 * (1 << 17) - 1000,
+                  secondary_world=4, world=4, layers_gathered=layers, distinct_layers=2)
+    s, B, P2 = wl.shard_elems, wl.block, wl.secondary_world
+    assert wl.distinct_layers * s <= wl.n
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    g0 = synth.gradients(wl.n, wl.cfg_id)
+    peers = [[oracle.quantize_blockwise_i8(synth.bf16_weights(s, wl.cfg_id, j + 1, it=k), B)
+              for j in range(P2 - 1)] for k in range(wl.distinct_layers)]
+    outs = {}
+    for streams in (1, 3):
+        pipe = PartitionPipeline(wl, streams=streams)
+        pipe.load(p0, g0)
+        for k in range(wl.distinct_layers):
+            pipe.load_layer_peers(k, [q[0] for q in peers[k]], [q[1] for q in peers[k]])
+        pipe.step()
+        pipe.enable_timing()
+        pipe.step()
+        pipe.wait()
+        assert len(pipe.kernel_times_ms()["gather"]) == layers
+        pipe.timing = None
+        k_last = (layers - 1) % wl.distinct_layers
+        codes = to_host(pipe.codes, np.int8)[k_last * s:(k_last + 1) * s]
+        scales = to_host(pipe.scales, np.float32)[k_last * s // B:(k_last + 1) * s // B]
+        expect = oracle.dequant_gather_layer([codes] + [q[0] for q in peers[k_last]],
+                                             [scales] + [q[1] for q in peers[k_last]], s, B,
+                                             wl.layer_elems)
+        got = to_host(pipe.out, np.uint16)
+        assert_bits_equal(got, expect, "layer %d gathered last, %d stream(s)" % (k_last, streams))
+        outs[streams] = [t.cpu().numpy().copy() for t in (pipe.master, pipe.primary, pipe.codes,
+                                                          pipe.out)]
+        del pipe
+    for a, b in zip(outs[1], outs[3]):
+        assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "one stream vs three")
+
+
 def test_pipeline_with_qgz_receive(zpp):
     """The qgZ receive at the start of each step: the mean of 8 int4 copies of
     the partition's gradient (quantized by the oracle, as the senders would)
