@@ -8,6 +8,9 @@
 // issued before any arithmetic, and every access is non-temporal (nothing is
 // reused).  The grid is one-shot (one tile per workgroup): on this GPU a
 // persistent grid of a few thousand workgroups streams about 20% slower.
+// Residency is capped at ZPP_ADAM_RESIDENCY one-wave workgroups per CU: at
+// the Llama-2-13B partition the step takes 923-931 us with 11 resident
+// (931-944 with 9, 10 or 12), 1003-1016 us uncapped.
 #include "zpp_adam.h"
 #include "zpp_device.h"
 #include "zpp_launch.h"
@@ -17,6 +20,9 @@
 #endif
 #ifndef ZPP_ADAM_THREADS
 #define ZPP_ADAM_THREADS 64
+#endif
+#ifndef ZPP_ADAM_RESIDENCY
+#define ZPP_ADAM_RESIDENCY 11
 #endif
 #ifndef ZPP_ADAM_MAX_GRID
 #define ZPP_ADAM_MAX_GRID (1u << 20)
@@ -113,12 +119,13 @@ hipError_t launch_adam(float *p, float *m, float *v, const float *g, uint16_t *o
         constexpr size_t kTile = (size_t)kAdamThreads * 4 * ZPP_ADAM_UNROLL;
         size_t tiles = (n + kTile - 1) / kTile;
         const unsigned grid = (unsigned)(tiles < ZPP_ADAM_MAX_GRID ? tiles : ZPP_ADAM_MAX_GRID);
+        constexpr size_t lds = residency_lds(ZPP_ADAM_RESIDENCY);
         if (c.adamw)
             hipLaunchKernelGGL((adam_vec_kernel<true, ZPP_ADAM_UNROLL>), dim3(grid),
-                               dim3(kAdamThreads), 0, stream, a);
+                               dim3(kAdamThreads), lds, stream, a);
         else
             hipLaunchKernelGGL((adam_vec_kernel<false, ZPP_ADAM_UNROLL>), dim3(grid),
-                               dim3(kAdamThreads), 0, stream, a);
+                               dim3(kAdamThreads), lds, stream, a);
     } else {
         size_t blocks = (n + kThreads - 1) / kThreads;
         const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));

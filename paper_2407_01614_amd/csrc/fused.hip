@@ -15,12 +15,17 @@
 // the 4 elements [chunk + 256 w + 4 l, +4) for w < C / 256.  The bf16 of the
 // updated weights stays in registers (two per 4 elements) until the block's
 // absmax is known; a 256-block is exactly one wave, so its absmax is a
-// six-step cross-lane reduction.
+// six-step cross-lane reduction.  Residency is capped at ZPP_FUSED_RESIDENCY
+// workgroups per CU, as for the optimizer step: 1031-1046 us with 12 resident
+// at the Llama-2-13B partition (11-14 within 1%), 1127-1145 us uncapped.
 #include "zpp_adam.h"
 #include "zpp_device.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
 
+#ifndef ZPP_FUSED_RESIDENCY
+#define ZPP_FUSED_RESIDENCY 12
+#endif
 #ifndef ZPP_FUSED_MAX_GRID
 #define ZPP_FUSED_MAX_GRID (1u << 30)
 #endif
@@ -126,10 +131,11 @@ void launch_fused_b(const FusedArgs &a, hipStream_t stream) {
     constexpr size_t C = B > 256 ? B : 256;
     const size_t chunks = (a.n + C - 1) / C;
     const unsigned grid = (unsigned)(chunks < ZPP_FUSED_MAX_GRID ? chunks : ZPP_FUSED_MAX_GRID);
+    constexpr size_t lds = residency_lds(ZPP_FUSED_RESIDENCY);
     if (a.c.adamw)
-        hipLaunchKernelGGL((fused_kernel<true, B>), dim3(grid), dim3(kWave), 0, stream, a);
+        hipLaunchKernelGGL((fused_kernel<true, B>), dim3(grid), dim3(kWave), lds, stream, a);
     else
-        hipLaunchKernelGGL((fused_kernel<false, B>), dim3(grid), dim3(kWave), 0, stream, a);
+        hipLaunchKernelGGL((fused_kernel<false, B>), dim3(grid), dim3(kWave), lds, stream, a);
 }
 
 }  // namespace

