@@ -6,15 +6,21 @@
 // the shard, so the pointer is a uniform (scalar) load.  Vector kernel: a lane
 // turns 8 codes (one 8-byte load) and one scale (shared by the 32 lanes of a
 // 256-block, served from cache) into 8 bf16 (one 16-byte store), about three
-// VALU operations per element.
+// VALU operations per element.  Shape, swept at the Llama-2-13B layer:
+// two-wave workgroups with two rows per wave, at most 12 workgroups per CU,
+// 149-150 us; four-wave workgroups with four rows (uncapped) 155-156 us, one
+// row 178-181 us.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
 #ifndef ZPP_GATHER_UNROLL
-#define ZPP_GATHER_UNROLL 4
+#define ZPP_GATHER_UNROLL 2
 #endif
 #ifndef ZPP_GATHER_THREADS
-#define ZPP_GATHER_THREADS 256
+#define ZPP_GATHER_THREADS 128
+#endif
+#ifndef ZPP_GATHER_RESIDENCY
+#define ZPP_GATHER_RESIDENCY 12
 #endif
 #ifndef ZPP_GATHER_MAX_GRID_X
 #define ZPP_GATHER_MAX_GRID_X (1u << 20)
@@ -160,7 +166,7 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
         const unsigned gx =
             (unsigned)(tiles < ZPP_GATHER_MAX_GRID_X ? tiles : ZPP_GATHER_MAX_GRID_X);
         hipLaunchKernelGGL((gather_vec_kernel<ZPP_GATHER_UNROLL>), dim3(gx, num_shards),
-                           dim3(kGatherThreads), 0, stream, a);
+                           dim3(kGatherThreads), residency_lds(ZPP_GATHER_RESIDENCY), stream, a);
     } else {
         const size_t blocks = (per_shard + kThreads - 1) / kThreads;
         const unsigned gx = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
