@@ -1,20 +1,21 @@
 // Secondary refresh: bit copy of the local rank's bf16 weights into the hpZ
 // secondary partition (Algorithm 1, forward loop; Eq. 1).  2 B read + 2 B
 // written per element.  Each thread moves U 16-byte vectors per tile, all
-// loads issued before the stores, non-temporal both ways.  Residency is
-// capped at ZPP_REFRESH_RESIDENCY four-wave workgroups per CU: 126-128 us at
-// the Llama-2-13B partition against 129-131 us uncapped.
+// loads issued before the stores, non-temporal both ways.  Shape, swept at
+// the Llama-2-13B partition (813 MB moved): one-wave workgroups with one
+// vector per lane, residency left to the hardware, 120.7-123.1 us; four-wave
+// workgroups with four vectors per lane 124.3-131.1 us, capped or not.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
 #ifndef ZPP_REFRESH_UNROLL
-#define ZPP_REFRESH_UNROLL 4
+#define ZPP_REFRESH_UNROLL 1
 #endif
 #ifndef ZPP_REFRESH_THREADS
-#define ZPP_REFRESH_THREADS 256
+#define ZPP_REFRESH_THREADS 64
 #endif
 #ifndef ZPP_REFRESH_RESIDENCY
-#define ZPP_REFRESH_RESIDENCY 5
+#define ZPP_REFRESH_RESIDENCY 0
 #endif
 #ifndef ZPP_REFRESH_MAX_GRID
 #define ZPP_REFRESH_MAX_GRID (1u << 20)
