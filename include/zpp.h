@@ -169,8 +169,8 @@ ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
  *   (int8_t[shard_elems] and float[ceil(shard_elems/block)] each); they are
  *   read during the call only.  num_shards in [1, ZPP_MAX_SHARDS]; every
  *   pointer non-NULL.  out_bf16: uint16_t[layer_elems] out.
- * layer_elems <= num_shards * shard_elems, block a power of two in
- *   [64, 4096] (ZPP_EINVAL otherwise).
+ * shard_elems >= 1, layer_elems <= num_shards * shard_elems (layer_elems 0
+ *   is a no-op), block a power of two in [64, 4096] (ZPP_EINVAL otherwise).
  * Order on `stream`: wait for every event of wait_events[0..num_wait) on the
  * device (the paper's fix: no gather before the copies it reads are
  * complete), gather, record `done_after` (lets the next refresh of these
