@@ -17,9 +17,10 @@ streams ordered by events (with and without one step's gather overlapping the
 next step's Adam), the fused step + refresh + quantize kernel in place of the
 three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
-timing only), the qgZ gradient side, and the step preceded by the qgZ
-receive.  The CPU baseline times the plain CPU oracle on a bounded sample of
-the same workload on this host.
+timing only), the qgZ gradient side, the step preceded by the qgZ receive,
+and, for context, PyTorch's fused AdamW on a partition of the same size.  The
+CPU baseline times the plain CPU oracle on a bounded sample of the same
+workload on this host.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload llama-2-13b]
 """
@@ -124,6 +125,44 @@ def qgz_measure(pipe, wl, reps, num_src=8):
     res["sources"] = num_src
     del ex, out
     return res
+
+
+def torch_adamw_context(wl, reps):
+    """Context, not the product path: PyTorch's own fused AdamW step
+    (torch.optim.AdamW(fused=True)) on a partition of the same size, followed
+    by the bf16 copy of the weights that the partition step emits in the same
+    pass; timed with events over `reps` steps.  Same hyperparameters and the
+    same 30 B per element of algorithmic traffic."""
+    import torch
+    from paper_2407_01614_amd import synth
+    p = torch.nn.Parameter(synth.device_normal_f32(wl.n, synth.WEIGHT_STD, wl.cfg_id,
+                                                   synth.KIND_MASTER))
+    p.grad = synth.device_normal_f32(wl.n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD)
+    out = torch.empty(wl.n, dtype=torch.bfloat16, device="cuda")
+    opt = torch.optim.AdamW([p], lr=wl.lr, betas=(wl.beta1, wl.beta2), eps=wl.eps,
+                            weight_decay=wl.weight_decay, fused=True)
+
+    def step():
+        opt.step()
+        out.copy_(p.detach())
+
+    for _ in range(3):
+        step()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for a, b in evs:
+        a.record()
+        step()
+        b.record()
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in evs) / reps
+    gbps = 30.0 * wl.n / (ms * 1e-3) / 1e9
+    del opt, p, out
+    torch.cuda.empty_cache()
+    return {"what": "torch.optim.AdamW(fused=True).step() + bf16 copy of the weights, same "
+                    "partition and hyperparameters (context, not the product path)",
+            "ms_per_step": round(ms, 4), "GB/s": round(gbps, 1),
+            "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def copy_reference(reps=20):
@@ -306,6 +345,7 @@ def main():
         sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
     qgz = qgz_measure(pipe, wl, args.steps)
     copy_ref = copy_reference()
+    torch_ctx = torch_adamw_context(wl, args.steps)
     # the whole iteration seen by the rank: qgZ receive (8 int4 sources ->
     # mean gradient) feeding the step
     from paper_2407_01614_amd import synth as _synth
@@ -369,6 +409,9 @@ def main():
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
         "sync_ab_ms_per_step": sync_ab,
         "copy_reference": copy_ref,
+        "torch_fused_adamw_context": dict(
+            torch_ctx, speedup_of_partition_step=round(
+                torch_ctx["ms_per_step"] / (kernels["adam"]["mean_us"] * 1e-3), 3)),
         "qgz_gradient_side": qgz,
         "step_with_qgz_receive": {
             "ms_per_step": round(qgz_ms, 4), "GB/s": round(qgz_gbps, 1),
