@@ -275,6 +275,34 @@ def cpu_baseline(wl, frac, threads=1, steps=1):
             "seconds": {k: round(v, 3) for k, v in secs_by.items()}}
 
 
+def gpu_clock_state():
+    """Clock policy of GPU 0 as amd-smi reports it (graphics clock range and
+    whether it is locked, HBM clock) and its market name, or None.  Called before this process
+    initialises the GPU, so the query runs in a child of a process without a
+    GPU context; the current clocks are idle values then, the ranges are what
+    the run may use."""
+    import subprocess
+
+    def query(*args):
+        res = subprocess.run(["amd-smi", *args, "--json"], capture_output=True, text=True,
+                             timeout=20)
+        return json.loads(res.stdout)["gpu_data"][0]
+
+    try:
+        clk = query("metric", "--clock")["clock"]
+        gfx, mem = clk["gfx_0"], clk["mem_0"]
+        state = {"gfx_mhz_min": gfx["min_clk"]["value"], "gfx_mhz_max": gfx["max_clk"]["value"],
+                 "gfx_clock_locked": gfx["clk_locked"], "gfx_deep_sleep": gfx["deep_sleep"],
+                 "hbm_mhz": mem["clk"]["value"], "source": "amd-smi metric --clock"}
+    except Exception:
+        return None
+    try:
+        state["market_name"] = query("static", "--asic")["asic"]["market_name"]
+    except Exception:
+        pass
+    return state
+
+
 def host_threads():
     """Threads for the all-cores CPU baseline: the CPUs this process may run
     on, at most 16 (the host share of one GPU)."""
@@ -292,6 +320,7 @@ def main():
               % args.gpus, file=sys.stderr)
         sys.exit(2)
 
+    clocks = gpu_clock_state()
     import torch
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import WORKLOADS
@@ -418,6 +447,10 @@ def main():
             "frac_of_peak": round(qgz_gbps / HBM_PEAK_GBPS, 4),
             "kernels": kernel_table(qgz_kb, qgz_times)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
+        "gpu": {"name": torch.cuda.get_device_name(0),
+                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
+                "memory_gib": round(torch.cuda.get_device_properties(0).total_memory / 2**30, 1),
+                "clocks": clocks},
     }
     del pipe
     torch.cuda.empty_cache()
