@@ -166,50 +166,84 @@ def independent_streams(zpp, tries=8):
     pytest.skip("no two streams of this process run side by side")
 
 
-def run_race(zpp, fixed, s=1 << 20, B=256, spin_cycles=100_000_000):
-    """Refresh + quantize shard 0 on the copy stream behind a long device-side
-    spin; gather on the comm stream, waiting on the quantize's event only when
-    `fixed`.  The secondary starts as NaN poison, standing in for the
+class RaceSetup:
+    """Shard 0 is refreshed from `src` and quantized on the copy stream behind
+    a long device-side spin; the gather of shard 0 and a peer shard runs on the
+    comm stream.  The secondary starts as NaN poison, standing in for the
     uninitialised torch.empty buffer of the paper's allocation."""
-    src = synth.bf16_weights(s, 90, 0)
-    peer = synth.bf16_weights(s, 90, 1)
-    pc, ps = oracle.quantize_blockwise_i8(peer, B)
-    sc, ss = oracle.quantize_blockwise_i8(src, B)
-    expect = oracle.dequant_gather_layer([sc, pc], [ss, ps], s, B, 2 * s)
-    tsrc, tpc, tps = to_dev(src), to_dev(pc), to_dev(ps)
-    copy, comm = independent_streams(zpp)
-    sec = empty_dev(s, np.uint16, fill=0x7FC0)
-    codes = empty_dev(s, np.int8, fill=0)
-    scales = empty_dev(s // B, np.float32, fill=float("nan"))
-    out = empty_dev(2 * s, np.uint16, fill=0)
-    torch.cuda.synchronize()
-    done = zpp.Event()
-    with torch.cuda.stream(copy):
-        torch.cuda._sleep(spin_cycles)  # bounded spin kernel: the copy is still queued
-    zpp.refresh_secondary(sec, tsrc, stream=copy)
-    zpp.quantize_blockwise_i8(sec, codes, scales, block=B, stream=copy, done_after=done)
-    zpp.dequant_gather_layer([codes, tpc], [scales, tps], s, 2 * s, out, block=B, stream=comm,
-                             wait_events=[done] if fixed else [])
-    torch.cuda.synchronize()
-    return to_host(out, np.uint16), expect
+
+    def __init__(self, zpp, s=1 << 20, B=256):
+        self.zpp, self.s, self.B = zpp, s, B
+        src = synth.bf16_weights(s, 90, 0)
+        peer = synth.bf16_weights(s, 90, 1)
+        pc, ps = oracle.quantize_blockwise_i8(peer, B)
+        sc, ss = oracle.quantize_blockwise_i8(src, B)
+        self.expect = oracle.dequant_gather_layer([sc, pc], [ss, ps], s, B, 2 * s)
+        self.tsrc, self.tpc, self.tps = to_dev(src), to_dev(pc), to_dev(ps)
+        self.copy, self.comm = independent_streams(zpp)
+        self.sec = empty_dev(s, np.uint16)
+        self.codes = empty_dev(s, np.int8)
+        self.scales = empty_dev(s // B, np.float32)
+        self.out = empty_dev(2 * s, np.uint16)
+        self.done = zpp.Event()
+
+    def run(self, fixed, spin_cycles=100_000_000):
+        """One race: poison every buffer, then the spin, refresh and
+        quantization on the copy stream and the gather on the comm stream,
+        which waits on the quantization's event only when `fixed`."""
+        zpp, B, s = self.zpp, self.B, self.s
+        self.sec.fill_(0x7FC0)
+        self.codes.fill_(0)
+        self.scales.fill_(float("nan"))
+        self.out.fill_(0)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(self.copy):
+            torch.cuda._sleep(spin_cycles)  # bounded spin kernel: the copy is still queued
+        zpp.refresh_secondary(self.sec, self.tsrc, stream=self.copy)
+        zpp.quantize_blockwise_i8(self.sec, self.codes, self.scales, block=B, stream=self.copy,
+                                  done_after=self.done)
+        zpp.dequant_gather_layer([self.codes, self.tpc], [self.scales, self.tps], s, 2 * s,
+                                 self.out, block=B, stream=self.comm,
+                                 wait_events=[self.done] if fixed else [])
+        torch.cuda.synchronize()
+        return to_host(self.out, np.uint16)
 
 
 def test_fix_orders_gather_after_refresh(zpp):
-    """With the event wait (the paper's fix) the gather is exact, every time."""
-    for _ in range(5):
-        got, expect = run_race(zpp, fixed=True)
-        assert_bits_equal(got, expect, "gather after the fix")
+    """With the event wait (the paper's fix) the gather is exact, every time,
+    over 100 races in which the copy is held back behind a spin."""
+    race = RaceSetup(zpp)
+    for rep in range(100):
+        assert_bits_equal(race.run(fixed=True), race.expect, "gather after the fix, race %d" % rep)
+
+
+def test_serialized_launches_give_the_same_result(zpp):
+    """With every kernel launch serialized by the runtime
+    (AMD_SERIALIZE_KERNEL=3: each launch waits for the previous work and is
+    waited for) the fixed path must still agree with the oracle: the smoke
+    pass (Adam, refresh and quantization on two streams, the gather on a
+    third after the event) runs in one child process with that setting."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    env = dict(os.environ, AMD_SERIALIZE_KERNEL="3")
+    res = subprocess.run([sys.executable, "-c", "import __graft_entry__ as g; g.smoke()"],
+                         cwd=root, env=env, capture_output=True, text=True, timeout=300)
+    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
+    assert "smoke ok" in res.stdout
 
 
 def test_race_without_the_fix_reads_poison(zpp):
     """Without the wait the gather runs while the copy is still queued behind
     the spin and reads the poisoned shard: NaN in the gathered layer, as the
     paper reports for stock hpZ."""
-    got, expect = run_race(zpp, fixed=False)
-    s = 1 << 20
+    race = RaceSetup(zpp)
+    got = race.run(fixed=False)
+    s = race.s
     nan = (got & 0x7FFF) > 0x7F80
     assert nan[:s].mean() > 0.99, "the racy gather did not see the poison"
-    assert_bits_equal(got[s:], expect[s:], "peer shard")
+    assert_bits_equal(got[s:], race.expect[s:], "peer shard")
 
 
 def test_iterations_with_buffer_reuse(zpp):
