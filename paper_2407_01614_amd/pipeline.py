@@ -29,6 +29,8 @@ overlap the next iteration's optimizer step.
 Buffers are laid out flat in HBM, one allocation per array, 256-byte
 aligned (torch's allocator), so every kernel takes its 16-byte vector path.
 """
+import functools
+
 import numpy as np
 import torch
 
@@ -156,9 +158,9 @@ class PartitionPipeline:
         G = wl.layers_gathered
         for i in range(G):
             codes, scales = self.layer_shards(i % wl.distinct_layers)
-            self._timed("gather", stream, lambda: zpp.dequant_gather_layer(
-                codes, scales, wl.shard_elems, wl.layer_elems, self.out, block=wl.block,
-                stream=stream, wait_events=waits if i == 0 else (),
+            self._timed("gather", stream, functools.partial(
+                zpp.dequant_gather_layer, codes, scales, wl.shard_elems, wl.layer_elems,
+                self.out, block=wl.block, stream=stream, wait_events=waits if i == 0 else (),
                 done_after=done_after if i == G - 1 else None))
 
     def load_synthetic(self):
