@@ -20,6 +20,8 @@ Tolerances:
 import numpy as np
 import torch
 
+import oracle
+
 REL_TOL = 1e-5
 
 
@@ -96,6 +98,43 @@ def assert_adam_close(got, ref, lr, what="", prev=None, g=None, hp=None, adamw=T
         e = rel_err(a[ok], r[ok], tau)
         assert e.max() <= REL_TOL, "%s %s rel err %.3g" % (what, name, e.max())
     assert_bf16_primary(gb, gp, rb, rp, tau_p, what + " bf16")
+
+
+class ChunkedAdam:
+    """The oracle's Adam state for a whole partition, kept in chunks that a
+    pool of host threads steps and checks side by side (the oracle's calls
+    and numpy's array work release the GIL).  Each chunk carries its own
+    first-moment tolerance (MomentTolerance) from the common start."""
+
+    def __init__(self, p0, hp, ex, parts=64):
+        n = p0.size
+        step = -(-n // parts)
+        self.rs = [(a, min(n, a + step)) for a in range(0, n, step)]
+        self.hp, self.ex, self.t = hp, ex, 0
+        self.st = [dict(p=p0[a:b].copy(), m=np.zeros(b - a, np.float32),
+                        v=np.zeros(b - a, np.float32), mt=MomentTolerance())
+                   for a, b in self.rs]
+
+    def step(self, g):
+        self.t += 1
+
+        def one(k):
+            st, (a, b) = self.st[k], self.rs[k]
+            st["tau"] = st["mt"].step((st["p"], st["m"], st["v"]), g[a:b], self.hp)
+            st["p"], st["m"], st["v"], st["b"] = oracle.adam_step(
+                st["p"], st["m"], st["v"], g[a:b], step=self.t, **self.hp)
+
+        list(self.ex.map(one, range(len(self.rs))))
+
+    def check(self, got, what):
+        """got: whole (p, m, v, bf16) arrays, `self.t` steps after the start."""
+        def one(k):
+            st, (a, b) = self.st[k], self.rs[k]
+            assert_adam_close(tuple(x[a:b] for x in got), (st["p"], st["m"], st["v"], st["b"]),
+                              self.hp["lr"], "%s [%d, %d)" % (what, a, b), steps=self.t,
+                              m_tau=st["tau"])
+
+        list(self.ex.map(one, range(len(self.rs))))
 
 
 def bf16_value(h):

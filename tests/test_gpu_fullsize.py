@@ -3,12 +3,16 @@
 The full Llama-2-13B rank partition (203,372,880 elements) and layer
 (317,204,480 elements over 8 shards), and the padded Falcon-7B layer, run
 through the same entry points with the same sizes as the benchmark, so the
-kernels and grids are the ones it times.  The oracle checks a sample of
-outputs it can compute one by one (elementwise Adam, whole quantization
-blocks, whole gathered blocks); properties that hold at any size are checked
-on everything.  Inputs are drawn on the device by the seeded generators; the
-sampled inputs are copied to the host before any kernel touches them.
+kernels and grids are the ones it times.  The quantization and the gather
+are compared with the oracle over the whole arrays (the oracle runs on
+block-aligned ranges from a pool of host threads); the optimizer step over a
+sample of elements it computes one by one, plus properties that hold at any
+size on everything.  Inputs are drawn on the device by the seeded
+generators and copied to the host before any kernel touches them.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -17,13 +21,12 @@ import oracle
 from paper_2407_01614_amd import synth
 from paper_2407_01614_amd.pipeline import PartitionPipeline
 from paper_2407_01614_amd.workloads import WORKLOADS
-from parity import MomentTolerance, assert_adam_close, assert_bits_equal
+from parity import ChunkedAdam, assert_adam_close, assert_bits_equal
 
 pytestmark = pytest.mark.gpu
 
 WL = WORKLOADS["llama-2-13b"]
 F7 = WORKLOADS["falcon-7b-layer"]
-NSAMPLE = 1 << 20
 NBLOCKS = 4096
 
 
@@ -38,18 +41,35 @@ def f32hp(hp):
     return {k: float(np.float32(v)) for k, v in hp.items()}
 
 
-def sample_indices(n, k, seed):
-    g = np.random.default_rng(seed)
-    idx = np.unique(np.concatenate([g.integers(0, n, size=k), np.arange(4096),
-                                    np.arange(n - 4096, n)]))
-    return torch.from_numpy(idx).cuda()
-
-
 def host(t, idx, dtype):
     return t.index_select(0, idx).cpu().numpy().view(dtype)
 
 
+def pool():
+    try:
+        k = len(os.sched_getaffinity(0))
+    except AttributeError:
+        k = os.cpu_count() or 1
+    return ThreadPoolExecutor(max(1, min(16, k)))
+
+
+def oracle_quantize_whole(x, B, ex):
+    """The oracle's quantization of a whole array, on block-aligned ranges."""
+    n = x.size
+    step = max(B, -(-n // 64) // B * B)
+    parts = list(ex.map(lambda a: oracle.quantize_blockwise_i8(x[a:a + step], B),
+                        range(0, n, step)))
+    return np.concatenate([c for c, _ in parts]), np.concatenate([sc for _, sc in parts])
+
+
+def whole(t, dtype):
+    return t.cpu().numpy().view(dtype)
+
+
 def test_fullsize_adam_two_steps(zpp):
+    """Two steps over the whole Llama-2-13B partition (203,372,880 elements),
+    every element against the oracle after each; then properties on
+    everything."""
     n = WL.n
     hp = f32hp(WL.adam)
     p = synth.device_normal_f32(n, synth.WEIGHT_STD, WL.cfg_id, synth.KIND_MASTER)
@@ -58,24 +78,17 @@ def test_fullsize_adam_two_steps(zpp):
     m = torch.zeros(n, device="cuda")
     v = torch.zeros(n, device="cuda")
     out = torch.empty(n, dtype=torch.int16, device="cuda")
-    idx = sample_indices(n, NSAMPLE, 1)
-    p0, gh1, gh2 = host(p, idx, np.float32), host(g1, idx, np.float32), host(g2, idx, np.float32)
+    p0, gh1, gh2 = whole(p, np.float32), whole(g1, np.float32), whole(g2, np.float32)
     torch.cuda.synchronize()
-    zpp.adam_partition_step(p, m, v, g1, out, step=1, **hp)
-    torch.cuda.synchronize()
-    got1 = tuple(host(t, idx, d) for t, d in ((p, np.float32), (m, np.float32),
-                                              (v, np.float32), (out, np.uint16)))
-    zpp.adam_partition_step(p, m, v, g2, out, step=2, **hp)
-    torch.cuda.synchronize()
-    got2 = tuple(host(t, idx, d) for t, d in ((p, np.float32), (m, np.float32),
-                                              (v, np.float32), (out, np.uint16)))
-    z = np.zeros_like(p0)
-    r1 = oracle.adam_step(p0, z, z, gh1, step=1, **hp)
-    assert_adam_close(got1, r1, hp["lr"], "step 1")
-    r2 = oracle.adam_step(r1[0], r1[1], r1[2], gh2, step=2, **hp)
-    mt = MomentTolerance()
-    mt.step((p0, z, z), gh1, hp)
-    assert_adam_close(got2, r2, hp["lr"], "step 2", steps=2, m_tau=mt.step(r1[:3], gh2, hp))
+    with pool() as ex:
+        ref = ChunkedAdam(p0, hp, ex)
+        for t, (g, gh) in enumerate(((g1, gh1), (g2, gh2)), start=1):
+            zpp.adam_partition_step(p, m, v, g, out, step=t, **hp)
+            torch.cuda.synchronize()
+            ref.step(gh)
+            ref.check(tuple(whole(x, d) for x, d in ((p, np.float32), (m, np.float32),
+                                                     (v, np.float32), (out, np.uint16))),
+                      "step %d" % t)
     # properties on everything: finite, bf16 is the rounding of the master
     assert torch.isfinite(p).all() and torch.isfinite(v).all() and (v >= 0).all()
     hi = (p.view(torch.int32) >> 16).to(torch.int16)
@@ -89,26 +102,22 @@ def block_sample(nblocks, k, seed):
 
 
 def test_fullsize_quantize(zpp):
+    """Every block of the Llama-2-13B partition (794,427 blocks; the last
+    holds 80 elements) against the oracle, bit for bit."""
     n, B = WL.n, WL.block
     nb = (n + B - 1) // B
+    assert n - (nb - 1) * B == 80
     x = synth.device_bf16_weights(n, WL.cfg_id, rank=0)
-    kb = block_sample(nb, NBLOCKS, 2)  # whole blocks; the short last block separately
-    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
-    xs = host(x, eidx, np.uint16)
-    tail = x[(nb - 1) * B:].cpu().numpy().view(np.uint16)
-    assert tail.size == n - (nb - 1) * B == 80
+    xh = x.cpu().numpy().view(np.uint16)
     codes = torch.empty(n, dtype=torch.int8, device="cuda")
     scales = torch.empty(nb, dtype=torch.float32, device="cuda")
     torch.cuda.synchronize()
     zpp.quantize_blockwise_i8(x, codes, scales, block=B)
     torch.cuda.synchronize()
-    rc, rs = oracle.quantize_blockwise_i8(xs, B)
-    assert_bits_equal(host(codes, eidx, np.int8), rc, "sampled blocks codes")
-    assert_bits_equal(host(scales, torch.from_numpy(kb).cuda(), np.float32), rs,
-                      "sampled blocks scales")
-    tc, ts = oracle.quantize_blockwise_i8(tail, B)
-    assert_bits_equal(codes[(nb - 1) * B:].cpu().numpy(), tc, "tail codes")
-    assert_bits_equal(scales[nb - 1:].cpu().numpy(), ts, "tail scale")
+    with pool() as ex:
+        rc, rs = oracle_quantize_whole(xh, B, ex)
+    assert_bits_equal(codes.cpu().numpy(), rc, "whole codes")
+    assert_bits_equal(scales.cpu().numpy(), rs, "whole scales")
     # properties on everything
     assert torch.isfinite(scales).all() and (scales > 0).all()
     assert int(codes.min()) >= -127 and int(codes.max()) <= 127
@@ -118,31 +127,21 @@ def test_fullsize_quantize(zpp):
 
 @pytest.mark.parametrize("wl", [WL, F7], ids=["llama-2-13b-layer", "falcon-7b-layer"])
 def test_fullsize_gather(zpp, wl):
+    """The whole gathered layer (317,204,480 or 207,070,080 elements, the
+    latter through a padded last shard) against the oracle, bit for bit."""
     N, P2, B, s = wl.layer_elems, wl.secondary_world, wl.block, wl.shard_elems
     codes = [synth.device_random_codes(s, wl.cfg_id, rank=j) for j in range(P2)]
     scales = [synth.device_random_scales(s // B, wl.cfg_id, rank=j) for j in range(P2)]
     out = torch.full((N,), 0x5A5A, dtype=torch.int16, device="cuda")
-    nbl = (N + B - 1) // B  # output blocks; with a padded last shard the last one is short
-    kb = block_sample(nbl, NBLOCKS, 3)
     torch.cuda.synchronize()
     zpp.dequant_gather_layer(codes, scales, s, N, out, block=B)
     torch.cuda.synchronize()
-    hc = np.empty((kb.size, B), np.int8)
-    hs = np.empty(kb.size, np.float32)
-    per = s // B
-    for i, k in enumerate(kb):
-        j, kk = divmod(int(k), per)
-        hc[i] = codes[j][kk * B:(kk + 1) * B].cpu().numpy()
-        hs[i] = scales[j][kk].item()
-    ref = oracle.dequant_blockwise_i8(hc.ravel(), hs, B)
-    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
-    assert_bits_equal(host(out, eidx, np.uint16), ref, "sampled gathered blocks")
-    # the end of the layer, through the last (possibly padded) shard
-    j_last = (N - 1) // s
-    lo = j_last * s
-    tail_ref = oracle.dequant_gather_layer([codes[j_last].cpu().numpy()],
-                                           [scales[j_last].cpu().numpy()], s, B, N - lo)
-    assert_bits_equal(out[lo:].cpu().numpy().view(np.uint16), tail_ref, "last shard")
+    hc = [c.cpu().numpy() for c in codes]
+    hs = [x.cpu().numpy() for x in scales]
+    with pool() as ex:
+        ref = list(ex.map(lambda j: oracle.dequant_gather_layer(
+            [hc[j]], [hs[j]], s, B, min(s, N - j * s)), range(P2)))
+    assert_bits_equal(out.cpu().numpy().view(np.uint16), np.concatenate(ref), "whole layer")
     assert not bool(((out & 0x7FFF) > 0x7F80).any()), "NaN in the gathered layer"
 
 
@@ -219,67 +218,56 @@ def test_fullsize_other_workloads(zpp, name):
     """The other rank-partition workloads, through the benchmark's pipeline
     (one stream, as timed): Llama-2-7B for 2 iterations, Falcon-40B for its
     10 iterations with fresh gradients each time and 60 layer gathers per
-    iteration over 2 stored layers.  The oracle follows the sampled elements' Adam state
-    through every iteration; the gathered layer is checked on sampled blocks
-    against the oracle's dequantization of the codes the gather read (the
-    peers' codes, drawn by the seeded generator) and, for the local shard,
-    by the round-trip bound."""
+    iteration over 2 stored layers.  The oracle follows the whole partition's
+    Adam state through every iteration; after the last, the quantized
+    secondary and the layer gathered last are compared whole, bit for bit,
+    with the oracle's quantization of the GPU's primary and its gather of the
+    shards that layer read."""
     wl = WORKLOADS[name]
     iters = wl.iterations if wl.iterations > 1 else 2
     hp = f32hp(wl.adam)
-    n, B, s = wl.n, wl.block, wl.shard_elems
+    n, B, s, N, P2 = wl.n, wl.block, wl.shard_elems, wl.layer_elems, wl.secondary_world
     pipe = PartitionPipeline(wl, streams=1)
     pipe.master.copy_(synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER))
     pipe.exp_avg.zero_()
     pipe.exp_avg_sq.zero_()
     for k, (pcodes, pscales) in enumerate(pipe.layer_peers):
-        for j in range(wl.secondary_world - 1):
+        for j in range(P2 - 1):
             pcodes[j].copy_(synth.device_random_codes(s, wl.cfg_id, rank=64 * k + j + 1))
             pscales[j].copy_(synth.device_random_scales(s // B, wl.cfg_id, rank=64 * k + j + 1))
-    idx = sample_indices(n, 1 << 18, 5)
-    p = host(pipe.master, idx, np.float32)
-    m = np.zeros_like(p)
-    v = np.zeros_like(p)
-    mt = MomentTolerance()
-    for t in range(1, iters + 1):
-        g = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, it=t)
-        pipe.grad.copy_(g)
-        gh = host(g, idx, np.float32)
-        del g
-        pipe.step()
-        pipe.wait()
-        got = tuple(host(tt, idx, d) for tt, d in ((pipe.master, np.float32),
+    with pool() as ex:
+        ref = ChunkedAdam(whole(pipe.master, np.float32), hp, ex)
+        for t in range(1, iters + 1):
+            g = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, it=t)
+            pipe.grad.copy_(g)
+            gh = whole(g, np.float32)
+            del g
+            pipe.step()
+            pipe.wait()
+            ref.step(gh)
+            del gh
+        ref.check(tuple(whole(tt, d) for tt, d in ((pipe.master, np.float32),
                                                    (pipe.exp_avg, np.float32),
                                                    (pipe.exp_avg_sq, np.float32),
-                                                   (pipe.primary, np.uint16)))
-        tau_m = mt.step((p, m, v), gh, hp)
-        p, m, v, b = oracle.adam_step(p, m, v, gh, step=t, **hp)
-        assert_adam_close(got, (p, m, v, b), hp["lr"], "%s iteration %d" % (name, t), steps=t,
-                          m_tau=tau_m)
-    assert torch.equal(pipe.secondary, pipe.primary)
-    # the layer gathered last in the step (of `layers_gathered`, cycling over
-    # the stored layers) is the one left in the output
-    k_last = (wl.layers_gathered - 1) % wl.distinct_layers
-    peer_codes, peer_scales = pipe.layer_peers[k_last]
-    # peers' part of the gathered layer: sampled whole blocks of each peer
-    rng = np.random.default_rng(6)
-    N = wl.layer_elems
-    for j in range(1, wl.secondary_world):
-        lo = j * s
-        valid = min(s, N - lo)
-        if valid <= 0:
-            continue
-        kb = np.unique(rng.integers(0, valid // B, size=64))
-        codes = np.concatenate([peer_codes[j - 1][k * B:(k + 1) * B].cpu().numpy() for k in kb])
-        scl = peer_scales[j - 1][torch.from_numpy(kb).cuda()].cpu().numpy()
-        ref = oracle.dequant_blockwise_i8(codes, scl, B)
-        eidx = torch.from_numpy((lo + kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
-        assert_bits_equal(host(pipe.out, eidx, np.uint16), ref, "%s peer %d" % (name, j))
-    # local shard: round trip of the primary within half a quantization step
-    lo = k_last * s
-    prim = (pipe.primary[lo:lo + s].to(torch.int32) << 16).view(torch.float32).to(torch.float64)
-    of = (pipe.out[:s].to(torch.int32) << 16).view(torch.float32).to(torch.float64)
-    sc = pipe.scales[lo // B:(lo + s) // B].to(torch.float64).repeat_interleave(B)
-    assert bool(((prim - of).abs() <= sc * (0.5 + 2.0 ** -15) + of.abs() * 2.0 ** -8).all())
+                                                   (pipe.primary, np.uint16))),
+                  "%s after %d iterations" % (name, iters))
+        del ref
+        assert torch.equal(pipe.secondary, pipe.primary)
+        prim = whole(pipe.primary, np.uint16)
+        codes, scales = whole(pipe.codes, np.int8), whole(pipe.scales, np.float32)
+        rc, rs = oracle_quantize_whole(prim, B, ex)
+        assert_bits_equal(codes, rc, "%s codes" % name)
+        assert_bits_equal(scales, rs, "%s scales" % name)
+        # the layer gathered last in the step (of `layers_gathered`, cycling
+        # over the stored layers) is the one left in the output; its local
+        # shard is codes [k s, (k+1) s) of this rank's quantized secondary
+        k_last = (wl.layers_gathered - 1) % wl.distinct_layers
+        peer_codes, peer_scales = pipe.layer_peers[k_last]
+        shard_c = [codes[k_last * s:(k_last + 1) * s]] + [whole(c, np.int8) for c in peer_codes]
+        shard_s = ([scales[k_last * s // B:(k_last + 1) * s // B]]
+                   + [whole(x, np.float32) for x in peer_scales])
+        ref = list(ex.map(lambda j: oracle.dequant_gather_layer(
+            [shard_c[j]], [shard_s[j]], s, B, min(s, N - j * s)), range(P2)))
+    assert_bits_equal(whole(pipe.out, np.uint16), np.concatenate(ref), "%s layer" % name)
     del pipe
     torch.cuda.empty_cache()

@@ -25,7 +25,7 @@ import torch
 import oracle
 from paper_2407_01614_amd.pipeline import PartitionPipeline
 from paper_2407_01614_amd.workloads import WORKLOADS
-from parity import assert_adam_close, assert_bits_equal
+from parity import ChunkedAdam, assert_bits_equal
 
 pytestmark = pytest.mark.gpu
 
@@ -81,17 +81,11 @@ def test_whole_arrays_one_step_llama2_13b(zpp, fused):
     pool = ThreadPoolExecutor(threads())
     try:
         # Adam over the whole partition
-        rs = ranges(n, 4 * threads(), B)
-
-        def adam(r):
-            z = np.zeros(r[1] - r[0], np.float32)
-            return oracle.adam_step(p0[r[0]:r[1]], z, z, g[r[0]:r[1]], step=1, **hp)
-
-        res = list(pool.map(adam, rs))
-        ref = tuple(np.concatenate([x[k] for x in res]) for k in range(4))
-        del res
-        assert_adam_close((got_p, got_m, got_v, got_b), ref, hp["lr"], "whole partition")
+        ref = ChunkedAdam(p0, hp, pool)
+        ref.step(g)
+        ref.check((got_p, got_m, got_v, got_b), "whole partition")
         del ref
+        rs = ranges(n, 4 * threads(), B)
         # refresh
         assert_bits_equal(got_sec, got_b, "secondary = primary")
         # quantization of the GPU's own secondary, block by block
