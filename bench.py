@@ -17,8 +17,9 @@ streams ordered by events (with and without one step's gather overlapping the
 next step's Adam), the fused step + refresh + quantize kernel in place of the
 three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
-timing only), the qgZ gradient side, the step preceded by the qgZ receive,
-and, for context, PyTorch's fused AdamW on a partition of the same size.  The
+timing only), the qgZ gradient side, the step preceded by the qgZ receive
+(as its own kernel, and fused into the partition step), and, for context,
+PyTorch's fused AdamW on a partition of the same size.  The
 CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
 
@@ -386,8 +387,13 @@ def main():
         del g
     torch.cuda.synchronize()
     qgz_ms, qgz_times, qgz_kb, qgz_step_bytes = run(False, "event", True)
-    pipe.exchange = None
     qgz_gbps = qgz_step_bytes / (qgz_ms * 1e-3) / 1e9
+    # the same, with the receive fused into the partition step
+    pipe.fuse_receive = True
+    fr_ms, fr_times, fr_kb, fr_step_bytes = run(False, "event", True)
+    fr_gbps = fr_step_bytes / (fr_ms * 1e-3) / 1e9
+    pipe.fuse_receive = False
+    pipe.exchange = None
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = kernel_table(kb, times)
     fused_kernels = kernel_table(fused_kb, fused_times)
@@ -446,6 +452,10 @@ def main():
             "ms_per_step": round(qgz_ms, 4), "GB/s": round(qgz_gbps, 1),
             "frac_of_peak": round(qgz_gbps / HBM_PEAK_GBPS, 4),
             "kernels": kernel_table(qgz_kb, qgz_times)},
+        "step_with_fused_qgz_receive": {
+            "ms_per_step": round(fr_ms, 4), "GB/s": round(fr_gbps, 1),
+            "frac_of_peak": round(fr_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(fr_kb, fr_times)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
         "gpu": {"name": torch.cuda.get_device_name(0),
                 "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,

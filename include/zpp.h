@@ -228,6 +228,39 @@ ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
                                          hipStream_t stream, const hipEvent_t *wait_events,
                                          uint32_t num_wait, hipEvent_t done_after);
 
+/* qgZ receive fused into the partition step: the rank's optimizer step takes
+ * its gradient straight from the num_src int4 copies of its partition that
+ * the exchange replacing the ReduceScatter delivered (Background section:
+ * qgZ; Algorithm 1, backward loop and the closing optimizer.step()).
+ * Results are bit for bit those of zpp_dequant_reduce_i4(src_codes,
+ * src_scales, num_src, n, block, scale_out, g) into an fp32 buffer g
+ * followed by zpp_adam_partition_step(master, exp_avg, exp_avg_sq, g,
+ * primary_bf16, n, hp), without the buffer: for every i < n
+ *     acc = 0;  for q in 0..num_src-1: acc = fma(code_q[i], scale_q[i/block], acc)
+ *     g = acc * scale_out;  then the Adam(W) update of zpp_adam_partition_step
+ * at 26 B + num_src * (0.5 B + 4/block B) of HBM traffic per element instead
+ * of 30 B + num_src * (0.5 B + 4/block B) + 4 B + 4 B.
+ * master, exp_avg, exp_avg_sq: float[n] in place.  src_codes, src_scales:
+ * HOST arrays of num_src DEVICE pointers (uint8_t[ceil(n/2)], packed as
+ * zpp_quantize_blockwise_i4 writes them, and float[ceil(n/block)] each),
+ * read during the call only; num_src in [1, ZPP_MAX_SHARDS].  block: a power
+ * of two in [64, 4096].  scale_out finite (1/num_src for the data-parallel
+ * mean).  primary_bf16: uint16_t[n] out.  hp as for zpp_adam_partition_step.
+ * Order on `stream`: wait for every event of wait_events[0..num_wait) (the
+ * exchange that delivered the sources), step, record `done_after`.
+ * No two of the four outputs may overlap, nor any output a source range
+ * (ZPP_EOVERLAP).  Alignment: floats and scales 4, bf16 2 bytes
+ * (ZPP_EALIGN); 16-byte state arrays, an 8-byte primary and 2-byte codes
+ * select the vector kernel. */
+ZPP_API zpp_status zpp_qgz_receive_adam_step(float *master, float *exp_avg, float *exp_avg_sq,
+                                             const uint8_t *const *src_codes,
+                                             const float *const *src_scales, uint32_t num_src,
+                                             uint32_t block, float scale_out,
+                                             uint16_t *primary_bf16, size_t n,
+                                             const zpp_adam_hparams *hp, hipStream_t stream,
+                                             const hipEvent_t *wait_events, uint32_t num_wait,
+                                             hipEvent_t done_after);
+
 /* Static, NUL-terminated description of a status code. */
 ZPP_API const char *zpp_status_string(zpp_status s);
 

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzpp.so")
 
 SOURCES = ["zpp_api.hip", "adam.hip", "refresh.hip", "quant.hip", "gather.hip", "fused.hip",
-           "qgz.hip"]
+           "qgz.hip", "receive_adam.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

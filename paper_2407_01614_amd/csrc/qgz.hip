@@ -193,10 +193,6 @@ struct ReduceArgs {
     float *out;
 };
 
-__device__ __forceinline__ float i4_code(uint32_t w, int e) {
-    return (float)((int32_t)(w << (28 - 4 * e)) >> 28);
-}
-
 // A lane holds G groups of 4 consecutive elements; group t of lane l in a
 // wave's tile starts at 256 t + 4 l, so each source is read as 128-byte
 // contiguous wave loads (2 bytes per lane) and every store of the wave

@@ -40,7 +40,7 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // once (the optimizer step: four arrays read, four written) run faster with
 // fewer workgroups resident per CU than the hardware would otherwise place:
 // too many waves in flight oversubscribe the memory channels.  The optimizer
-// step, the fused step and the gather use it.  A launch caps
+// step, the fused step, the step with the qgZ receive and the gather use it.  A launch caps
 // residency by reserving dynamic LDS that its kernel never touches: a CU then
 // holds at most kLdsPerCU / residency_lds(k) = k such workgroups, and the
 // dispatcher still hands out the one-shot grid as workgroups retire.

@@ -56,4 +56,12 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
                                     uint32_t block, float scale_out, float *out,
                                     bool vector_path, hipStream_t stream);
 
+// The qgZ receive fused into the partition step: the gradient of every
+// element is the dequantize-and-reduce of the num_src int4 sources (times
+// scale_out), fed straight into the Adam update of p, m, v and the bf16 out.
+hipError_t launch_receive_adam(float *p, float *m, float *v, const uint8_t *const *src_codes,
+                               const float *const *src_scales, uint32_t num_src, uint32_t block,
+                               float scale_out, uint16_t *out, size_t n, const AdamConsts &c,
+                               bool vector_path, hipStream_t stream);
+
 }  // namespace zpp

@@ -1,5 +1,6 @@
-// Device-side pieces of the blockwise int8 quantization shared by the
-// quantize kernel and the fused optimizer-step epilogue.
+// Device-side pieces of the blockwise quantization shared by the kernels: the
+// int8 decisions of the quantize kernel and the fused optimizer-step
+// epilogue, and the int4 decode of the qgZ receive.
 #pragma once
 
 #include "zpp_device.h"
@@ -80,6 +81,13 @@ __device__ __forceinline__ uint32_t quant_word(uint32_t w0, uint32_t w1, const B
 // max of the |x| bit patterns of the two bf16 in a word
 __device__ __forceinline__ u16x2 absbits2(uint32_t w) {
     return __builtin_bit_cast(u16x2, w & 0x7FFF7FFFu);
+}
+
+// int4 code e (4-bit two's complement, nibble e of w, e = 0 the lowest) as a
+// float; shared by the qgZ dequantize-and-reduce and the receive fused into
+// the partition step, which must form the same gradient.
+__device__ __forceinline__ float i4_code(uint32_t w, int e) {
+    return (float)((int32_t)(w << (28 - 4 * e)) >> 28);
 }
 
 }  // namespace zpp

@@ -37,7 +37,7 @@ import torch
 from . import synth
 from . import zpp
 from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_gather, bytes_quant,
-                        bytes_reduce_i4)
+                        bytes_receive_adam, bytes_reduce_i4)
 
 
 SYNC_MODES = ("event", "host", "none")
@@ -51,10 +51,14 @@ class PartitionPipeline:
     fix as a host-side wait) or "none" (stock hpZ: no edge at all; the gather
     may read codes that are not written yet, so only its timing means
     anything).  `streams=1` runs every kernel on the compute stream in path
-    order; `sync` and `overlap` do not apply there."""
+    order; `sync` and `overlap` do not apply there.  `qgz_sources` > 0 opens
+    every step with the qgZ receive of that many int4 gradient copies, as its
+    own dequantize-and-reduce kernel writing `grad`, or, with `fuse_receive`,
+    inside the partition step (`zpp_qgz_receive_adam_step`, no `grad`
+    written; separate kernels only)."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
-                 qgz_sources=0, streams=3):
+                 qgz_sources=0, streams=3, fuse_receive=False):
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         if streams not in (1, 3):
@@ -65,6 +69,7 @@ class PartitionPipeline:
         self.sync = sync
         self.overlap = overlap
         self.streams = streams
+        self.fuse_receive = fuse_receive
         # with qgz_sources > 0 every step starts with the qgZ receive: the mean
         # of that many int4 copies of this partition's gradient becomes `grad`
         self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device)
@@ -183,10 +188,7 @@ class PartitionPipeline:
     def enable_timing(self):
         """Record a HIP timing-event pair around every kernel, on the stream
         that kernel runs on."""
-        names = ("fused", "gather") if self.fused else ("adam", "refresh", "quant", "gather")
-        if self.exchange is not None:
-            names = ("reduce_i4",) + names
-        self.timing = {k: [] for k in names}
+        self.timing = {k: [] for k in self.kernel_bytes()}
 
     def _timed(self, name, stream, fn):
         if self.timing is None:
@@ -226,7 +228,7 @@ class PartitionPipeline:
                 zpp.stream_wait(self.compute, self.ev_gather)
             else:
                 zpp.stream_wait(self.compute, self.ev_refresh)
-        if self.exchange is not None:
+        if self._receive_apart():
             self._timed("reduce_i4", self.compute,
                         lambda: self.exchange.reduce(self.grad, stream=self.compute))
         if self.fused:
@@ -235,9 +237,7 @@ class PartitionPipeline:
                 self.secondary, self.codes, self.scales, step=t, block=B, stream=self.compute,
                 done_after=self.ev_quant, **wl.adam))
         else:
-            self._timed("adam", self.compute, lambda: zpp.adam_partition_step(
-                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
-                stream=self.compute, **wl.adam))
+            self._partition_step(t, self.compute)
             self.ev_primary.record(self.compute)
             zpp.stream_wait(self.copy, self.ev_primary)
             self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
@@ -273,7 +273,7 @@ class PartitionPipeline:
             # work (the quantization, then the gather) into this stream
             zpp.stream_wait(cs, self.ev_quant)
             zpp.stream_wait(cs, self.ev_gather)
-        if self.exchange is not None:
+        if self._receive_apart():
             self._timed("reduce_i4", cs, lambda: self.exchange.reduce(self.grad, stream=cs))
         if self.fused:
             self._timed("fused", cs, lambda: zpp.adam_step_refresh_quantize(
@@ -281,14 +281,34 @@ class PartitionPipeline:
                 self.secondary, self.codes, self.scales, step=t, block=B, stream=cs,
                 **wl.adam))
         else:
-            self._timed("adam", cs, lambda: zpp.adam_partition_step(
-                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
-                stream=cs, **wl.adam))
+            self._partition_step(t, cs)
             self._timed("refresh", cs, lambda: zpp.refresh_secondary(
                 self.secondary, self.primary, n, stream=cs))
             self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
                 self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
         self._gathers(cs)
+
+    def _receive_fused(self):
+        if self.fuse_receive and self.fused:
+            raise ValueError("the receive fuses into the separate partition step only")
+        return self.exchange is not None and self.fuse_receive
+
+    def _receive_apart(self):
+        return self.exchange is not None and not self._receive_fused()
+
+    def _partition_step(self, t, stream):
+        """The Adam step of the separate-kernel path: from `grad`, or with the
+        qgZ receive fused in, from the int4 copies of the gradient."""
+        wl = self.wl
+        if self._receive_fused():
+            ex = self.exchange
+            self._timed("receive_adam", stream, lambda: zpp.qgz_receive_adam_step(
+                self.master, self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales, self.primary,
+                step=t, block=ex.block, scale_out=1.0 / ex.num_src, stream=stream, **wl.adam))
+        else:
+            self._timed("adam", stream, lambda: zpp.adam_partition_step(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
+                stream=stream, **wl.adam))
 
     def wait(self):
         """Block the host until every stream of the pipeline is idle."""
@@ -311,13 +331,16 @@ class PartitionPipeline:
         wl = self.wl
         gather = float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems, wl.block))
         out = {}
-        if self.exchange is not None:
+        if self._receive_apart():
             out["reduce_i4"] = float(bytes_reduce_i4(wl.n, self.exchange.num_src, wl.block))
         if self.fused:
             out.update({"fused": float(bytes_fused(wl.n, wl.block)), "gather": gather})
             return out
+        if self._receive_fused():
+            out["receive_adam"] = float(bytes_receive_adam(wl.n, self.exchange.num_src, wl.block))
+        else:
+            out["adam"] = BYTES_ADAM * wl.n
         out.update({
-            "adam": BYTES_ADAM * wl.n,
             "refresh": BYTES_REFRESH * wl.n,
             "quant": float(bytes_quant(wl.n, wl.block)),
             "gather": gather,

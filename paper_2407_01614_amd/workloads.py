@@ -129,3 +129,9 @@ def bytes_quant_i4(n, block=BLOCK):
 def bytes_reduce_i4(n, num_src, block=BLOCK):
     # read every source's packed codes and scales, write the fp32 result
     return num_src * ((n + 1) // 2 + 4 * ((n + block - 1) // block)) + 4 * n
+
+
+def bytes_receive_adam(n, num_src, block=BLOCK):
+    # the partition step without its gradient read (26 B: p, m, v in and out,
+    # bf16 out) plus every source's packed codes and scales
+    return 26 * n + num_src * ((n + 1) // 2 + 4 * ((n + block - 1) // block))

@@ -52,6 +52,9 @@ _lib.zpp_quantize_blockwise_i4.argtypes = [_P, _sz, _u32, _P, _P, _P, _P, _P]
 _lib.zpp_dequant_reduce_i4.restype = ctypes.c_int
 _lib.zpp_dequant_reduce_i4.argtypes = [_P, _P, _u32, _sz, _u32, ctypes.c_float, _P, _P, _P, _u32,
                                        _P]
+_lib.zpp_qgz_receive_adam_step.restype = ctypes.c_int
+_lib.zpp_qgz_receive_adam_step.argtypes = [_P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P,
+                                           _sz, ctypes.POINTER(AdamHParams), _P, _P, _u32, _P]
 _lib.zpp_status_string.restype = ctypes.c_char_p
 _lib.zpp_status_string.argtypes = [ctypes.c_int]
 _lib.zpp_last_hip_error.restype = ctypes.c_int
@@ -59,7 +62,8 @@ _lib.zpp_last_hip_error.argtypes = []
 
 EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
            "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
-           "zpp_dequant_reduce_i4", "zpp_status_string", "zpp_last_hip_error")
+           "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step", "zpp_status_string",
+           "zpp_last_hip_error")
 
 
 class ZppError(RuntimeError):
@@ -350,6 +354,39 @@ def dequant_reduce_i4(src_codes, src_scales, n, out, *, block=256, scale_out=1.0
                                     stream_handle(stream), warr, len(waits),
                                     _event_handle(done_after))
     _check(st, "zpp_dequant_reduce_i4")
+
+
+def qgz_receive_adam_step(master, exp_avg, exp_avg_sq, src_codes, src_scales, primary_bf16, *,
+                          lr, beta1, beta2, eps, weight_decay, step, adamw=True, block=256,
+                          scale_out=1.0, n=None, stream=None, wait_events=(), done_after=None):
+    """zpp_qgz_receive_adam_step: the partition step with its gradient taken
+    from len(src_codes) int4 copies (the mean when scale_out = 1/len)."""
+    for t, name in ((master, "master"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq")):
+        _dev(t, _F32, name)
+    _dev(primary_bf16, _BF16, "primary_bf16")
+    k = len(src_codes)
+    if k != len(src_scales) or not 1 <= k <= MAX_SHARDS:
+        raise ValueError("1..%d sources, one scales tensor each" % MAX_SHARDS)
+    if n is None:
+        n = master.numel()
+    for q in range(k):
+        _dev(src_codes[q], _U8, "src_codes[%d]" % q)
+        _dev(src_scales[q], _F32, "src_scales[%d]" % q)
+        if src_codes[q].numel() < (n + 1) // 2 or src_scales[q].numel() < num_blocks(n, block):
+            raise ValueError("source %d buffers too small" % q)
+    if any(t.numel() < n for t in (master, exp_avg, exp_avg_sq, primary_bf16)):
+        raise ValueError("a buffer holds fewer than n elements")
+    cptrs = (_P * k)(*[c.data_ptr() for c in src_codes])
+    sptrs = (_P * k)(*[x.data_ptr() for x in src_scales])
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    hp = AdamHParams(lr, beta1, beta2, eps, weight_decay, 1 if adamw else 0, int(step))
+    st = _lib.zpp_qgz_receive_adam_step(master.data_ptr(), exp_avg.data_ptr(),
+                                        exp_avg_sq.data_ptr(), cptrs, sptrs, k, block, scale_out,
+                                        primary_bf16.data_ptr(), n, ctypes.byref(hp),
+                                        stream_handle(stream), warr, len(waits),
+                                        _event_handle(done_after))
+    _check(st, "zpp_qgz_receive_adam_step")
 
 
 # --------------------------------------------------------------------------

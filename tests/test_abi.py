@@ -35,8 +35,8 @@ def test_header_declares_the_four_calls():
     names = declared_functions()
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
                "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
-               "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_status_string",
-               "zpp_last_hip_error"):
+               "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
+               "zpp_status_string", "zpp_last_hip_error"):
         assert fn in names
 
 
@@ -240,6 +240,44 @@ def test_dequant_reduce_i4_validation(zpp):
     assert reduce_i4(zpp, cs, ss, out=D + 8) == zpp.ZPP_EOVERLAP
     assert reduce_i4(zpp, cs, ss, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
     assert reduce_i4(zpp, [A] * 65, [C] * 65) == zpp.ZPP_EINVAL
+
+
+def receive(zpp, state=(A, B, C, E), codes=(F, G), scales=(H, H + 0x1000), n=1024, block=256,
+            scale_out=0.5, h=None, waits=None, nwait=0, num=None):
+    P = ctypes.c_void_p
+    k = len(codes) if num is None else num
+    carr = (P * len(codes))(*codes)
+    sarr = (P * len(scales))(*scales)
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_qgz_receive_adam_step(state[0], state[1], state[2], carr, sarr, k, block,
+                                             scale_out, state[3], n,
+                                             ctypes.byref(h) if h is not False else None, None,
+                                             warr, nwait, None)
+
+
+def test_qgz_receive_adam_validation(zpp):
+    assert receive(zpp, n=0, state=(None, None, None, None)) == zpp.ZPP_OK
+    assert receive(zpp, h=False) == zpp.ZPP_EINVAL
+    assert receive(zpp, h=hp(zpp, step=0)) == zpp.ZPP_EINVAL
+    assert receive(zpp, h=hp(zpp, beta2=1.0)) == zpp.ZPP_EINVAL
+    assert receive(zpp, block=96) == zpp.ZPP_EINVAL
+    assert receive(zpp, block=8192) == zpp.ZPP_EINVAL
+    assert receive(zpp, scale_out=float("nan")) == zpp.ZPP_EINVAL
+    assert receive(zpp, num=0) == zpp.ZPP_EINVAL
+    assert receive(zpp, codes=[F] * 65, scales=[H] * 65) == zpp.ZPP_EINVAL
+    assert receive(zpp, codes=(F, None)) == zpp.ZPP_EINVAL
+    assert receive(zpp, scales=(H, H + 2)) == zpp.ZPP_EALIGN
+    assert receive(zpp, state=(A, None, C, E)) == zpp.ZPP_EINVAL
+    assert receive(zpp, state=(A + 2, B, C, E)) == zpp.ZPP_EALIGN
+    assert receive(zpp, state=(A, B, C, E + 1)) == zpp.ZPP_EALIGN
+    assert receive(zpp, state=(A, B, C, A + 64)) == zpp.ZPP_EOVERLAP   # primary in master
+    assert receive(zpp, state=(A, A + 4092, C, E)) == zpp.ZPP_EOVERLAP  # moments in master
+    assert receive(zpp, codes=(F, A + 16)) == zpp.ZPP_EOVERLAP         # a source in master
+    assert receive(zpp, scales=(H, E + 8)) == zpp.ZPP_EOVERLAP         # a scale in primary
+    assert receive(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
+    assert receive(zpp, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
+    assert receive(zpp, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
 
 
 def test_no_oracle_in_product_path():

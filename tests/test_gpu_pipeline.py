@@ -434,3 +434,43 @@ def test_pipeline_with_qgz_receive(zpp):
     got = (to_host(pipe.master, np.float32), to_host(pipe.exp_avg, np.float32),
            to_host(pipe.exp_avg_sq, np.float32), to_host(pipe.primary, np.uint16))
     assert_adam_close(got, r2, hp["lr"], "after 2 steps", steps=2, m_tau=tau_m)
+
+
+@pytest.mark.parametrize("streams", [1, 3])
+def test_pipeline_fused_receive_equals_separate(zpp, streams):
+    """The qgZ receive fused into the partition step (no gradient buffer
+    written) leaves the pipeline in the same state as the separate
+    dequantize-and-reduce followed by the step, bit for bit, over two steps,
+    and its timed kernels are the fused one and the rest of the path."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small-qgz-fused", cfg_id=14, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
+                  secondary_world=4, world=4)
+    P = 8
+    quants = [oracle.quantize_blockwise_i4(synth.gradients(wl.n, wl.cfg_id, q), wl.block)
+              for q in range(P)]
+    peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
+                                          wl.block) for j in range(wl.secondary_world - 1)]
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    results = []
+    for fuse in (False, True):
+        pipe = PartitionPipeline(wl, qgz_sources=P, streams=streams, fuse_receive=fuse)
+        pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
+        for q, (c, sc) in enumerate(quants):
+            pipe.exchange.codes[q].copy_(torch.from_numpy(c))
+            pipe.exchange.scales[q].copy_(torch.from_numpy(sc))
+        torch.cuda.synchronize()
+        pipe.step()
+        pipe.enable_timing()
+        pipe.step()
+        pipe.wait()
+        names = set(pipe.kernel_times_ms())
+        assert names == ({"receive_adam", "refresh", "quant", "gather"} if fuse
+                         else {"reduce_i4", "adam", "refresh", "quant", "gather"})
+        results.append([t.cpu().numpy().copy() for t in (pipe.master, pipe.exp_avg,
+                                                         pipe.exp_avg_sq, pipe.primary,
+                                                         pipe.secondary, pipe.codes, pipe.scales,
+                                                         pipe.out)])
+        del pipe
+    for i, (a, b) in enumerate(zip(*results)):
+        assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)

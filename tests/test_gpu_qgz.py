@@ -1,5 +1,6 @@
-"""GPU parity of the qgZ gradient side (int4 quantization and the
-dequantize-and-reduce) against the CPU oracle, through the C ABI."""
+"""GPU parity of the qgZ gradient side (int4 quantization, the
+dequantize-and-reduce, and the receive fused into the partition step)
+against the CPU oracle and the unfused sequence, through the C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -7,7 +8,8 @@ import torch
 import oracle
 from paper_2407_01614_amd import synth
 from paper_2407_01614_amd.workloads import WORKLOADS
-from parity import assert_bits_equal, empty_dev, to_dev, to_host
+from parity import (assert_adam_close, assert_bits_equal, empty_dev, first_moment_scale,
+                    to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -198,3 +200,166 @@ def test_fullsize_qgz_partition(zpp):
         assert_bits_equal(codes[q][lo // 2:].cpu().numpy(), rt[q][0], "tail codes %d" % q)
     reft = oracle.dequant_reduce_i4([c for c, _ in rt], [s for _, s in rt], n - lo, block, 0.125)
     assert_bits_equal(out[lo:].cpu().numpy(), reft, "tail mean")
+
+
+# --------------------------------------------------------------------------
+# The qgZ receive fused into the partition step
+# --------------------------------------------------------------------------
+def f32hp(hp):
+    return {k: float(np.float32(v)) for k, v in hp.items()}
+
+
+HP = f32hp(dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1))
+HP_LOUD = f32hp(dict(lr=1e-2, beta1=0.8, beta2=0.9, eps=1e-6, weight_decay=0.5))
+
+
+def receive_state(n, cfg, pad=0, moments=False):
+    """Device master / moments / primary (viewed `pad` elements in) for a
+    receive step; nonzero moments when `moments`, as after a few steps."""
+    p = synth.master_weights(n, cfg)
+    m, v = synth.moments(n, cfg) if moments else (np.zeros(n, np.float32),) * 2
+    return (to_dev(p, pad=pad), to_dev(m, pad=pad), to_dev(v, pad=pad),
+            empty_dev(n, np.uint16, pad=pad, fill=0x5A5A)), (p, m, v)
+
+
+def run_two_kernels(zpp, quants, n, block, scale_out, state, step, hp, adamw):
+    """The reference sequence on the GPU: dequantize-and-reduce into a
+    gradient buffer, then the partition step from it."""
+    codes = [u8_dev(c) for c, _ in quants]
+    scales = [to_dev(s) for _, s in quants]
+    g = empty_dev(n, np.float32, fill=-7.0)
+    zpp.dequant_reduce_i4(codes, scales, n, g, block=block, scale_out=scale_out)
+    p, m, v, b = state
+    zpp.adam_partition_step(p, m, v, g, b, step=step, adamw=adamw, **hp)
+    torch.cuda.synchronize()
+    return to_host(g, np.float32)
+
+
+def run_receive(zpp, quants, n, block, scale_out, state, step, hp, adamw, pad_codes=0):
+    codes = [u8_dev(c, pad=pad_codes) for c, _ in quants]
+    scales = [to_dev(s) for _, s in quants]
+    p, m, v, b = state
+    zpp.qgz_receive_adam_step(p, m, v, codes, scales, b, step=step, adamw=adamw, block=block,
+                              scale_out=scale_out, **hp)
+    torch.cuda.synchronize()
+
+
+def host_state(state):
+    p, m, v, b = state
+    return (to_host(p, np.float32), to_host(m, np.float32), to_host(v, np.float32),
+            to_host(b, np.uint16))
+
+
+# (hyperparameters, moments before the step, step, AdamW or L2): the
+# workload's from zero moments at step 1, and exaggerated ones (decay and eps
+# visible) from random moments at step 3, as in the partition-step tests
+REGIMES = {"workload": (HP, False, 1, True), "loud-adamw": (HP_LOUD, True, 3, True),
+           "loud-l2": (HP_LOUD, True, 3, False)}
+
+
+@pytest.mark.parametrize("P,n,block", [
+    (1, 1, 256), (8, 7, 256), (8, 256, 256), (8, 256 * 9 + 81, 256), (3, 65536 + 8, 64),
+    (8, 100001, 128), (5, 256 * 33, 1024), (8, 1 << 18, 4096), (64, 256 * 5 + 3, 256),
+    (9, 256 * 40, 512)])
+@pytest.mark.parametrize("regime", sorted(REGIMES))
+def test_receive_adam_equals_reduce_then_step(zpp, P, n, block, regime):
+    """Bit for bit the dequantize-and-reduce followed by the partition step
+    (both on the GPU, from the same state), and within the Adam bar of the
+    oracle's two functions in sequence."""
+    hp, moments, step, adamw = REGIMES[regime]
+    quants = oracle_sources(P, n, block, 90 + P + n)
+    scale_out = float(np.float32(1.0 / P))
+    ref_state, host0 = receive_state(n, 91, moments=moments)
+    got_state, _ = receive_state(n, 91, moments=moments)
+    g = run_two_kernels(zpp, quants, n, block, scale_out, ref_state, step, hp, adamw)
+    run_receive(zpp, quants, n, block, scale_out, got_state, step, hp, adamw)
+    got, ref = host_state(got_state), host_state(ref_state)
+    for i, name in enumerate(("master", "exp_avg", "exp_avg_sq", "primary")):
+        assert_bits_equal(got[i], ref[i], "%s P=%d n=%d block=%d" % (name, P, n, block))
+    rg = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
+                                  scale_out)
+    assert_bits_equal(g, rg, "reduced gradient")
+    p, m, v = host0
+    r = oracle.adam_step(p, m, v, rg, step=step, adamw=adamw, **hp)
+    tau_m = first_moment_scale((p, m, v), rg, hp, adamw)
+    assert_adam_close(got, r, hp["lr"], "receive step vs oracle", m_tau=tau_m)
+
+
+@pytest.mark.parametrize("pads", [(1, 0), (0, 1), (3, 1)], ids=["state", "codes", "both"])
+def test_receive_adam_misaligned(zpp, pads):
+    """Misaligned state or codes take the any-alignment kernel: still the
+    two-kernel sequence bit for bit."""
+    n, block, P = 256 * 11 + 5, 128, 5
+    quants = oracle_sources(P, n, block, 92)
+    ref_state, _ = receive_state(n, 93)
+    got_state, _ = receive_state(n, 93, pad=pads[0])
+    run_two_kernels(zpp, quants, n, block, 0.2, ref_state, 1, HP, True)
+    run_receive(zpp, quants, n, block, 0.2, got_state, 1, HP, True, pad_codes=pads[1])
+    for a, b in zip(host_state(got_state), host_state(ref_state)):
+        assert_bits_equal(a, b, "misaligned %s" % (pads,))
+
+
+def test_receive_adam_special_scales(zpp):
+    """NaN, Inf, zero and subnormal source scales reach the update as the
+    reduce forms them."""
+    n, block, P = 256 * 8, 256, 4
+    quants = oracle_sources(P, n, block, 94)
+    quants[1][1][2] = np.nan
+    quants[2][1][3] = np.inf
+    quants[3][1][4] = 0.0
+    quants[0][1][5] = 1e-40
+    ref_state, _ = receive_state(n, 95)
+    got_state, _ = receive_state(n, 95)
+    run_two_kernels(zpp, quants, n, block, 1.0, ref_state, 1, HP, True)
+    run_receive(zpp, quants, n, block, 1.0, got_state, 1, HP, True)
+    for a, b in zip(host_state(got_state), host_state(ref_state)):
+        assert_bits_equal(a, b, "special scales")
+
+
+def test_fullsize_receive_adam(zpp):
+    """The Llama-2-13B partition from 8 int4 sources, in the configuration the
+    benchmark times: the whole state after the fused receive equals the
+    reduce-then-step sequence (compared on the device), and the whole
+    gradient the sequence formed equals the oracle's."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    wl = WORKLOADS["llama-2-13b"]
+    n, block, P = wl.n, wl.block, 8
+    nb = (n + block - 1) // block
+    hp = f32hp(wl.adam)
+    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
+    for q in range(P):
+        src = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, rank=q)
+        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=block)
+        torch.cuda.synchronize()
+        del src
+    p0 = synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER)
+    states = []
+    for _ in range(2):
+        states.append((p0.clone(), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda"),
+                       torch.empty(n, dtype=torch.int16, device="cuda")))
+    g = torch.empty(n, dtype=torch.float32, device="cuda")
+    zpp.dequant_reduce_i4(codes, scales, n, g, block=block, scale_out=1.0 / P)
+    p, m, v, b = states[0]
+    zpp.adam_partition_step(p, m, v, g, b, step=1, **hp)
+    p, m, v, b = states[1]
+    zpp.qgz_receive_adam_step(p, m, v, codes, scales, b, step=1, block=block, scale_out=1.0 / P,
+                              **hp)
+    torch.cuda.synchronize()
+    for a, r, name in zip(states[1], states[0], ("master", "exp_avg", "exp_avg_sq", "primary")):
+        assert torch.equal(a.view(torch.int32) if a.dtype == torch.float32 else a,
+                           r.view(torch.int32) if r.dtype == torch.float32 else r), name
+    hc = [c.cpu().numpy() for c in codes]
+    hs = [x.cpu().numpy() for x in scales]
+    step = -(-n // 64) // block * block
+    try:
+        k = len(os.sched_getaffinity(0))
+    except AttributeError:
+        k = os.cpu_count() or 1
+    with ThreadPoolExecutor(max(1, min(16, k))) as ex:
+        parts = list(ex.map(lambda a: oracle.dequant_reduce_i4(
+            [c[a // 2:(a + step) // 2 + 1] for c in hc],
+            [x[a // block:-(-(a + step) // block)] for x in hs],
+            min(step, n - a), block, float(np.float32(1.0 / P))), range(0, n, step)))
+    assert_bits_equal(g.cpu().numpy(), np.concatenate(parts), "whole gradient")
