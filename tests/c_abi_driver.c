@@ -6,8 +6,10 @@
  * quantization -> dequantize-and-gather of the layer over P' shards), with
  * the gather ordered after the quantization by an event (the fix).  The
  * results are checked against the CPU oracle (liboracle.so), which runs the
- * same iteration on the same inputs on its own.  Also checks a few
- * validation errors of the ABI.
+ * same iteration on the same inputs on its own.  Then the qgZ receive fused
+ * into the partition step (zpp_qgz_receive_adam_step) from int4 gradient
+ * copies, against the dequantize-and-reduce followed by the step and against
+ * the oracle.  Also checks a few validation errors of the ABI.
  *
  * Test infrastructure: built by the repository's build step, run by
  * tests/test_gpu_c_abi.py.  Prints "c abi ok" and exits 0 on success.
@@ -34,6 +36,11 @@ void orc_quantize_blockwise_i8(const uint16_t *x, size_t n, uint32_t block, int8
 void orc_dequant_gather_layer(const int8_t *const *shard_codes, const float *const *shard_scales,
                               uint32_t num_shards, size_t shard_elems, uint32_t block,
                               size_t layer_elems, uint16_t *out);
+void orc_quantize_blockwise_i4(const float *x, size_t n, uint32_t block, uint8_t *codes,
+                               float *scales);
+void orc_dequant_reduce_i4(const uint8_t *const *src_codes, const float *const *src_scales,
+                           uint32_t num_src, size_t n, uint32_t block, float scale_out,
+                           float *out);
 
 #define B 256u
 #define P2 4u
@@ -93,6 +100,98 @@ static double rel_err(double got, double ref, double floor_)
         return 0.0;
     const double d = fabs(ref) > floor_ ? fabs(ref) : floor_;
     return fabs(got - ref) / d;
+}
+
+#define NSRC 4u
+
+/* The qgZ receive fused into the partition step, from plain C: NSRC int4
+ * copies of a gradient (quantized by the oracle, as the senders would),
+ * uploaded on their own stream; the fused call waits on the upload's event.
+ * Its state must equal, bit for bit, that of the dequantize-and-reduce
+ * followed by the partition step, and match the oracle's. */
+static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
+{
+    const size_t nb = (n + B - 1) / B, nbytes = (n + 1) / 2;
+    const float scale_out = 1.0f / NSRC;
+    float *x = malloc(n * 4);
+    uint8_t *hc[NSRC];
+    float *hs[NSRC];
+    const uint8_t *dc[NSRC];
+    const float *ds[NSRC];
+    hipStream_t up, st;
+    HIP_OK(hipStreamCreateWithFlags(&up, hipStreamNonBlocking));
+    HIP_OK(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    for (unsigned q = 0; q < NSRC; q++) {
+        fill_normal(x, n, 1e-3, 200 + q);
+        hc[q] = malloc(nbytes);
+        hs[q] = malloc(nb * 4);
+        orc_quantize_blockwise_i4(x, n, B, hc[q], hs[q]);
+        uint8_t *c = dev_alloc(nbytes);
+        float *sc = dev_alloc(nb * 4);
+        HIP_OK(hipMemcpyAsync(c, hc[q], nbytes, hipMemcpyHostToDevice, up));
+        HIP_OK(hipMemcpyAsync(sc, hs[q], nb * 4, hipMemcpyHostToDevice, up));
+        dc[q] = c;
+        ds[q] = sc;
+    }
+    hipEvent_t uploaded, done;
+    HIP_OK(hipEventCreateWithFlags(&uploaded, hipEventDisableTiming));
+    HIP_OK(hipEventCreateWithFlags(&done, hipEventDisableTiming));
+    HIP_OK(hipEventRecord(uploaded, up));
+    float *d[2][3];
+    uint16_t *dprim[2];
+    for (int k = 0; k < 2; k++) {
+        for (int a = 0; a < 3; a++) {
+            d[k][a] = dev_alloc(n * 4);
+            if (a == 0)
+                HIP_OK(hipMemcpy(d[k][a], p0, n * 4, hipMemcpyHostToDevice));
+            else
+                HIP_OK(hipMemset(d[k][a], 0, n * 4));
+        }
+        dprim[k] = dev_alloc(n * 2);
+    }
+    float *dgrad = dev_alloc(n * 4);
+    HIP_OK(hipDeviceSynchronize());
+    /* the two-call sequence, then the fused call, both ordered after the upload */
+    EXPECT(zpp_dequant_reduce_i4(dc, ds, NSRC, n, B, scale_out, dgrad, st, &uploaded, 1, NULL) ==
+               ZPP_OK,
+           "dequant-reduce");
+    EXPECT(zpp_adam_partition_step(d[0][0], d[0][1], d[0][2], dgrad, dprim[0], n, hp, st) ==
+               ZPP_OK,
+           "adam from the reduced gradient");
+    EXPECT(zpp_qgz_receive_adam_step(d[1][0], d[1][1], d[1][2], dc, ds, NSRC, B, scale_out,
+                                     dprim[1], n, hp, st, &uploaded, 1, done) == ZPP_OK,
+           "fused receive step");
+    HIP_OK(hipEventSynchronize(done));
+    float *h[2][3], *hg = malloc(n * 4), *rg = malloc(n * 4);
+    uint16_t *hp16[2];
+    for (int k = 0; k < 2; k++) {
+        for (int a = 0; a < 3; a++) {
+            h[k][a] = malloc(n * 4);
+            HIP_OK(hipMemcpy(h[k][a], d[k][a], n * 4, hipMemcpyDeviceToHost));
+        }
+        hp16[k] = malloc(n * 2);
+        HIP_OK(hipMemcpy(hp16[k], dprim[k], n * 2, hipMemcpyDeviceToHost));
+    }
+    HIP_OK(hipMemcpy(hg, dgrad, n * 4, hipMemcpyDeviceToHost));
+    for (int a = 0; a < 3; a++)
+        EXPECT(memcmp(h[0][a], h[1][a], n * 4) == 0, "fused receive state array %d differs", a);
+    EXPECT(memcmp(hp16[0], hp16[1], n * 2) == 0, "fused receive primary differs");
+    orc_dequant_reduce_i4((const uint8_t *const *)hc, (const float *const *)hs, NSRC, n, B,
+                          scale_out, rg);
+    EXPECT(memcmp(hg, rg, n * 4) == 0, "reduced gradient differs from the oracle's");
+    float *rp = malloc(n * 4), *rm = calloc(n, 4), *rv = calloc(n, 4);
+    uint16_t *rprim = malloc(n * 2);
+    memcpy(rp, p0, n * 4);
+    orc_adam_step(rp, rm, rv, rg, rprim, n, hp->lr, hp->beta1, hp->beta2, hp->eps,
+                  hp->weight_decay, hp->step, hp->adamw);
+    double ep = 0, e;
+    for (size_t i = 0; i < n; i++)
+        if ((e = rel_err(h[1][0][i], rp[i], hp->lr)) > ep) ep = e;
+    EXPECT(ep <= 1e-5, "fused receive master rel err %g", ep);
+    printf("qgz receive step: %u sources, bit-identical to reduce + step, master rel err %.3g\n",
+           NSRC, ep);
+    HIP_OK(hipStreamDestroy(up));
+    HIP_OK(hipStreamDestroy(st));
 }
 
 static void check_validation(void)
@@ -269,6 +368,7 @@ int main(int argc, char **argv)
     EXPECT(same * 100 >= nb * 99, "only %zu of %zu blocks agree", same, nb);
     EXPECT(memcmp(gout + s, rout + s, (N - s) * 2) == 0, "gather of the peer shards");
 
+    check_receive(n, p, &hp);
     check_validation();
 
     printf("adam rel err p %.3g m %.3g v %.3g, bf16 %d ulp, %zu/%zu blocks bit-exact "

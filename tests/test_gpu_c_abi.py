@@ -1,7 +1,9 @@
 """The C ABI used from plain C: tests/c_abi_driver (built with the library by
 the repository's build step) runs one iteration of the path with hipMalloc'd
 buffers, three streams and caller-owned events, and checks it against the
-oracle's C library.  It runs as a child process of the test runner."""
+oracle's C library; then the qgZ receive fused into the partition step,
+against the dequantize-and-reduce followed by the step.  It runs as a child
+process of the test runner."""
 import os
 import subprocess
 import sys
