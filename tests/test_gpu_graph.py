@@ -115,3 +115,77 @@ def test_iteration_in_a_hip_graph(zpp, fused):
     finally:
         h.hipGraphExecDestroy(exe)
         h.hipGraphDestroy(graph)
+
+
+def test_receive_iteration_in_a_hip_graph(zpp):
+    """An iteration that opens with the qgZ receive fused into the partition
+    step (int4 gradient copies -> Adam), then the refresh, the quantization
+    and the gather, on one stream, captured into a HIP graph and replayed
+    three times with eager work in between: every replay equals the same
+    iteration run eagerly from the same state, bit for bit."""
+    n, B, P, P2 = (1 << 20) + 256, 256, 4, 2
+    hp = dict(lr=float(np.float32(1e-4)), beta1=float(np.float32(0.9)),
+              beta2=float(np.float32(0.95)), eps=float(np.float32(1e-8)),
+              weight_decay=float(np.float32(0.1)))
+    p0 = torch.from_numpy(synth.master_weights(n, 111)).cuda()
+    src_c, src_s = [], []
+    for q in range(P):
+        g = synth.device_normal_f32(n, synth.GRAD_STD, 111, synth.KIND_GRAD, rank=q)
+        c = torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda")
+        s = torch.empty((n + B - 1) // B, dtype=torch.float32, device="cuda")
+        zpp.quantize_blockwise_i4(g, c, s, block=B)
+        src_c.append(c)
+        src_s.append(s)
+    peer_c = synth.device_random_codes(n, 111, rank=1)
+    peer_s = synth.device_random_scales(n // B, 111, rank=1)
+    torch.cuda.synchronize()
+
+    def state():
+        return dict(p=p0.clone(), m=torch.zeros(n, device="cuda"), v=torch.zeros(n, device="cuda"),
+                    prim=torch.empty(n, dtype=torch.int16, device="cuda"),
+                    sec=torch.empty(n, dtype=torch.int16, device="cuda"),
+                    codes=torch.empty(n, dtype=torch.int8, device="cuda"),
+                    scales=torch.empty(n // B, dtype=torch.float32, device="cuda"),
+                    out=torch.empty(P2 * n, dtype=torch.int16, device="cuda"))
+
+    stream = torch.cuda.Stream()
+
+    def iteration(st):
+        zpp.qgz_receive_adam_step(st["p"], st["m"], st["v"], src_c, src_s, st["prim"], step=1,
+                                  block=B, scale_out=1.0 / P, stream=stream, **hp)
+        zpp.refresh_secondary(st["sec"], st["prim"], stream=stream)
+        zpp.quantize_blockwise_i8(st["sec"], st["codes"], st["scales"], block=B, stream=stream)
+        zpp.dequant_gather_layer([st["codes"], peer_c], [st["scales"], peer_s], n, P2 * n,
+                                 st["out"], block=B, stream=stream)
+
+    def snapshot(st):
+        return [to_host(st[k], np.uint8) for k in ("p", "m", "v", "prim", "sec", "codes",
+                                                    "scales", "out")]
+
+    ref_state = state()
+    torch.cuda.synchronize()
+    refs = []
+    for _ in range(3):
+        iteration(ref_state)
+        torch.cuda.synchronize()
+        refs.append(snapshot(ref_state))
+
+    h = hip()
+    st = state()
+    torch.cuda.synchronize()
+    graph = ctypes.c_void_p()
+    exe = ctypes.c_void_p()
+    assert h.hipStreamBeginCapture(stream.cuda_stream, HIP_CAPTURE_MODE_RELAXED) == 0
+    iteration(st)
+    assert h.hipStreamEndCapture(stream.cuda_stream, ctypes.byref(graph)) == 0
+    assert h.hipGraphInstantiate(ctypes.byref(exe), graph, None, None, 0) == 0
+    try:
+        for r in range(3):
+            assert h.hipGraphLaunch(exe, stream.cuda_stream) == 0
+            torch.cuda.synchronize()
+            for i, (a, b) in enumerate(zip(snapshot(st), refs[r])):
+                assert_bits_equal(a, b, "replay %d output %d" % (r, i))
+            _ = (st["p"].sum() + 1).item()
+    finally:
+        h.hipGraphExecDestroy(exe)
+        h.hipGraphDestroy(graph)
