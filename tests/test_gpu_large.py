@@ -114,3 +114,53 @@ def test_gather_past_4g(zpp):
     assert_bits_equal(out[start:].cpu().numpy().view(np.uint16), tail_ref, "tail")
     del codes, scales, out
     torch.cuda.empty_cache()
+
+
+def test_receive_adam_past_4g(zpp):
+    """The qgZ receive fused into the partition step over more than 2^32
+    elements from 2 int4 sources: sampled whole blocks (around 2^32 and the
+    ragged tail included) against the oracle's dequantize-and-reduce followed
+    by its Adam step."""
+    n, B, P = BIG, 256, 2
+    nb = (n + B - 1) // B
+    hp = {k: float(np.float32(v)) for k, v in
+          dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1).items()}
+    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
+    for q in range(P):
+        src = synth.device_normal_f32(n, synth.GRAD_STD, 104, synth.KIND_GRAD, rank=q)
+        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=B)
+        torch.cuda.synchronize()
+        del src
+    torch.cuda.empty_cache()
+    p = synth.device_normal_f32(n, synth.WEIGHT_STD, 104, synth.KIND_MASTER)
+    m = torch.zeros(n, device="cuda")
+    v = torch.zeros(n, device="cuda")
+    out = torch.empty(n, dtype=torch.int16, device="cuda")
+    g = np.random.default_rng(5)
+    kb = np.unique(np.concatenate([g.integers(0, nb - 1, size=2048),
+                                   [(1 << 32) // B - 1, (1 << 32) // B, nb - 2]]))
+    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
+    cidx = torch.from_numpy((kb[:, None] * (B // 2) + np.arange(B // 2)[None, :]).ravel()).cuda()
+    sidx = torch.from_numpy(kb).cuda()
+    ph = p.index_select(0, eidx).cpu().numpy()
+    hc = [c.index_select(0, cidx).cpu().numpy() for c in codes]
+    hs = [s.index_select(0, sidx).cpu().numpy() for s in scales]
+    tail = n - (nb - 1) * B
+    tp = p[(nb - 1) * B:].cpu().numpy()
+    tc = [c[(nb - 1) * B // 2:].cpu().numpy() for c in codes]
+    ts = [s[nb - 1:].cpu().numpy() for s in scales]
+    zpp.qgz_receive_adam_step(p, m, v, codes, scales, out, step=1, block=B, scale_out=0.5, **hp)
+    torch.cuda.synchronize()
+    half = float(np.float32(0.5))
+    for what, idx, p_ref, c_ref, s_ref, k in (
+            ("sampled blocks", eidx, ph, hc, hs, kb.size * B),
+            ("tail", torch.arange((nb - 1) * B, n, device="cuda"), tp, tc, ts, tail)):
+        gr = oracle.dequant_reduce_i4(c_ref, s_ref, k, B, half)
+        z = np.zeros(k, np.float32)
+        got = tuple(t.index_select(0, idx).cpu().numpy().view(d) for t, d in
+                    ((p, np.float32), (m, np.float32), (v, np.float32), (out, np.uint16)))
+        assert_adam_close(got, oracle.adam_step(p_ref, z, z, gr, step=1, **hp), hp["lr"],
+                          "receive step past 2^32, " + what)
+    del p, m, v, out, codes, scales
+    torch.cuda.empty_cache()
