@@ -18,7 +18,8 @@ next step's Adam), the fused step + refresh + quantize kernel in place of the
 three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
 timing only), the qgZ gradient side, the step preceded by the qgZ receive
-(as its own kernel, and fused into the partition step), and, for context,
+(as its own kernel, fused into the partition step, and inside the single
+pass of step, refresh and quantization), and, for context,
 PyTorch's fused AdamW on a partition of the same size.  The
 CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
@@ -388,10 +389,13 @@ def main():
     torch.cuda.synchronize()
     qgz_ms, qgz_times, qgz_kb, qgz_step_bytes = run(False, "event", True)
     qgz_gbps = qgz_step_bytes / (qgz_ms * 1e-3) / 1e9
-    # the same, with the receive fused into the partition step
+    # the same, with the receive fused into the partition step, and into the
+    # single pass of step, refresh and quantization
     pipe.fuse_receive = True
     fr_ms, fr_times, fr_kb, fr_step_bytes = run(False, "event", True)
     fr_gbps = fr_step_bytes / (fr_ms * 1e-3) / 1e9
+    ff_ms, ff_times, ff_kb, ff_step_bytes = run(True, "event", True)
+    ff_gbps = ff_step_bytes / (ff_ms * 1e-3) / 1e9
     pipe.fuse_receive = False
     pipe.exchange = None
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -456,6 +460,10 @@ def main():
             "ms_per_step": round(fr_ms, 4), "GB/s": round(fr_gbps, 1),
             "frac_of_peak": round(fr_gbps / HBM_PEAK_GBPS, 4),
             "kernels": kernel_table(fr_kb, fr_times)},
+        "step_with_qgz_receive_single_pass": {
+            "ms_per_step": round(ff_ms, 4), "GB/s": round(ff_gbps, 1),
+            "frac_of_peak": round(ff_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(ff_kb, ff_times)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
         "gpu": {"name": torch.cuda.get_device_name(0),
                 "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,

@@ -261,6 +261,35 @@ ZPP_API zpp_status zpp_qgz_receive_adam_step(float *master, float *exp_avg, floa
                                              const hipEvent_t *wait_events, uint32_t num_wait,
                                              hipEvent_t done_after);
 
+/* The whole pass of one rank's partition with the qgZ receive: the partition
+ * step taking its gradient from the int4 copies (as
+ * zpp_qgz_receive_adam_step), then the secondary refresh and the qwZ
+ * quantization of the new bf16 weights (as zpp_adam_step_refresh_quantize),
+ * in one pass over HBM.  Results are bit for bit those of
+ * zpp_qgz_receive_adam_step into primary_bf16, zpp_refresh_secondary from
+ * it and zpp_quantize_blockwise_i8 of it, at 29 B + num_src * (0.5 B +
+ * 4/grad_block B) + 4/block B of HBM traffic per element instead of
+ * 33 B + num_src * (0.5 B + 4/grad_block B) + 4/block B.
+ * master, exp_avg, exp_avg_sq: float[n] in place.  src_codes, src_scales,
+ * num_src, scale_out: as for zpp_qgz_receive_adam_step, with int4 blocks of
+ * grad_block (a power of two in [64, 4096]).  primary_bf16: uint16_t[n] out;
+ * secondary_bf16: uint16_t[n] out, or NULL to keep no bf16 secondary copy;
+ * codes: int8_t[n] out; scales: float[ceil(n/block)] out, int8 blocks of
+ * block (a power of two in [64, 4096]).  hp as for zpp_adam_partition_step.
+ * Order on `stream`: wait for every event of wait_events[0..num_wait),
+ * run, record `done_after` (the event a gather of the codes waits on).
+ * No two outputs may overlap, nor any output a source range (ZPP_EOVERLAP).
+ * Alignment: floats and scales 4, bf16 2 bytes (ZPP_EALIGN); 16-byte state
+ * arrays, 8-byte bf16 arrays, 4-byte codes and 2-byte source codes select
+ * the single-pass kernel, otherwise the three scalar kernels run one after
+ * another. */
+ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *const *src_codes,
+    const float *const *src_scales, uint32_t num_src, uint32_t grad_block, float scale_out,
+    uint16_t *primary_bf16, uint16_t *secondary_bf16, int8_t *codes, float *scales, size_t n,
+    uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after);
+
 /* Static, NUL-terminated description of a status code. */
 ZPP_API const char *zpp_status_string(zpp_status s);
 

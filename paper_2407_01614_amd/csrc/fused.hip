@@ -17,14 +17,21 @@
 // absmax is known; a 256-block is exactly one wave, so its absmax is a
 // six-step cross-lane reduction.  Residency is capped at ZPP_FUSED_RESIDENCY
 // workgroups per CU, as for the optimizer step: 1031-1046 us with 12 resident
-// at the Llama-2-13B partition (11-14 within 1%), 1127-1145 us uncapped.
+// at the Llama-2-13B partition (9-20 within 1%), 1127-1145 us uncapped.  With
+// the qgZ receive in place of the fp32 gradient (8 int4 sources) the cap is
+// ZPP_FUSED_RECV_RESIDENCY: 1111 us with 13, 1118 with 14, 1150 with 12, 1216
+// with 11, 1142 uncapped.
 #include "zpp_adam.h"
 #include "zpp_device.h"
+#include "zpp_i4grad.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
 
 #ifndef ZPP_FUSED_RESIDENCY
 #define ZPP_FUSED_RESIDENCY 12
+#endif
+#ifndef ZPP_FUSED_RECV_RESIDENCY
+#define ZPP_FUSED_RECV_RESIDENCY 13
 #endif
 #ifndef ZPP_FUSED_MAX_GRID
 #define ZPP_FUSED_MAX_GRID (1u << 30)
@@ -35,7 +42,6 @@ namespace {
 
 struct FusedArgs {
     float *p, *m, *v;
-    const float *g;
     uint16_t *primary;
     uint16_t *secondary;  // may be null: no bf16 secondary copy is kept
     int8_t *codes;
@@ -44,8 +50,10 @@ struct FusedArgs {
     AdamConsts c;
 };
 
-template <bool ADAMW, int B>
-__global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a) {
+// The gradient comes from `gs`: the fp32 array of the partition step
+// (F32Grad), or the int4 copies of the qgZ receive (I4Grad, zpp_i4grad.h).
+template <bool ADAMW, int B, class GS>
+__global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a, GS gs) {
     constexpr int C = B > 256 ? B : 256;  // elements per chunk (one wave)
     constexpr int W = C / 256;            // float4 groups per lane
     constexpr int L = B < 256 ? B / 4 : kWave;  // lanes per quant block
@@ -63,7 +71,7 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a) {
                 f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
                 f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
                 f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
-                const f32x4 G = ld_nt(reinterpret_cast<const f32x4 *>(a.g + i));
+                const f32x4 G = grad_load4(gs, i);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     float p = P[e], m = M[e], v = V[e];
@@ -88,7 +96,7 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a) {
                     h[e] = 0u;
                     if (i + e < a.n) {
                         float p = a.p[i + e], m = a.m[i + e], v = a.v[i + e];
-                        adam_update<ADAMW>(p, m, v, a.g[i + e], a.c);
+                        adam_update<ADAMW>(p, m, v, grad_at(gs, i + e), a.c);
                         a.p[i + e] = p;
                         a.m[i + e] = m;
                         a.v[i + e] = v;
@@ -126,16 +134,39 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a) {
     }
 }
 
-template <int B>
-void launch_fused_b(const FusedArgs &a, hipStream_t stream) {
+// Workgroups per CU for each gradient source.
+template <class GS> constexpr int fused_residency();
+template <> constexpr int fused_residency<F32Grad>() { return ZPP_FUSED_RESIDENCY; }
+template <> constexpr int fused_residency<I4Grad>() { return ZPP_FUSED_RECV_RESIDENCY; }
+
+template <int B, class GS>
+void launch_fused_b(const FusedArgs &a, const GS &gs, hipStream_t stream) {
     constexpr size_t C = B > 256 ? B : 256;
     const size_t chunks = (a.n + C - 1) / C;
     const unsigned grid = (unsigned)(chunks < ZPP_FUSED_MAX_GRID ? chunks : ZPP_FUSED_MAX_GRID);
-    constexpr size_t lds = residency_lds(ZPP_FUSED_RESIDENCY);
+    constexpr size_t lds = residency_lds(fused_residency<GS>());
     if (a.c.adamw)
-        hipLaunchKernelGGL((fused_kernel<true, B>), dim3(grid), dim3(kWave), lds, stream, a);
+        hipLaunchKernelGGL((fused_kernel<true, B, GS>), dim3(grid), dim3(kWave), lds, stream, a,
+                           gs);
     else
-        hipLaunchKernelGGL((fused_kernel<false, B>), dim3(grid), dim3(kWave), lds, stream, a);
+        hipLaunchKernelGGL((fused_kernel<false, B, GS>), dim3(grid), dim3(kWave), lds, stream, a,
+                           gs);
+}
+
+template <class GS>
+hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
+                           hipStream_t stream) {
+    switch (block) {
+    case 64: launch_fused_b<64>(a, gs, stream); break;
+    case 128: launch_fused_b<128>(a, gs, stream); break;
+    case 256: launch_fused_b<256>(a, gs, stream); break;
+    case 512: launch_fused_b<512>(a, gs, stream); break;
+    case 1024: launch_fused_b<1024>(a, gs, stream); break;
+    case 2048: launch_fused_b<2048>(a, gs, stream); break;
+    case 4096: launch_fused_b<4096>(a, gs, stream); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -154,18 +185,30 @@ hipError_t launch_fused(float *p, float *m, float *v, const float *g, uint16_t *
             e = launch_quantize(primary, n, block, codes, scales, false, stream);
         return e;
     }
-    const FusedArgs a{p, m, v, g, primary, secondary, codes, scales, n, c};
-    switch (block) {
-    case 64: launch_fused_b<64>(a, stream); break;
-    case 128: launch_fused_b<128>(a, stream); break;
-    case 256: launch_fused_b<256>(a, stream); break;
-    case 512: launch_fused_b<512>(a, stream); break;
-    case 1024: launch_fused_b<1024>(a, stream); break;
-    case 2048: launch_fused_b<2048>(a, stream); break;
-    case 4096: launch_fused_b<4096>(a, stream); break;
-    default: return hipErrorInvalidValue;
+    const FusedArgs a{p, m, v, primary, secondary, codes, scales, n, c};
+    return launch_fused_gs(a, F32Grad{g}, block, stream);
+}
+
+hipError_t launch_fused_receive(float *p, float *m, float *v, const uint8_t *const *src_codes,
+                                const float *const *src_scales, uint32_t num_src,
+                                uint32_t grad_block, float scale_out, uint16_t *primary,
+                                uint16_t *secondary, int8_t *codes, float *scales, size_t n,
+                                uint32_t block, const AdamConsts &c, bool vector_path,
+                                hipStream_t stream) {
+    if (!vector_path) {
+        // any alignment: the receive step, the refresh and the quantization
+        // as scalar kernels, one after another on the stream
+        hipError_t e = launch_receive_adam(p, m, v, src_codes, src_scales, num_src, grad_block,
+                                           scale_out, primary, n, c, false, stream);
+        if (e == hipSuccess && secondary)
+            e = launch_refresh(secondary, primary, n, false, stream);
+        if (e == hipSuccess)
+            e = launch_quantize(primary, n, block, codes, scales, false, stream);
+        return e;
     }
-    return hipGetLastError();
+    const FusedArgs a{p, m, v, primary, secondary, codes, scales, n, c};
+    return launch_fused_gs(a, make_i4grad(src_codes, src_scales, num_src, grad_block, scale_out),
+                           block, stream);
 }
 
 }  // namespace zpp

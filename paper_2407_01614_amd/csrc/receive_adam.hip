@@ -16,8 +16,8 @@
 // Lane layout of the partition step: one wave per 256-element tile, lane l
 // holds elements [256 t + 4 l, +4): one 16-byte access per state array, one
 // 2-byte load of codes per source (a wave reads 128 contiguous bytes of each
-// source) and one scale per source.  Sources are loaded eight at a time, all
-// eight in flight before their fma passes.  Residency is capped at
+// source) and one scale per source (zpp_i4grad.h: sources taken eight at a
+// time, all eight in flight before their fma passes).  Residency is capped at
 // ZPP_RECV_RESIDENCY workgroups per CU: at the Llama-2-13B partition with 8
 // sources 994-1001 us with 12 (13: 995-999, 11: 1001-1008, 14: 1003-1011),
 // 1027 us uncapped.  Scales loaded as wave-uniform scalar loads (possible for
@@ -25,8 +25,8 @@
 // hidden the way the vector loads' is.
 #include "zpp_adam.h"
 #include "zpp_device.h"
+#include "zpp_i4grad.h"
 #include "zpp_launch.h"
-#include "zpp_quant.h"
 
 #ifndef ZPP_RECV_RESIDENCY
 #define ZPP_RECV_RESIDENCY 12
@@ -39,42 +39,16 @@ namespace zpp {
 namespace {
 
 struct RecvArgs {
-    const uint8_t *codes[kMaxShards];
-    const float *scales[kMaxShards];
+    I4Grad src;
     float *p, *m, *v;
     uint16_t *out;
     size_t n;
-    uint32_t num_src;
-    uint32_t block_shift;  // log2(block)
-    float scale_out;
     AdamConsts c;
 };
 
-constexpr int kBatch = 8;
-
-// The output scale, applied as its own rounded multiply: the two-kernel
-// sequence stores this product to memory before the update reads it, so it
-// must not be contracted into an add of the update.
-__device__ __forceinline__ float scaled(float acc, float scale_out) {
-#pragma clang fp contract(off)
-    return acc * scale_out;
-}
-
-// The gradient of element i from the sources, one element at a time (tails
-// and the any-alignment kernel).
-__device__ __forceinline__ float gradient_at(const RecvArgs &a, size_t i) {
-    float acc = 0.0f;
-    for (uint32_t q = 0; q < a.num_src; ++q) {
-        const uint32_t byte = a.codes[q][i / 2];
-        const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
-        acc = __builtin_fmaf(i4_code(nib, 0), a.scales[q][i >> a.block_shift], acc);
-    }
-    return scaled(acc, a.scale_out);
-}
-
 template <bool ADAMW>
 __device__ __forceinline__ void scalar_step(const RecvArgs &a, size_t i) {
-    const float g = gradient_at(a, i);
+    const float g = i4grad_at(a.src, i);
     float p = a.p[i], m = a.m[i], v = a.v[i];
     adam_update<ADAMW>(p, m, v, g, a.c);
     a.p[i] = p;
@@ -99,33 +73,11 @@ __global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs a) {
         f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
         f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
         f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
-        float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (uint32_t q0 = 0; q0 < a.num_src; q0 += kBatch) {
-            uint32_t w[kBatch];
-            float s[kBatch];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                const uint32_t q = q0 + j;
-                w[j] = 0u;
-                s[j] = 0.0f;
-                if (q < a.num_src) {
-                    w[j] = ld_nt(reinterpret_cast<const uint16_t *>(a.codes[q] + i / 2));
-                    s[j] = a.scales[q][i >> a.block_shift];
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                if (q0 + j < a.num_src) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        acc[e] = __builtin_fmaf(i4_code(w[j], e), s[j], acc[e]);
-                }
-            }
-        }
+        const f32x4 G = i4grad_load4(a.src, i);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float p = P[e], m = M[e], v = V[e];
-            adam_update<ADAMW>(p, m, v, scaled(acc[e], a.scale_out), a.c);
+            adam_update<ADAMW>(p, m, v, G[e], a.c);
             P[e] = p;
             M[e] = m;
             V[e] = v;
@@ -150,23 +102,30 @@ __global__ __launch_bounds__(kThreads) void recv_adam_scalar_kernel(RecvArgs a) 
 
 }  // namespace
 
+I4Grad make_i4grad(const uint8_t *const *src_codes, const float *const *src_scales,
+                   uint32_t num_src, uint32_t block, float scale_out) {
+    I4Grad s = {};
+    for (uint32_t q = 0; q < num_src; ++q) {
+        s.codes[q] = src_codes[q];
+        s.scales[q] = src_scales[q];
+    }
+    s.num_src = num_src;
+    s.block_shift = (uint32_t)__builtin_ctz(block);
+    s.scale_out = scale_out;
+    return s;
+}
+
 hipError_t launch_receive_adam(float *p, float *m, float *v, const uint8_t *const *src_codes,
                                const float *const *src_scales, uint32_t num_src, uint32_t block,
                                float scale_out, uint16_t *out, size_t n, const AdamConsts &c,
                                bool vector_path, hipStream_t stream) {
     RecvArgs a = {};
-    for (uint32_t q = 0; q < num_src; ++q) {
-        a.codes[q] = src_codes[q];
-        a.scales[q] = src_scales[q];
-    }
+    a.src = make_i4grad(src_codes, src_scales, num_src, block, scale_out);
     a.p = p;
     a.m = m;
     a.v = v;
     a.out = out;
     a.n = n;
-    a.num_src = num_src;
-    a.block_shift = (uint32_t)__builtin_ctz(block);
-    a.scale_out = scale_out;
     a.c = c;
     if (vector_path) {
         const size_t tiles = (n + 255) / 256;

@@ -409,6 +409,72 @@ ZPP_API zpp_status zpp_qgz_receive_adam_step(float *master, float *exp_avg, floa
     return record(stream, done_after);
 }
 
+ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *const *src_codes,
+    const float *const *src_scales, uint32_t num_src, uint32_t grad_block, float scale_out,
+    uint16_t *primary_bf16, uint16_t *secondary_bf16, int8_t *codes, float *scales, size_t n,
+    uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after) {
+    zpp_status st = check_hparams(hp);
+    if (st != ZPP_OK)
+        return st;
+    if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(grad_block) ||
+        !valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    if (!isfinite(scale_out))
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!src_codes || !src_scales)
+        return ZPP_EINVAL;
+    const size_t gblocks = (n + grad_block - 1) / grad_block;
+    const size_t nblocks = (n + block - 1) / block;
+    const size_t nbytes = (n + 1) / 2;
+    bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
+               aligned(primary_bf16, 8) && aligned(secondary_bf16, 8) && aligned(codes, 4);
+    for (uint32_t q = 0; q < num_src; ++q) {
+        if (!src_codes[q] || !src_scales[q])
+            return ZPP_EINVAL;
+        if (!aligned(src_scales[q], 4))
+            return ZPP_EALIGN;
+        vec = vec && aligned(src_codes[q], 2);
+    }
+    if (n) {
+        if (!master || !exp_avg || !exp_avg_sq || !primary_bf16 || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(master, 4) || !aligned(exp_avg, 4) || !aligned(exp_avg_sq, 4) ||
+            !aligned(primary_bf16, 2) || !aligned(secondary_bf16, 2) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const void *outs[7] = {master, exp_avg, exp_avg_sq, primary_bf16, codes, scales,
+                               secondary_bf16};
+        const size_t out_bytes[7] = {4 * n, 4 * n, 4 * n, 2 * n, n, 4 * nblocks,
+                                     secondary_bf16 ? 2 * n : 0};
+        if (any_overlap(outs, out_bytes, 7))
+            return ZPP_EOVERLAP;
+        for (int o = 0; o < 7; ++o)
+            for (uint32_t q = 0; q < num_src; ++q)
+                if (overlaps(outs[o], out_bytes[o], src_codes[q], nbytes) ||
+                    overlaps(outs[o], out_bytes[o], src_scales[q], 4 * gblocks))
+                    return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (n) {
+        const hipError_t e = zpp::launch_fused_receive(
+            master, exp_avg, exp_avg_sq, src_codes, src_scales, num_src, grad_block, scale_out,
+            primary_bf16, secondary_bf16, codes, scales, n, block, adam_consts(*hp), vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
 ZPP_API const char *zpp_status_string(zpp_status s) {
     switch (s) {
     case ZPP_OK: return "ok";

@@ -40,7 +40,7 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // once (the optimizer step: four arrays read, four written) run faster with
 // fewer workgroups resident per CU than the hardware would otherwise place:
 // too many waves in flight oversubscribe the memory channels.  The optimizer
-// step, the fused step, the step with the qgZ receive and the gather use it.  A launch caps
+// step, the fused steps, the step with the qgZ receive and the gather use it.  A launch caps
 // residency by reserving dynamic LDS that its kernel never touches: a CU then
 // holds at most kLdsPerCU / residency_lds(k) = k such workgroups, and the
 // dispatcher still hands out the one-shot grid as workgroups retire.
@@ -49,7 +49,8 @@ constexpr size_t kLdsPerCU = 160 * 1024;  // LDS of one gfx950 CU
 constexpr size_t residency_lds(int workgroups_per_cu) {
     return workgroups_per_cu <= 0 ? 0 : (kLdsPerCU / workgroups_per_cu) / 1024 * 1024;
 }
-static_assert(kLdsPerCU / residency_lds(11) == 11 && kLdsPerCU / residency_lds(12) == 12,
+static_assert(kLdsPerCU / residency_lds(11) == 11 && kLdsPerCU / residency_lds(12) == 12 &&
+                  kLdsPerCU / residency_lds(13) == 13,
               "a reservation caps residency at exactly the requested count");
 
 // Streaming accesses: every byte is touched once, so loads and stores are

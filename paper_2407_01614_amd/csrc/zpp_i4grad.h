@@ -1,0 +1,91 @@
+// The gradient that the qgZ receive delivers to the partition step: the sum,
+// over the num_src int4 copies of the rank's partition (one from each sending
+// rank, in rank order), of code * scale, accumulated with one fma per source
+// from 0, then one multiply by the output scale (1/P for the data-parallel
+// mean).  The dequantize-and-reduce kernel forms exactly this value and
+// writes it; the kernels that take the receive into the optimizer step form
+// it here, so that their results are bit for bit those of the separate calls.
+#pragma once
+
+#include "zpp_device.h"
+#include "zpp_launch.h"
+#include "zpp_quant.h"
+
+namespace zpp {
+
+struct I4Grad {
+    const uint8_t *codes[kMaxShards];  // packed int4, element 2i in the low nibble
+    const float *scales[kMaxShards];   // one per block of 2^block_shift elements
+    uint32_t num_src;
+    uint32_t block_shift;
+    float scale_out;
+};
+
+// The output scale, applied as its own rounded multiply: the separate calls
+// store this product to memory before the update reads it, so it must not be
+// contracted into an add of the update.
+__device__ __forceinline__ float i4grad_scaled(float acc, float scale_out) {
+#pragma clang fp contract(off)
+    return acc * scale_out;
+}
+
+// The gradient of one element (tails and the any-alignment kernels).
+__device__ __forceinline__ float i4grad_at(const I4Grad &s, size_t i) {
+    float acc = 0.0f;
+    for (uint32_t q = 0; q < s.num_src; ++q) {
+        const uint32_t byte = s.codes[q][i / 2];
+        const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
+        acc = __builtin_fmaf(i4_code(nib, 0), s.scales[q][i >> s.block_shift], acc);
+    }
+    return i4grad_scaled(acc, s.scale_out);
+}
+
+// The gradient of the four consecutive elements i .. i+3 (i a multiple of 4,
+// all four in range): one 2-byte code load and one scale per source, the
+// sources taken eight at a time with all eight loads in flight before their
+// fma passes, which keep the source order.
+__device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
+    constexpr int kBatch = 8;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
+        uint32_t w[kBatch];
+        float sc[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const uint32_t q = q0 + j;
+            w[j] = 0u;
+            sc[j] = 0.0f;
+            if (q < s.num_src) {
+                w[j] = ld_nt(reinterpret_cast<const uint16_t *>(s.codes[q] + i / 2));
+                sc[j] = s.scales[q][i >> s.block_shift];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            if (q0 + j < s.num_src) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[e] = __builtin_fmaf(i4_code(w[j], e), sc[j], acc[e]);
+            }
+        }
+    }
+    return f32x4{i4grad_scaled(acc[0], s.scale_out), i4grad_scaled(acc[1], s.scale_out),
+                 i4grad_scaled(acc[2], s.scale_out), i4grad_scaled(acc[3], s.scale_out)};
+}
+
+// The fp32 gradient array the separate partition step reads, behind the same
+// interface.
+struct F32Grad {
+    const float *g;
+};
+
+__device__ __forceinline__ float grad_at(const F32Grad &s, size_t i) { return s.g[i]; }
+__device__ __forceinline__ f32x4 grad_load4(const F32Grad &s, size_t i) {
+    return ld_nt(reinterpret_cast<const f32x4 *>(s.g + i));
+}
+__device__ __forceinline__ float grad_at(const I4Grad &s, size_t i) { return i4grad_at(s, i); }
+__device__ __forceinline__ f32x4 grad_load4(const I4Grad &s, size_t i) {
+    return i4grad_load4(s, i);
+}
+
+}  // namespace zpp

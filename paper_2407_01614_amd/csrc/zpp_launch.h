@@ -56,6 +56,23 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
                                     uint32_t block, float scale_out, float *out,
                                     bool vector_path, hipStream_t stream);
 
+struct I4Grad;
+
+// The int4 gradient sources of the qgZ receive, gathered for a kernel argument.
+I4Grad make_i4grad(const uint8_t *const *src_codes, const float *const *src_scales,
+                   uint32_t num_src, uint32_t block, float scale_out);
+
+// The fused pass with the qgZ receive: the gradient comes from num_src int4
+// copies (blocks of grad_block) instead of an fp32 array, then as
+// launch_fused (vector_path) or the receive step, refresh and quantization as
+// scalar kernels.
+hipError_t launch_fused_receive(float *p, float *m, float *v, const uint8_t *const *src_codes,
+                                const float *const *src_scales, uint32_t num_src,
+                                uint32_t grad_block, float scale_out, uint16_t *primary,
+                                uint16_t *secondary, int8_t *codes, float *scales, size_t n,
+                                uint32_t block, const AdamConsts &c, bool vector_path,
+                                hipStream_t stream);
+
 // The qgZ receive fused into the partition step: the gradient of every
 // element is the dequantize-and-reduce of the num_src int4 sources (times
 // scale_out), fed straight into the Adam update of p, m, v and the bf16 out.

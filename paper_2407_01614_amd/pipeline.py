@@ -36,8 +36,8 @@ import torch
 
 from . import synth
 from . import zpp
-from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_gather, bytes_quant,
-                        bytes_receive_adam, bytes_reduce_i4)
+from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_fused_receive,
+                        bytes_gather, bytes_quant, bytes_receive_adam, bytes_reduce_i4)
 
 
 SYNC_MODES = ("event", "host", "none")
@@ -55,7 +55,8 @@ class PartitionPipeline:
     every step with the qgZ receive of that many int4 gradient copies, as its
     own dequantize-and-reduce kernel writing `grad`, or, with `fuse_receive`,
     inside the partition step (`zpp_qgz_receive_adam_step`, no `grad`
-    written; separate kernels only)."""
+    written), and with `fused` too, inside the single pass of step, refresh
+    and quantization (`zpp_qgz_receive_step_refresh_quantize`)."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
                  qgz_sources=0, streams=3, fuse_receive=False):
@@ -232,10 +233,7 @@ class PartitionPipeline:
             self._timed("reduce_i4", self.compute,
                         lambda: self.exchange.reduce(self.grad, stream=self.compute))
         if self.fused:
-            self._timed("fused", self.compute, lambda: zpp.adam_step_refresh_quantize(
-                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
-                self.secondary, self.codes, self.scales, step=t, block=B, stream=self.compute,
-                done_after=self.ev_quant, **wl.adam))
+            self._fused_pass(t, self.compute, self.ev_quant)
         else:
             self._partition_step(t, self.compute)
             self.ev_primary.record(self.compute)
@@ -276,10 +274,7 @@ class PartitionPipeline:
         if self._receive_apart():
             self._timed("reduce_i4", cs, lambda: self.exchange.reduce(self.grad, stream=cs))
         if self.fused:
-            self._timed("fused", cs, lambda: zpp.adam_step_refresh_quantize(
-                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
-                self.secondary, self.codes, self.scales, step=t, block=B, stream=cs,
-                **wl.adam))
+            self._fused_pass(t, cs, None)
         else:
             self._partition_step(t, cs)
             self._timed("refresh", cs, lambda: zpp.refresh_secondary(
@@ -289,12 +284,26 @@ class PartitionPipeline:
         self._gathers(cs)
 
     def _receive_fused(self):
-        if self.fuse_receive and self.fused:
-            raise ValueError("the receive fuses into the separate partition step only")
         return self.exchange is not None and self.fuse_receive
 
     def _receive_apart(self):
         return self.exchange is not None and not self._receive_fused()
+
+    def _fused_pass(self, t, stream, done_after):
+        """Step, refresh and quantization in one pass: from `grad`, or with
+        the qgZ receive fused in, from the int4 copies of the gradient."""
+        wl, B = self.wl, self.wl.block
+        if self._receive_fused():
+            ex = self.exchange
+            self._timed("fused_receive", stream, lambda: zpp.qgz_receive_step_refresh_quantize(
+                self.master, self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales, self.primary,
+                self.secondary, self.codes, self.scales, step=t, grad_block=ex.block, block=B,
+                scale_out=1.0 / ex.num_src, stream=stream, done_after=done_after, **wl.adam))
+        else:
+            self._timed("fused", stream, lambda: zpp.adam_step_refresh_quantize(
+                self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
+                self.secondary, self.codes, self.scales, step=t, block=B, stream=stream,
+                done_after=done_after, **wl.adam))
 
     def _partition_step(self, t, stream):
         """The Adam step of the separate-kernel path: from `grad`, or with the
@@ -333,6 +342,10 @@ class PartitionPipeline:
         out = {}
         if self._receive_apart():
             out["reduce_i4"] = float(bytes_reduce_i4(wl.n, self.exchange.num_src, wl.block))
+        if self.fused and self._receive_fused():
+            out.update({"fused_receive": float(bytes_fused_receive(
+                wl.n, self.exchange.num_src, wl.block, self.exchange.block)), "gather": gather})
+            return out
         if self.fused:
             out.update({"fused": float(bytes_fused(wl.n, wl.block)), "gather": gather})
             return out

@@ -135,3 +135,10 @@ def bytes_receive_adam(n, num_src, block=BLOCK):
     # the partition step without its gradient read (26 B: p, m, v in and out,
     # bf16 out) plus every source's packed codes and scales
     return 26 * n + num_src * ((n + 1) // 2 + 4 * ((n + block - 1) // block))
+
+
+def bytes_fused_receive(n, num_src, block=BLOCK, grad_block=BLOCK):
+    # the receive step's 26 B + sources, the primary read back by nobody: the
+    # secondary (2 B), the codes (1 B) and the int8 scales written
+    return (bytes_receive_adam(n, num_src, grad_block) + 2 * n + n
+            + 4 * ((n + block - 1) // block))

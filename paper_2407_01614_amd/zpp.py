@@ -55,6 +55,10 @@ _lib.zpp_dequant_reduce_i4.argtypes = [_P, _P, _u32, _sz, _u32, ctypes.c_float, 
 _lib.zpp_qgz_receive_adam_step.restype = ctypes.c_int
 _lib.zpp_qgz_receive_adam_step.argtypes = [_P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P,
                                            _sz, ctypes.POINTER(AdamHParams), _P, _P, _u32, _P]
+_lib.zpp_qgz_receive_step_refresh_quantize.restype = ctypes.c_int
+_lib.zpp_qgz_receive_step_refresh_quantize.argtypes = [
+    _P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P, _P, _P, _P, _sz, _u32,
+    ctypes.POINTER(AdamHParams), _P, _P, _u32, _P]
 _lib.zpp_status_string.restype = ctypes.c_char_p
 _lib.zpp_status_string.argtypes = [ctypes.c_int]
 _lib.zpp_last_hip_error.restype = ctypes.c_int
@@ -62,8 +66,8 @@ _lib.zpp_last_hip_error.argtypes = []
 
 EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
            "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
-           "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step", "zpp_status_string",
-           "zpp_last_hip_error")
+           "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
+           "zpp_qgz_receive_step_refresh_quantize", "zpp_status_string", "zpp_last_hip_error")
 
 
 class ZppError(RuntimeError):
@@ -387,6 +391,51 @@ def qgz_receive_adam_step(master, exp_avg, exp_avg_sq, src_codes, src_scales, pr
                                         stream_handle(stream), warr, len(waits),
                                         _event_handle(done_after))
     _check(st, "zpp_qgz_receive_adam_step")
+
+
+def qgz_receive_step_refresh_quantize(master, exp_avg, exp_avg_sq, src_codes, src_scales,
+                                      primary_bf16, secondary_bf16, codes, scales, *, lr, beta1,
+                                      beta2, eps, weight_decay, step, adamw=True, grad_block=256,
+                                      block=256, scale_out=1.0, n=None, stream=None,
+                                      wait_events=(), done_after=None):
+    """zpp_qgz_receive_step_refresh_quantize: the receive step, the secondary
+    copy (``secondary_bf16`` may be None) and its int8 quantization in one
+    pass."""
+    for t, name in ((master, "master"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq"),
+                    (scales, "scales")):
+        _dev(t, _F32, name)
+    _dev(primary_bf16, _BF16, "primary_bf16")
+    if secondary_bf16 is not None:
+        _dev(secondary_bf16, _BF16, "secondary_bf16")
+    _dev(codes, _I8, "codes")
+    k = len(src_codes)
+    if k != len(src_scales) or not 1 <= k <= MAX_SHARDS:
+        raise ValueError("1..%d sources, one scales tensor each" % MAX_SHARDS)
+    if n is None:
+        n = master.numel()
+    for q in range(k):
+        _dev(src_codes[q], _U8, "src_codes[%d]" % q)
+        _dev(src_scales[q], _F32, "src_scales[%d]" % q)
+        if (src_codes[q].numel() < (n + 1) // 2
+                or src_scales[q].numel() < num_blocks(n, grad_block)):
+            raise ValueError("source %d buffers too small" % q)
+    bufs = [master, exp_avg, exp_avg_sq, primary_bf16, codes]
+    if secondary_bf16 is not None:
+        bufs.append(secondary_bf16)
+    if any(t.numel() < n for t in bufs) or scales.numel() < num_blocks(n, block):
+        raise ValueError("a buffer is too small for n = %d" % n)
+    cptrs = (_P * k)(*[c.data_ptr() for c in src_codes])
+    sptrs = (_P * k)(*[x.data_ptr() for x in src_scales])
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    hp = AdamHParams(lr, beta1, beta2, eps, weight_decay, 1 if adamw else 0, int(step))
+    st = _lib.zpp_qgz_receive_step_refresh_quantize(
+        master.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), cptrs, sptrs, k, grad_block,
+        scale_out, primary_bf16.data_ptr(),
+        secondary_bf16.data_ptr() if secondary_bf16 is not None else None, codes.data_ptr(),
+        scales.data_ptr(), n, block, ctypes.byref(hp), stream_handle(stream), warr, len(waits),
+        _event_handle(done_after))
+    _check(st, "zpp_qgz_receive_step_refresh_quantize")
 
 
 # --------------------------------------------------------------------------

@@ -36,7 +36,8 @@ def test_header_declares_the_four_calls():
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
                "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
                "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
-               "zpp_status_string", "zpp_last_hip_error"):
+               "zpp_qgz_receive_step_refresh_quantize", "zpp_status_string",
+               "zpp_last_hip_error"):
         assert fn in names
 
 
@@ -278,6 +279,39 @@ def test_qgz_receive_adam_validation(zpp):
     assert receive(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
     assert receive(zpp, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
     assert receive(zpp, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
+
+
+def receive_pass(zpp, state=(A, B, C, E, F, G, H), codes=(D, D + 0x100000),
+                 scales=(D + 0x200000, D + 0x300000), n=1024, grad_block=256, block=256,
+                 scale_out=0.5, h=None, waits=None, nwait=0):
+    """state: master, exp_avg, exp_avg_sq, primary, secondary, codes, scales."""
+    P = ctypes.c_void_p
+    carr = (P * len(codes))(*codes)
+    sarr = (P * len(scales))(*scales)
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_qgz_receive_step_refresh_quantize(
+        state[0], state[1], state[2], carr, sarr, len(codes), grad_block, scale_out, state[3],
+        state[4], state[5], state[6], n, block, ctypes.byref(h) if h is not False else None, None,
+        warr, nwait, None)
+
+
+def test_qgz_receive_pass_validation(zpp):
+    assert receive_pass(zpp, n=0, state=(None,) * 7) == zpp.ZPP_OK
+    assert receive_pass(zpp, h=False) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, grad_block=96) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, block=32) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, scale_out=float("inf")) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, codes=[D] * 65, scales=[D] * 65) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, codes=(D, None)) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, state=(A, B, C, E, F, None, H)) == zpp.ZPP_EINVAL
+    assert receive_pass(zpp, state=(A, B, C, E, F, G, H + 2)) == zpp.ZPP_EALIGN
+    assert receive_pass(zpp, state=(A, B, C, E, F + 1, G, H)) == zpp.ZPP_EALIGN
+    assert receive_pass(zpp, state=(A, B, C, E, E + 64, G, H)) == zpp.ZPP_EOVERLAP  # sec in prim
+    assert receive_pass(zpp, state=(A, B, C, E, F, G, G + 512)) == zpp.ZPP_EOVERLAP  # scales
+    assert receive_pass(zpp, codes=(D, A + 16)) == zpp.ZPP_EOVERLAP
+    assert receive_pass(zpp, scales=(D + 0x200000, F + 8)) == zpp.ZPP_EOVERLAP
+    assert receive_pass(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
 
 
 def test_no_oracle_in_product_path():

@@ -439,9 +439,10 @@ def test_pipeline_with_qgz_receive(zpp):
 @pytest.mark.parametrize("streams", [1, 3])
 def test_pipeline_fused_receive_equals_separate(zpp, streams):
     """The qgZ receive fused into the partition step (no gradient buffer
-    written) leaves the pipeline in the same state as the separate
-    dequantize-and-reduce followed by the step, bit for bit, over two steps,
-    and its timed kernels are the fused one and the rest of the path."""
+    written), alone or inside the single pass of step, refresh and
+    quantization, leaves the pipeline in the same state as the separate
+    dequantize-and-reduce followed by the step, bit for bit, over two steps;
+    the timed kernels are the ones each arrangement runs."""
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import Workload
     wl = Workload(name="small-qgz-fused", cfg_id=14, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
@@ -453,8 +454,13 @@ def test_pipeline_fused_receive_equals_separate(zpp, streams):
                                           wl.block) for j in range(wl.secondary_world - 1)]
     p0 = synth.master_weights(wl.n, wl.cfg_id)
     results = []
-    for fuse in (False, True):
-        pipe = PartitionPipeline(wl, qgz_sources=P, streams=streams, fuse_receive=fuse)
+    expect = {(False, False): {"reduce_i4", "adam", "refresh", "quant", "gather"},
+              (False, True): {"receive_adam", "refresh", "quant", "gather"},
+              (True, False): {"reduce_i4", "fused", "gather"},
+              (True, True): {"fused_receive", "gather"}}
+    for fused, fuse in expect:
+        pipe = PartitionPipeline(wl, qgz_sources=P, streams=streams, fused=fused,
+                                 fuse_receive=fuse)
         pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
         for q, (c, sc) in enumerate(quants):
             pipe.exchange.codes[q].copy_(torch.from_numpy(c))
@@ -464,13 +470,12 @@ def test_pipeline_fused_receive_equals_separate(zpp, streams):
         pipe.enable_timing()
         pipe.step()
         pipe.wait()
-        names = set(pipe.kernel_times_ms())
-        assert names == ({"receive_adam", "refresh", "quant", "gather"} if fuse
-                         else {"reduce_i4", "adam", "refresh", "quant", "gather"})
+        assert set(pipe.kernel_times_ms()) == expect[(fused, fuse)]
         results.append([t.cpu().numpy().copy() for t in (pipe.master, pipe.exp_avg,
                                                          pipe.exp_avg_sq, pipe.primary,
                                                          pipe.secondary, pipe.codes, pipe.scales,
                                                          pipe.out)])
         del pipe
-    for i, (a, b) in enumerate(zip(*results)):
-        assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)
+    for other in results[1:]:
+        for i, (a, b) in enumerate(zip(other, results[0])):
+            assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)

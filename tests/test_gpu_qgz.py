@@ -363,3 +363,119 @@ def test_fullsize_receive_adam(zpp):
             [x[a // block:-(-(a + step) // block)] for x in hs],
             min(step, n - a), block, float(np.float32(1.0 / P))), range(0, n, step)))
     assert_bits_equal(g.cpu().numpy(), np.concatenate(parts), "whole gradient")
+
+
+# --------------------------------------------------------------------------
+# The whole pass with the receive: step from int4 copies, refresh, quantize
+# --------------------------------------------------------------------------
+def run_receive_then_refresh_quantize(zpp, quants, n, grad_block, block, scale_out, state,
+                                      secondary, step, hp, adamw):
+    """The reference sequence on the GPU: the receive step, the refresh of
+    the secondary from its primary, the quantization of the primary."""
+    p, m, v, b = state
+    codes = [u8_dev(c) for c, _ in quants]
+    scales = [to_dev(s) for _, s in quants]
+    zpp.qgz_receive_adam_step(p, m, v, codes, scales, b, step=step, adamw=adamw,
+                              block=grad_block, scale_out=scale_out, **hp)
+    sec = empty_dev(n, np.uint16, fill=0x7FC0)
+    zpp.refresh_secondary(sec, b)
+    qc = empty_dev(n, np.int8, fill=0)
+    qs = empty_dev((n + block - 1) // block, np.float32, fill=-1.0)
+    zpp.quantize_blockwise_i8(b, qc, qs, block=block)
+    torch.cuda.synchronize()
+    return host_state(state) + ((to_host(sec, np.uint16) if secondary else None),
+                                to_host(qc, np.int8), to_host(qs, np.float32))
+
+
+def run_receive_pass(zpp, quants, n, grad_block, block, scale_out, state, secondary, step, hp,
+                     adamw, pad=0):
+    p, m, v, b = state
+    codes = [u8_dev(c, pad=pad) for c, _ in quants]
+    scales = [to_dev(s) for _, s in quants]
+    sec = empty_dev(n, np.uint16, pad=pad, fill=0x7FC0) if secondary else None
+    qc = empty_dev(n, np.int8, pad=pad, fill=0)
+    qs = empty_dev((n + block - 1) // block, np.float32, fill=-1.0)
+    zpp.qgz_receive_step_refresh_quantize(p, m, v, codes, scales, b, sec, qc, qs, step=step,
+                                          adamw=adamw, grad_block=grad_block, block=block,
+                                          scale_out=scale_out, **hp)
+    torch.cuda.synchronize()
+    return host_state(state) + ((to_host(sec, np.uint16) if secondary else None),
+                                to_host(qc, np.int8), to_host(qs, np.float32))
+
+
+@pytest.mark.parametrize("P,n,grad_block,block,secondary", [
+    (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
+    (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
+    (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False)])
+@pytest.mark.parametrize("regime", sorted(REGIMES))
+def test_receive_pass_equals_three_calls(zpp, P, n, grad_block, block, secondary, regime):
+    """Bit for bit the receive step, then the refresh and the quantization of
+    its primary (all on the GPU, from the same state)."""
+    hp, moments, step, adamw = REGIMES[regime]
+    quants = oracle_sources(P, n, grad_block, 96 + P + n)
+    scale_out = float(np.float32(1.0 / P))
+    ref_state, _ = receive_state(n, 97, moments=moments)
+    got_state, _ = receive_state(n, 97, moments=moments)
+    ref = run_receive_then_refresh_quantize(zpp, quants, n, grad_block, block, scale_out,
+                                            ref_state, secondary, step, hp, adamw)
+    got = run_receive_pass(zpp, quants, n, grad_block, block, scale_out, got_state, secondary,
+                           step, hp, adamw)
+    names = ("master", "exp_avg", "exp_avg_sq", "primary", "secondary", "codes", "scales")
+    for a, b, name in zip(got, ref, names):
+        if a is None:
+            continue
+        assert_bits_equal(a, b, "%s P=%d n=%d blocks %d/%d" % (name, P, n, grad_block, block))
+
+
+@pytest.mark.parametrize("pad", [1, 3])
+def test_receive_pass_misaligned(zpp, pad):
+    """Misaligned arrays take the three scalar kernels: the same results."""
+    n, grad_block, block, P = 256 * 11 + 5, 128, 256, 5
+    quants = oracle_sources(P, n, grad_block, 98)
+    ref_state, _ = receive_state(n, 99)
+    got_state, _ = receive_state(n, 99, pad=pad)
+    ref = run_receive_then_refresh_quantize(zpp, quants, n, grad_block, block, 0.2, ref_state,
+                                            True, 1, HP, True)
+    got = run_receive_pass(zpp, quants, n, grad_block, block, 0.2, got_state, True, 1, HP, True,
+                           pad=pad)
+    for a, b in zip(got, ref):
+        assert_bits_equal(a, b, "misaligned pad=%d" % pad)
+
+
+def test_fullsize_receive_pass(zpp):
+    """The Llama-2-13B partition from 8 int4 sources: the single pass equals
+    the receive step, the refresh and the quantization, compared whole on the
+    device."""
+    wl = WORKLOADS["llama-2-13b"]
+    n, B, P = wl.n, wl.block, 8
+    nb = (n + B - 1) // B
+    hp = f32hp(wl.adam)
+    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
+    for q in range(P):
+        src = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, rank=q)
+        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=B)
+        torch.cuda.synchronize()
+        del src
+    p0 = synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER)
+    outs = []
+    for single in (False, True):
+        p, m, v = p0.clone(), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+        prim = torch.empty(n, dtype=torch.int16, device="cuda")
+        sec = torch.empty(n, dtype=torch.int16, device="cuda")
+        qc = torch.empty(n, dtype=torch.int8, device="cuda")
+        qs = torch.empty(nb, dtype=torch.float32, device="cuda")
+        if single:
+            zpp.qgz_receive_step_refresh_quantize(p, m, v, codes, scales, prim, sec, qc, qs,
+                                                  step=1, scale_out=1.0 / P, **hp)
+        else:
+            zpp.qgz_receive_adam_step(p, m, v, codes, scales, prim, step=1, scale_out=1.0 / P,
+                                      **hp)
+            zpp.refresh_secondary(sec, prim)
+            zpp.quantize_blockwise_i8(prim, qc, qs)
+        torch.cuda.synchronize()
+        outs.append([p.view(torch.int32), m.view(torch.int32), v.view(torch.int32), prim, sec,
+                     qc, qs.view(torch.int32)])
+    for a, b, name in zip(outs[1], outs[0], ("master", "exp_avg", "exp_avg_sq", "primary",
+                                             "secondary", "codes", "scales")):
+        assert torch.equal(a, b), name
