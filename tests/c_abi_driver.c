@@ -9,7 +9,10 @@
  * same iteration on the same inputs on its own.  Then the qgZ receive fused
  * into the partition step (zpp_qgz_receive_adam_step) from int4 gradient
  * copies, against the dequantize-and-reduce followed by the step and against
- * the oracle.  Also checks a few validation errors of the ABI.
+ * the oracle, and the single receive pass that also writes the secondary
+ * and its int8 quantization (zpp_qgz_receive_step_refresh_quantize) against
+ * the same sequence and the oracle's quantization.  Also checks a few
+ * validation errors of the ABI.
  *
  * Test infrastructure: built by the repository's build step, run by
  * tests/test_gpu_c_abi.py.  Prints "c abi ok" and exits 0 on success.
@@ -137,9 +140,10 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     HIP_OK(hipEventCreateWithFlags(&uploaded, hipEventDisableTiming));
     HIP_OK(hipEventCreateWithFlags(&done, hipEventDisableTiming));
     HIP_OK(hipEventRecord(uploaded, up));
-    float *d[2][3];
-    uint16_t *dprim[2];
-    for (int k = 0; k < 2; k++) {
+    /* state 0: reduce then step; 1: the receive step; 2: the single pass */
+    float *d[3][3];
+    uint16_t *dprim[3];
+    for (int k = 0; k < 3; k++) {
         for (int a = 0; a < 3; a++) {
             d[k][a] = dev_alloc(n * 4);
             if (a == 0)
@@ -150,6 +154,9 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         dprim[k] = dev_alloc(n * 2);
     }
     float *dgrad = dev_alloc(n * 4);
+    uint16_t *dsec = dev_alloc(n * 2);
+    int8_t *dq8 = dev_alloc(n);
+    float *ds8 = dev_alloc(nb * 4);
     HIP_OK(hipDeviceSynchronize());
     /* the two-call sequence, then the fused call, both ordered after the upload */
     EXPECT(zpp_dequant_reduce_i4(dc, ds, NSRC, n, B, scale_out, dgrad, st, &uploaded, 1, NULL) ==
@@ -159,12 +166,21 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
                ZPP_OK,
            "adam from the reduced gradient");
     EXPECT(zpp_qgz_receive_adam_step(d[1][0], d[1][1], d[1][2], dc, ds, NSRC, B, scale_out,
-                                     dprim[1], n, hp, st, &uploaded, 1, done) == ZPP_OK,
+                                     dprim[1], n, hp, st, &uploaded, 1, NULL) == ZPP_OK,
            "fused receive step");
+    EXPECT(zpp_qgz_receive_step_refresh_quantize(d[2][0], d[2][1], d[2][2], dc, ds, NSRC, B,
+                                                 scale_out, dprim[2], dsec, dq8, ds8, n, B, hp,
+                                                 st, &uploaded, 1, done) == ZPP_OK,
+           "single receive pass");
     HIP_OK(hipEventSynchronize(done));
-    float *h[2][3], *hg = malloc(n * 4), *rg = malloc(n * 4);
-    uint16_t *hp16[2];
-    for (int k = 0; k < 2; k++) {
+    float *h[3][3], *hg = malloc(n * 4), *rg = malloc(n * 4), *hs8 = malloc(nb * 4),
+          *rs8 = malloc(nb * 4);
+    uint16_t *hp16[3], *hsec = malloc(n * 2);
+    int8_t *hq8 = malloc(n), *rq8 = malloc(n);
+    HIP_OK(hipMemcpy(hsec, dsec, n * 2, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hq8, dq8, n, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hs8, ds8, nb * 4, hipMemcpyDeviceToHost));
+    for (int k = 0; k < 3; k++) {
         for (int a = 0; a < 3; a++) {
             h[k][a] = malloc(n * 4);
             HIP_OK(hipMemcpy(h[k][a], d[k][a], n * 4, hipMemcpyDeviceToHost));
@@ -173,9 +189,16 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         HIP_OK(hipMemcpy(hp16[k], dprim[k], n * 2, hipMemcpyDeviceToHost));
     }
     HIP_OK(hipMemcpy(hg, dgrad, n * 4, hipMemcpyDeviceToHost));
-    for (int a = 0; a < 3; a++)
-        EXPECT(memcmp(h[0][a], h[1][a], n * 4) == 0, "fused receive state array %d differs", a);
-    EXPECT(memcmp(hp16[0], hp16[1], n * 2) == 0, "fused receive primary differs");
+    for (int k = 1; k < 3; k++) {
+        for (int a = 0; a < 3; a++)
+            EXPECT(memcmp(h[0][a], h[k][a], n * 4) == 0, "receive %d: state array %d differs", k,
+                   a);
+        EXPECT(memcmp(hp16[0], hp16[k], n * 2) == 0, "receive %d: primary differs", k);
+    }
+    EXPECT(memcmp(hsec, hp16[0], n * 2) == 0, "single receive pass: secondary differs");
+    orc_quantize_blockwise_i8(hp16[0], n, B, rq8, rs8);
+    EXPECT(memcmp(hq8, rq8, n) == 0, "single receive pass: codes differ from the oracle's");
+    EXPECT(memcmp(hs8, rs8, nb * 4) == 0, "single receive pass: scales differ from the oracle's");
     orc_dequant_reduce_i4((const uint8_t *const *)hc, (const float *const *)hs, NSRC, n, B,
                           scale_out, rg);
     EXPECT(memcmp(hg, rg, n * 4) == 0, "reduced gradient differs from the oracle's");
@@ -188,7 +211,8 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     for (size_t i = 0; i < n; i++)
         if ((e = rel_err(h[1][0][i], rp[i], hp->lr)) > ep) ep = e;
     EXPECT(ep <= 1e-5, "fused receive master rel err %g", ep);
-    printf("qgz receive step: %u sources, bit-identical to reduce + step, master rel err %.3g\n",
+    printf("qgz receive step and single pass: %u sources, bit-identical to reduce + step, "
+           "codes and scales equal to the oracle's, master rel err %.3g\n",
            NSRC, ep);
     HIP_OK(hipStreamDestroy(up));
     HIP_OK(hipStreamDestroy(st));

@@ -117,12 +117,14 @@ def test_iteration_in_a_hip_graph(zpp, fused):
         h.hipGraphDestroy(graph)
 
 
-def test_receive_iteration_in_a_hip_graph(zpp):
+@pytest.mark.parametrize("single_pass", [False, True], ids=["step", "single-pass"])
+def test_receive_iteration_in_a_hip_graph(zpp, single_pass):
     """An iteration that opens with the qgZ receive fused into the partition
     step (int4 gradient copies -> Adam), then the refresh, the quantization
-    and the gather, on one stream, captured into a HIP graph and replayed
-    three times with eager work in between: every replay equals the same
-    iteration run eagerly from the same state, bit for bit."""
+    (or all three in the single receive pass) and the gather, on one stream,
+    captured into a HIP graph and replayed three times with eager work in
+    between: every replay equals the same iteration run eagerly from the same
+    state, bit for bit."""
     n, B, P, P2 = (1 << 20) + 256, 256, 4, 2
     hp = dict(lr=float(np.float32(1e-4)), beta1=float(np.float32(0.9)),
               beta2=float(np.float32(0.95)), eps=float(np.float32(1e-8)),
@@ -151,10 +153,17 @@ def test_receive_iteration_in_a_hip_graph(zpp):
     stream = torch.cuda.Stream()
 
     def iteration(st):
-        zpp.qgz_receive_adam_step(st["p"], st["m"], st["v"], src_c, src_s, st["prim"], step=1,
-                                  block=B, scale_out=1.0 / P, stream=stream, **hp)
-        zpp.refresh_secondary(st["sec"], st["prim"], stream=stream)
-        zpp.quantize_blockwise_i8(st["sec"], st["codes"], st["scales"], block=B, stream=stream)
+        if single_pass:
+            zpp.qgz_receive_step_refresh_quantize(
+                st["p"], st["m"], st["v"], src_c, src_s, st["prim"], st["sec"], st["codes"],
+                st["scales"], step=1, grad_block=B, block=B, scale_out=1.0 / P, stream=stream,
+                **hp)
+        else:
+            zpp.qgz_receive_adam_step(st["p"], st["m"], st["v"], src_c, src_s, st["prim"],
+                                      step=1, block=B, scale_out=1.0 / P, stream=stream, **hp)
+            zpp.refresh_secondary(st["sec"], st["prim"], stream=stream)
+            zpp.quantize_blockwise_i8(st["sec"], st["codes"], st["scales"], block=B,
+                                      stream=stream)
         zpp.dequant_gather_layer([st["codes"], peer_c], [st["scales"], peer_s], n, P2 * n,
                                  st["out"], block=B, stream=stream)
 

@@ -116,11 +116,14 @@ def test_gather_past_4g(zpp):
     torch.cuda.empty_cache()
 
 
-def test_receive_adam_past_4g(zpp):
+@pytest.mark.parametrize("single_pass", [False, True], ids=["step", "single-pass"])
+def test_receive_adam_past_4g(zpp, single_pass):
     """The qgZ receive fused into the partition step over more than 2^32
     elements from 2 int4 sources: sampled whole blocks (around 2^32 and the
     ragged tail included) against the oracle's dequantize-and-reduce followed
-    by its Adam step."""
+    by its Adam step.  The single pass also writes the secondary (equal to the
+    primary everywhere) and its int8 quantization (the oracle's quantization
+    of the GPU's primary on the same blocks, bit for bit)."""
     n, B, P = BIG, 256, 2
     nb = (n + B - 1) // B
     hp = {k: float(np.float32(v)) for k, v in
@@ -147,20 +150,36 @@ def test_receive_adam_past_4g(zpp):
     hc = [c.index_select(0, cidx).cpu().numpy() for c in codes]
     hs = [s.index_select(0, sidx).cpu().numpy() for s in scales]
     tail = n - (nb - 1) * B
+    tidx = torch.arange((nb - 1) * B, n, device="cuda")
     tp = p[(nb - 1) * B:].cpu().numpy()
     tc = [c[(nb - 1) * B // 2:].cpu().numpy() for c in codes]
     ts = [s[nb - 1:].cpu().numpy() for s in scales]
-    zpp.qgz_receive_adam_step(p, m, v, codes, scales, out, step=1, block=B, scale_out=0.5, **hp)
+    if single_pass:
+        sec = torch.empty(n, dtype=torch.int16, device="cuda")
+        q8 = torch.empty(n, dtype=torch.int8, device="cuda")
+        s8 = torch.empty(nb, dtype=torch.float32, device="cuda")
+        zpp.qgz_receive_step_refresh_quantize(p, m, v, codes, scales, out, sec, q8, s8, step=1,
+                                              grad_block=B, block=B, scale_out=0.5, **hp)
+    else:
+        zpp.qgz_receive_adam_step(p, m, v, codes, scales, out, step=1, block=B, scale_out=0.5,
+                                  **hp)
     torch.cuda.synchronize()
     half = float(np.float32(0.5))
-    for what, idx, p_ref, c_ref, s_ref, k in (
-            ("sampled blocks", eidx, ph, hc, hs, kb.size * B),
-            ("tail", torch.arange((nb - 1) * B, n, device="cuda"), tp, tc, ts, tail)):
+    for what, idx, p_ref, c_ref, s_ref, k, blocks in (
+            ("sampled blocks", eidx, ph, hc, hs, kb.size * B, sidx),
+            ("tail", tidx, tp, tc, ts, tail, torch.tensor([nb - 1], device="cuda"))):
         gr = oracle.dequant_reduce_i4(c_ref, s_ref, k, B, half)
         z = np.zeros(k, np.float32)
         got = tuple(t.index_select(0, idx).cpu().numpy().view(d) for t, d in
                     ((p, np.float32), (m, np.float32), (v, np.float32), (out, np.uint16)))
         assert_adam_close(got, oracle.adam_step(p_ref, z, z, gr, step=1, **hp), hp["lr"],
                           "receive step past 2^32, " + what)
+        if single_pass:
+            rc, rs = oracle.quantize_blockwise_i8(got[3], B)
+            assert_bits_equal(q8.index_select(0, idx).cpu().numpy(), rc, "codes, " + what)
+            assert_bits_equal(s8.index_select(0, blocks).cpu().numpy(), rs, "scales, " + what)
+    if single_pass:
+        assert torch.equal(sec, out)
+        del sec, q8, s8
     del p, m, v, out, codes, scales
     torch.cuda.empty_cache()
