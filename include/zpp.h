@@ -290,8 +290,10 @@ ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
     uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
     uint32_t num_wait, hipEvent_t done_after);
 
-/* Static, NUL-terminated description of a status code. */
-ZPP_API const char *zpp_status_string(zpp_status s);
+/* Static, NUL-terminated description of a status code.  Takes any int, so
+ * that a caller may pass whatever status value it holds: a value that is not
+ * one of zpp_status gives "unknown status". */
+ZPP_API const char *zpp_status_string(int status);
 
 /* hipError_t (as int) of the last call on this host thread that returned
  * ZPP_EHIP; 0 if none. */

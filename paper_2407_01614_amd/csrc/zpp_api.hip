@@ -475,8 +475,8 @@ ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
     return record(stream, done_after);
 }
 
-ZPP_API const char *zpp_status_string(zpp_status s) {
-    switch (s) {
+ZPP_API const char *zpp_status_string(int status) {
+    switch (status) {
     case ZPP_OK: return "ok";
     case ZPP_EINVAL: return "invalid argument";
     case ZPP_EALIGN: return "misaligned pointer";
