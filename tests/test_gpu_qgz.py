@@ -442,6 +442,30 @@ def test_receive_pass_misaligned(zpp, pad):
         assert_bits_equal(a, b, "misaligned pad=%d" % pad)
 
 
+def test_receive_pass_special_scales(zpp):
+    """NaN, Inf, zero and subnormal source scales through the single pass:
+    the blocks they poison quantize as the separate quantizer quantizes them
+    (NaN scale, zero codes), everything else bit for bit as the three calls."""
+    n, block, P = 256 * 8 + 40, 256, 4
+    quants = oracle_sources(P, n, block, 102)
+    quants[1][1][2] = np.nan
+    quants[2][1][3] = np.inf
+    quants[3][1][4] = 0.0
+    quants[0][1][5] = 1e-40
+    quants[2][1][8] = np.nan  # the partial last block
+    ref_state, _ = receive_state(n, 103)
+    got_state, _ = receive_state(n, 103)
+    ref = run_receive_then_refresh_quantize(zpp, quants, n, block, block, 1.0, ref_state, True,
+                                            1, HP, True)
+    got = run_receive_pass(zpp, quants, n, block, block, 1.0, got_state, True, 1, HP, True)
+    names = ("master", "exp_avg", "exp_avg_sq", "primary", "secondary", "codes", "scales")
+    for a, b, name in zip(got, ref, names):
+        assert_bits_equal(a, b, "special scales, " + name)
+    scales = got[6].view(np.uint32)
+    assert scales[2] == 0x7FC00000 and scales[8] == 0x7FC00000, "poisoned blocks keep NaN scales"
+    assert not got[5][2 * 256:3 * 256].any(), "a NaN block's codes are zero"
+
+
 def test_fullsize_receive_pass(zpp):
     """The Llama-2-13B partition from 8 int4 sources: the single pass equals
     the receive step, the refresh and the quantization, compared whole on the
