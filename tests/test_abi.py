@@ -72,9 +72,25 @@ def test_c_driver_is_built_and_links():
         assert lib in out, out
 
 
-def test_hparams_layout(zpp):
-    assert ctypes.sizeof(zpp.AdamHParams) == 32
-    assert zpp.AdamHParams.step.offset == 24
+def test_hparams_layout(zpp, tmp_path):
+    """The binding's mirror of zpp_adam_hparams has the C compiler's layout:
+    the same size and every field at the same offset."""
+    fields = [f for f, _ in zpp.AdamHParams._fields_]
+    src = ('#include <stddef.h>\n#include <stdio.h>\n#include "zpp.h"\nint main(void){\n'
+           '  printf("size %zu\\n", sizeof(zpp_adam_hparams));\n'
+           + "".join('  printf("%s %%zu\\n", offsetof(zpp_adam_hparams, %s));\n' % (f, f)
+                     for f in fields)
+           + '  return 0;\n}\n')
+    exe = str(tmp_path / "layout")
+    r = subprocess.run(["gcc", "-x", "c", "-std=c99", "-D__HIP_PLATFORM_AMD__",
+                        "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", "-",
+                        "-o", exe], input=src, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    got = dict(line.split() for line in subprocess.run(
+        [exe], capture_output=True, text=True, check=True).stdout.splitlines())
+    assert int(got["size"]) == ctypes.sizeof(zpp.AdamHParams) == 32
+    for f in fields:
+        assert int(got[f]) == getattr(zpp.AdamHParams, f).offset, f
 
 
 def test_status_strings(zpp):
