@@ -274,7 +274,9 @@ def refresh_secondary(secondary_bf16, src_bf16, count=None, *, stream=None, wait
 
 
 def num_blocks(n, block):
-    return (n + block - 1) // block
+    """Blocks of `block` elements covering n; 0 for a block size the library
+    rejects anyway (it reports that as ZPP_EINVAL)."""
+    return (n + block - 1) // block if block > 0 else 0
 
 
 def quantize_blockwise_i8(src_bf16, codes, scales, *, block=256, n=None, stream=None,
