@@ -1,0 +1,84 @@
+"""bench.py's host-side logic on the CPU: the one-GPU contract, the lookup of
+counter-measured traffic (valid only while the kernel's sources are the
+ones measured), the per-kernel table, the block-aligned splitting and the
+CPU-baseline leg's record on a tiny sample."""
+import hashlib
+import importlib.util
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def _digest(sources):
+    h = hashlib.sha256()
+    for fn in sources:
+        with open(os.path.join(ROOT, "paper_2407_01614_amd", "csrc", fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def test_measured_traffic_only_for_current_sources(bench, tmp_path):
+    sources = ["adam.hip", "zpp_adam.h", "zpp_device.h"]
+    path = str(tmp_path / "traffic.json")
+    entry = {"bytes_per_launch": 6101178697.4, "source_digest": _digest(sources)}
+    with open(path, "w") as f:
+        json.dump({"workload": "llama-2-13b", "kernels": {"adam": entry}}, f)
+    assert bench.measured_traffic(path, "llama-2-13b", "adam", sources) == 6101178697
+    # another workload, another kernel, or sources changed since the counters were taken
+    assert bench.measured_traffic(path, "llama-2-7b", "adam", sources) is None
+    assert bench.measured_traffic(path, "llama-2-13b", "gather", sources) is None
+    assert bench.measured_traffic(path, "llama-2-13b", "adam", sources[:2]) is None
+    assert bench.measured_traffic(str(tmp_path / "absent.json"), "llama-2-13b", "adam",
+                                  sources) is None
+
+
+def test_kernel_table(bench):
+    kb = {"adam": 6.0e9, "gather": 1.0e9}
+    times = {"adam": [1.0, 0.9, 1.1], "gather": [0.2, 0.2]}  # ms per launch
+    t = bench.kernel_table(kb, times)
+    assert t["adam"]["mean_us"] == 1000.0 and t["adam"]["median_us"] == 1000.0
+    assert t["adam"]["min_us"] == 900.0
+    assert t["adam"]["GB/s"] == 6000.0 and t["adam"]["frac_of_peak"] == 0.75
+    assert t["gather"]["GB/s"] == 5000.0 and t["gather"]["bytes"] == 1.0e9
+
+
+@pytest.mark.parametrize("n,parts,align", [(1000, 3, 256), (256, 8, 256), (1 << 20, 16, 256),
+                                           (257, 2, 256), (5, 4, 1)])
+def test_chunks_cover_in_aligned_ranges(bench, n, parts, align):
+    r = bench._chunks(n, parts, align)
+    assert r[0][0] == 0 and r[-1][1] == n
+    for (a, b), (c, _) in zip(r, r[1:]):
+        assert b == c and b % align == 0
+    assert all(a < b for a, b in r)
+
+
+def test_cpu_baseline_record(bench):
+    from paper_2407_01614_amd.workloads import WORKLOADS
+    wl = WORKLOADS["tiny"]
+    for threads in (1, 2):
+        rec = bench.cpu_baseline(wl, 0.05, threads=threads, steps=2)
+        assert rec["kind"] == "oracle" and rec["unit"] == "GB/s" and rec["cores"] == threads
+        assert rec["value"] > 0
+        assert set(rec["seconds"]) == {"adam", "refresh", "quant", "gather"}
+        assert "2 step(s)" in rec["sample"]
