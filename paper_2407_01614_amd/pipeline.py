@@ -237,18 +237,28 @@ class PartitionPipeline:
         else:
             self._partition_step(t, self.compute)
             self.ev_primary.record(self.compute)
-            zpp.stream_wait(self.copy, self.ev_primary)
+            if self.timing is not None:
+                # the refresh waits on the primary itself (wait_before); a
+                # timed run waits first, so that the start of the timing pair
+                # follows the wait
+                zpp.stream_wait(self.copy, self.ev_primary)
             self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
                 self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary,
                 done_after=self.ev_refresh))
-            if t > 1:
+            if t > 1 and not serial:
+                # the quantization rewrites the codes the last gather read;
+                # in serial order the step already waited for that gather
+                # before the partition step, which the copy stream follows
                 zpp.stream_wait(self.copy, self.ev_gather)
             self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
                 self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
                 done_after=self.ev_quant))
         waits = []
         if self.sync == "event":
-            zpp.stream_wait(self.comm, self.ev_quant)
+            # the gather waits on the quantization itself (the fix, through
+            # wait_events); a timed run waits first, as for the refresh
+            if self.timing is not None:
+                zpp.stream_wait(self.comm, self.ev_quant)
             waits = [self.ev_quant]
         elif self.sync == "host":
             self.ev_quant.synchronize()
