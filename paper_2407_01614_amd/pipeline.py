@@ -107,6 +107,7 @@ class PartitionPipeline:
         self.ev_gather = zpp.Event()
         self.step_count = 0
         self.timing = None
+        self._timing_fence = True
         self._prev_streams = streams
 
     # ------------------------------------------------------------------
@@ -186,16 +187,21 @@ class PartitionPipeline:
     # ------------------------------------------------------------------
     # one iteration
     # ------------------------------------------------------------------
-    def enable_timing(self):
-        """Record a HIP timing-event pair around every kernel, on the stream
-        that kernel runs on."""
-        self.timing = {k: [] for k in self.kernel_bytes()}
+    def enable_timing(self, kernels=None, system_fence=True):
+        """Record a HIP timing-event pair around every kernel (or those named
+        in `kernels`), on the stream that kernel runs on.  With
+        `system_fence=False` the events skip the system-scope fence, so that
+        timing one kernel inside an otherwise uninstrumented run costs the
+        stream next to nothing."""
+        self.timing = {k: [] for k in self.kernel_bytes() if kernels is None or k in kernels}
+        self._timing_fence = system_fence
 
     def _timed(self, name, stream, fn):
-        if self.timing is None:
+        if self.timing is None or name not in self.timing:
             fn()
             return
-        a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+        a = zpp.Event(timing=True, system_fence=self._timing_fence)
+        b = zpp.Event(timing=True, system_fence=self._timing_fence)
         a.record(stream)
         fn()
         b.record(stream)

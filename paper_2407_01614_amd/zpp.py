@@ -106,16 +106,23 @@ def _hip_lib():
 
 HIP_EVENT_DEFAULT = 0x0
 HIP_EVENT_DISABLE_TIMING = 0x2
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
 
 
 class Event:
-    """A HIP event on the current device (timing disabled unless asked)."""
+    """A HIP event on the current device (timing disabled unless asked).
 
-    def __init__(self, timing=False):
+    `system_fence=False` creates it without the system-scope fence of a
+    record: for timing events only, whose records then cost the stream next
+    to nothing; such an event must not order memory for the host."""
+
+    def __init__(self, timing=False, system_fence=True):
         h = _hip_lib()
         ev = _P()
-        err = h.hipEventCreateWithFlags(ctypes.byref(ev),
-                                        HIP_EVENT_DEFAULT if timing else HIP_EVENT_DISABLE_TIMING)
+        flags = HIP_EVENT_DEFAULT if timing else HIP_EVENT_DISABLE_TIMING
+        if not system_fence:
+            flags |= HIP_EVENT_DISABLE_SYSTEM_FENCE
+        err = h.hipEventCreateWithFlags(ctypes.byref(ev), flags)
         if err:
             raise RuntimeError("hipEventCreateWithFlags failed: %d" % err)
         self.handle = ev.value
