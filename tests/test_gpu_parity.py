@@ -122,6 +122,36 @@ def test_adam_large_step_count(zpp):
     assert_adam_close(got, ref, hp["lr"], prev=(p, m, v), g=g, hp=hp)
 
 
+DEGENERATE = {
+    "lr=0": dict(lr=0.0, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1),
+    "wd=0": dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0),
+    "beta1=0": dict(lr=1e-3, beta1=0.0, beta2=0.95, eps=1e-8, weight_decay=0.1),
+    "beta2=0": dict(lr=1e-3, beta1=0.9, beta2=0.0, eps=1e-8, weight_decay=0.1),
+    "betas=0": dict(lr=1e-3, beta1=0.0, beta2=0.0, eps=1e-8, weight_decay=0.1),
+    "eps=0": dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=0.0, weight_decay=0.1),
+}
+
+
+@pytest.mark.parametrize("adamw", [True, False], ids=["adamw", "l2"])
+@pytest.mark.parametrize("case", sorted(DEGENERATE))
+def test_adam_degenerate_hyperparameters(zpp, case, adamw):
+    """Hyperparameters at the edges the method allows, from a mid-training
+    state (step 3, nonzero moments): a zero learning rate leaves the master
+    bit for bit; zero decay, betas of 0 (no momentum: m = g, v = g^2) and a
+    zero eps all match the oracle."""
+    hp = f32hp(DEGENERATE[case])
+    n = 256 * 37 + 11
+    p = synth.master_weights(n, 44)
+    g = synth.gradients(n, 44)
+    m, v = synth.moments(n, 44)
+    got = run_adam_gpu(zpp, p, m, v, g, hp, 3, adamw=adamw)
+    ref = oracle.adam_step(p, m, v, g, step=3, adamw=adamw, **hp)
+    assert_adam_close(got, ref, hp["lr"], case, prev=(p, m, v), g=g, hp=hp, adamw=adamw)
+    if hp["lr"] == 0.0:
+        assert_bits_equal(got[0], p, "master with lr = 0")
+        assert_bits_equal(got[3], ref[3], "primary with lr = 0")
+
+
 def test_adam_checkpoint_resume_is_bitwise(zpp):
     """k steps, save the state to the host, reload it into fresh buffers and
     take one more step: bit-identical to k+1 uninterrupted steps."""

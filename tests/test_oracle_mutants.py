@@ -16,7 +16,7 @@ import test_oracle_pins as pins
 
 BF16 = [pins.check_bf16_rne, pins.check_adam_step1_closed_form, pins.check_dequant_vs_library]
 ADAM = [pins.check_adam_step1_closed_form, pins.check_adam_vs_torch,
-        pins.check_adam_multistep_vs_torch]
+        pins.check_adam_multistep_vs_torch, pins.check_adam_zero_betas_closed_form]
 QUANT = [pins.check_quant_integer_blocks, pins.check_quant_ties_to_even,
          pins.check_quant_nearest_code, pins.check_quant_symmetry_and_scaling,
          pins.check_quant_special_blocks, pins.check_quant_block_boundaries,

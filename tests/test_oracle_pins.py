@@ -6,8 +6,9 @@ see them fail.  Pins used:
   * bf16 rounding: torch's CPU float32 -> bfloat16 conversion (a library RNE
     routine), exhaustive over all 2^16 bf16 patterns for the reverse way;
   * Adam: the closed form of step 1 from zero moments (m_hat = g,
-    v_hat = g^2), and torch.optim.AdamW / Adam (float64, single-tensor path)
-    as an independent implementation at arbitrary steps and states;
+    v_hat = g^2), the same closed form at any step from any moments when
+    both betas are 0, and torch.optim.AdamW / Adam (float64, single-tensor
+    path) as an independent implementation at arbitrary steps and states;
   * quantization: exact integer constructions (codes known in advance),
     power-of-two scaling, ties-to-even cases, sign symmetry, an error bound
     checked in exact rational arithmetic, special blocks;
@@ -167,6 +168,39 @@ def check_adam_step1_closed_form(orc):
 
 def test_adam_step1_closed_form():
     check_adam_step1_closed_form(oracle.default())
+
+
+def check_adam_zero_betas_closed_form(orc):
+    """With beta1 = beta2 = 0 the moments are the step's own gradient and its
+    square and both bias corrections are 1, so any step t from any moments
+    reduces to the step-1 closed form (with m1 = g', v1 = g'^2, where g' is
+    the gradient, plus wd p0 in the L2 form)."""
+    rng = np.random.default_rng(17)
+    n = 1 << 12
+    base = hp32(HP_LOUD)
+    hp = dict(base, beta1=0.0, beta2=0.0)
+    for adamw in (True, False):
+        for t in (1, 2, 7, 1000):
+            p0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+            g = (rng.standard_normal(n) * 10.0 ** rng.uniform(-6, -2, n)).astype(np.float32)
+            m0 = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+            v0 = (rng.standard_normal(n) * 1e-3).astype(np.float32) ** 2
+            p1, m1, v1, _ = orc.adam_step(p0, m0, v0, g, step=t, adamw=adamw, **hp)
+            lr, eps, wd = hp["lr"], hp["eps"], hp["weight_decay"]
+            p64, g64 = p0.astype(np.float64), g.astype(np.float64)
+            if adamw:
+                gg = g64
+                ep = p64 * (1.0 - lr * wd) - lr * gg / (np.abs(gg) + eps)
+            else:
+                gg = g64 + wd * p64
+                ep = p64 - lr * gg / (np.abs(gg) + eps)
+            assert ulp_diff_f32(p1, ep.astype(np.float32)).max() <= 1, (adamw, t)
+            assert ulp_diff_f32(m1, gg.astype(np.float32)).max() <= 1, (adamw, t)
+            assert ulp_diff_f32(v1, (gg * gg).astype(np.float32)).max() <= 1, (adamw, t)
+
+
+def test_adam_zero_betas_closed_form():
+    check_adam_zero_betas_closed_form(oracle.default())
 
 
 def test_adam_zero_grad_only_decays():
