@@ -22,7 +22,8 @@ three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
 timing only), the qgZ gradient side, the step preceded by the qgZ receive
 (as its own kernel, fused into the partition step, and inside the single
-pass of step, refresh and quantization), and, for context,
+pass of step, refresh and quantization; the last two also with the eight
+int4 copies interleaved in one receive buffer), and, for context,
 PyTorch's fused AdamW on a partition of the same size.  The
 CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
@@ -408,6 +409,19 @@ def main():
     fr_gbps = fr_step_bytes / (fr_ms * 1e-3) / 1e9
     ff_ms, ff_times, ff_kb, ff_step_bytes = run(True, "event", True)
     ff_gbps = ff_step_bytes / (ff_ms * 1e-3) / 1e9
+    # both again with the 8 copies interleaved in one receive buffer
+    pipe.exchange = None
+    torch.cuda.empty_cache()
+    pipe.exchange = GradientExchange(wl.n, 8, wl.block, interleaved=True)
+    for q in range(8):
+        g = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id, _synth.KIND_GRAD, rank=q)
+        pipe.exchange.quantize(q, g)
+        del g
+    torch.cuda.synchronize()
+    il_ms, il_times, il_kb, il_step_bytes = run(False, "event", True)
+    il_gbps = il_step_bytes / (il_ms * 1e-3) / 1e9
+    ilf_ms, ilf_times, ilf_kb, ilf_step_bytes = run(True, "event", True)
+    ilf_gbps = ilf_step_bytes / (ilf_ms * 1e-3) / 1e9
     pipe.fuse_receive = False
     pipe.exchange = None
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -480,6 +494,14 @@ def main():
             "ms_per_step": round(ff_ms, 4), "GB/s": round(ff_gbps, 1),
             "frac_of_peak": round(ff_gbps / HBM_PEAK_GBPS, 4),
             "kernels": kernel_table(ff_kb, ff_times)},
+        "step_with_fused_qgz_receive_interleaved": {
+            "ms_per_step": round(il_ms, 4), "GB/s": round(il_gbps, 1),
+            "frac_of_peak": round(il_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(il_kb, il_times)},
+        "step_with_qgz_receive_single_pass_interleaved": {
+            "ms_per_step": round(ilf_ms, 4), "GB/s": round(ilf_gbps, 1),
+            "frac_of_peak": round(ilf_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(ilf_kb, ilf_times)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
         "gpu": {"name": torch.cuda.get_device_name(0),
                 "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,

@@ -290,6 +290,59 @@ ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
     uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
     uint32_t num_wait, hipEvent_t done_after);
 
+/* The qgZ receive buffer interleaved: the num_src int4 copies of an n-element
+ * partition in ONE buffer, block by block, instead of num_src separate
+ * arrays.  With B = the int4 block and k = i / B:
+ *   source q's code of element i: byte (k * num_src + q) * B/2 + (i mod B)/2,
+ *       low nibble for even i, high nibble for odd i (packing as
+ *       zpp_quantize_blockwise_i4);
+ *   source q's scale of block k:  float (k * num_src + q).
+ * Codes: uint8_t[ceil(n/B) * num_src * B/2]; scales:
+ * float[ceil(n/B) * num_src].  With num_src = 1 it is the plain layout of
+ * zpp_quantize_blockwise_i4.  A receiving kernel then reads each block's
+ * codes of all sources within one contiguous run rather than from num_src
+ * separate arrays.  The exchange that fills it (each sending rank writing its
+ * slots, e.g. by peer stores within a node) is not part of this library;
+ * zpp_quantize_blockwise_i4_interleaved writes one source's slots. */
+
+/* zpp_quantize_blockwise_i4 (same blocks, scales, codes and rules) writing
+ * source `source` of num_src into an interleaved receive buffer (layout
+ * above); the other sources' slots are left as they are.  num_src in
+ * [1, ZPP_MAX_SHARDS], source < num_src, n <= SIZE_MAX / 16 / num_src.
+ * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
+ * No two of src, the codes buffer and the scales buffer may overlap
+ * (ZPP_EOVERLAP).  Alignment: src and scales 4 bytes (ZPP_EALIGN); 16-byte
+ * src and 2-byte codes select the vector kernel. */
+ZPP_API zpp_status zpp_quantize_blockwise_i4_interleaved(const float *src, size_t n,
+                                                         uint32_t block, uint32_t source,
+                                                         uint32_t num_src, uint8_t *codes,
+                                                         float *scales, hipStream_t stream,
+                                                         hipEvent_t wait_before,
+                                                         hipEvent_t done_after);
+
+/* zpp_qgz_receive_adam_step with its num_src int4 copies in one interleaved
+ * receive buffer (layout above): the same arithmetic in the same order, so
+ * the same bits.  codes, scales: DEVICE pointers to the interleaved buffer,
+ * B = block.  n <= SIZE_MAX / 16 / num_src.  Everything else as for
+ * zpp_qgz_receive_adam_step, alignment included; the two input ranges may
+ * overlap each other, not an output. */
+ZPP_API zpp_status zpp_qgz_receive_adam_step_interleaved(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *codes, const float *scales,
+    uint32_t num_src, uint32_t block, float scale_out, uint16_t *primary_bf16, size_t n,
+    const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after);
+
+/* zpp_qgz_receive_step_refresh_quantize with its num_src int4 copies in one
+ * interleaved receive buffer (src_codes, src_scales; layout above, B =
+ * grad_block): the same bits.  Everything else as there, alignment
+ * included. */
+ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize_interleaved(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *src_codes,
+    const float *src_scales, uint32_t num_src, uint32_t grad_block, float scale_out,
+    uint16_t *primary_bf16, uint16_t *secondary_bf16, int8_t *codes, float *scales, size_t n,
+    uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after);
+
 /* Static, NUL-terminated description of a status code.  Takes any int, so
  * that a caller may pass whatever status value it holds: a value that is not
  * one of zpp_status gives "unknown status". */

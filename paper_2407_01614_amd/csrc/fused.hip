@@ -33,6 +33,9 @@
 #ifndef ZPP_FUSED_RECV_RESIDENCY
 #define ZPP_FUSED_RECV_RESIDENCY 13
 #endif
+#ifndef ZPP_FUSED_RECV_IL_RESIDENCY
+#define ZPP_FUSED_RECV_IL_RESIDENCY 14
+#endif
 #ifndef ZPP_FUSED_MAX_GRID
 #define ZPP_FUSED_MAX_GRID (1u << 30)
 #endif
@@ -138,6 +141,7 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a, GS gs) {
 template <class GS> constexpr int fused_residency();
 template <> constexpr int fused_residency<F32Grad>() { return ZPP_FUSED_RESIDENCY; }
 template <> constexpr int fused_residency<I4Grad>() { return ZPP_FUSED_RECV_RESIDENCY; }
+template <> constexpr int fused_residency<I4GradIl>() { return ZPP_FUSED_RECV_IL_RESIDENCY; }
 
 template <int B, class GS>
 void launch_fused_b(const FusedArgs &a, const GS &gs, hipStream_t stream) {
@@ -208,6 +212,27 @@ hipError_t launch_fused_receive(float *p, float *m, float *v, const uint8_t *con
     }
     const FusedArgs a{p, m, v, primary, secondary, codes, scales, n, c};
     return launch_fused_gs(a, make_i4grad(src_codes, src_scales, num_src, grad_block, scale_out),
+                           block, stream);
+}
+
+hipError_t launch_fused_receive_il(float *p, float *m, float *v, const uint8_t *src_codes,
+                                   const float *src_scales, uint32_t num_src, uint32_t grad_block,
+                                   float scale_out, uint16_t *primary, uint16_t *secondary,
+                                   int8_t *codes, float *scales, size_t n, uint32_t block,
+                                   const AdamConsts &c, bool vector_path, hipStream_t stream) {
+    if (!vector_path) {
+        // any alignment: the receive step, the refresh and the quantization
+        // as scalar kernels, one after another on the stream
+        hipError_t e = launch_receive_adam_il(p, m, v, src_codes, src_scales, num_src, grad_block,
+                                              scale_out, primary, n, c, false, stream);
+        if (e == hipSuccess && secondary)
+            e = launch_refresh(secondary, primary, n, false, stream);
+        if (e == hipSuccess)
+            e = launch_quantize(primary, n, block, codes, scales, false, stream);
+        return e;
+    }
+    const FusedArgs a{p, m, v, primary, secondary, codes, scales, n, c};
+    return launch_fused_gs(a, make_i4grad_il(src_codes, src_scales, num_src, grad_block, scale_out),
                            block, stream);
 }
 

@@ -91,16 +91,24 @@ __device__ __forceinline__ uint32_t abs_bits_max4(const f32x4 &v) {
 // and every code store writes 128 contiguous bytes.  A block of B values
 // spans L = min(B/4, 64) lanes and G = max(1, B/256) groups per lane; a
 // wave covers C = max(B, 256) values per tile and keeps U tiles in flight.
+// Where the codes and scale of one source go in a receive buffer of P
+// sources interleaved block by block (block k of B elements: source q's B/2
+// code bytes at (k P + q) B/2, its scale at k P + q); P = 1, q = 0 is the
+// plain layout (byte i / 2, scale k).
+__device__ __forceinline__ size_t i4_out_byte(size_t i, uint32_t shift, uint32_t q, uint32_t P) {
+    return (((i >> shift) * P + q) << (shift - 1)) + ((i & (((size_t)1 << shift) - 1)) >> 1);
+}
+
 template <int B, int U>
 __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
     const float *__restrict__ src, size_t n, uint8_t *__restrict__ codes,
-    float *__restrict__ scales) {
+    float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
+    constexpr uint32_t kShift = __builtin_ctz(B);
     constexpr int C = B > 256 ? B : 256;
     constexpr int G = C / 256;
     constexpr int L = B < 256 ? B / 4 : kWave;
     constexpr int kWaves = kQgzThreads / kWave;
     const size_t ntiles = (n + C - 1) / C;
-    const size_t nbytes = (n + 1) / 2;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     for (size_t t0 = ((size_t)blockIdx.x * kWaves + wave) * U; t0 < ntiles;
@@ -138,16 +146,17 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
                 for (int g = 0; g < G; ++g) {
                     const size_t i = tile * C + (size_t)g * 256 + (size_t)lane * 4;
                     const uint32_t h = i4_half(x[u][g], q);
-                    const size_t byte0 = i / 2;
-                    if (byte0 + 2 <= nbytes) {
+                    const size_t byte0 = i4_out_byte(i, kShift, q_src, num_src);
+                    // the second byte holds elements i + 2 and i + 3
+                    if (i + 2 < n) {
                         st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
-                    } else if (byte0 < nbytes) {
+                    } else if (i < n) {
                         codes[byte0] = (uint8_t)h;
                     }
                 }
                 const size_t k = (tile * C + (size_t)lane * 4) / B;
                 if (lane % L == 0 && k * B < n)
-                    scales[k] = q.scale;
+                    scales[k * num_src + q_src] = q.scale;
             }
         }
     }
@@ -157,7 +166,8 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
 // byte is written by the lane that owns its even element.
 __global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(
     const float *__restrict__ src, size_t n, uint32_t block, uint8_t *__restrict__ codes,
-    float *__restrict__ scales) {
+    float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
+    const uint32_t shift = __builtin_ctz(block);
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
     const size_t wave0 = (size_t)blockIdx.x * (kQgzThreads / kWave) + threadIdx.x / kWave;
@@ -176,10 +186,10 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(
             const float x0 = src[i];
             const float x1 = (i + 1 < hi) ? src[i + 1] : 0.0f;
             const uint32_t h = i4_half(f32x4{x0, x1, 0.0f, 0.0f}, q);
-            codes[i / 2] = (uint8_t)(h & 0xFFu);
+            codes[i4_out_byte(i, shift, q_src, num_src)] = (uint8_t)(h & 0xFFu);
         }
         if (lane == 0)
-            scales[k] = q.scale;
+            scales[k * num_src + q_src] = q.scale;
     }
 }
 
@@ -285,29 +295,30 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_scalar_kernel(ReduceArg
 
 template <int B>
 void launch_quant_i4_b(const float *src, size_t n, uint8_t *codes, float *scales,
-                       hipStream_t stream) {
+                       uint32_t q_src, uint32_t num_src, hipStream_t stream) {
     constexpr size_t C = B > 256 ? B : 256;
     constexpr size_t kTilesPerBlock = (kQgzThreads / kWave) * ZPP_QGZ_QUANT_UNROLL;
     const size_t ntiles = (n + C - 1) / C;
     const size_t need = (ntiles + kTilesPerBlock - 1) / kTilesPerBlock;
     const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
     hipLaunchKernelGGL((quant_i4_kernel<B, ZPP_QGZ_QUANT_UNROLL>), dim3(grid), dim3(kQgzThreads),
-                       0, stream, src, n, codes, scales);
+                       0, stream, src, n, codes, scales, q_src, num_src);
 }
 
 }  // namespace
 
-hipError_t launch_quantize_i4(const float *src, size_t n, uint32_t block, uint8_t *codes,
-                              float *scales, bool vector_path, hipStream_t stream) {
+hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uint32_t source,
+                                 uint32_t num_src, uint8_t *codes, float *scales,
+                                 bool vector_path, hipStream_t stream) {
     if (vector_path) {
         switch (block) {
-        case 64: launch_quant_i4_b<64>(src, n, codes, scales, stream); break;
-        case 128: launch_quant_i4_b<128>(src, n, codes, scales, stream); break;
-        case 256: launch_quant_i4_b<256>(src, n, codes, scales, stream); break;
-        case 512: launch_quant_i4_b<512>(src, n, codes, scales, stream); break;
-        case 1024: launch_quant_i4_b<1024>(src, n, codes, scales, stream); break;
-        case 2048: launch_quant_i4_b<2048>(src, n, codes, scales, stream); break;
-        case 4096: launch_quant_i4_b<4096>(src, n, codes, scales, stream); break;
+        case 64: launch_quant_i4_b<64>(src, n, codes, scales, source, num_src, stream); break;
+        case 128: launch_quant_i4_b<128>(src, n, codes, scales, source, num_src, stream); break;
+        case 256: launch_quant_i4_b<256>(src, n, codes, scales, source, num_src, stream); break;
+        case 512: launch_quant_i4_b<512>(src, n, codes, scales, source, num_src, stream); break;
+        case 1024: launch_quant_i4_b<1024>(src, n, codes, scales, source, num_src, stream); break;
+        case 2048: launch_quant_i4_b<2048>(src, n, codes, scales, source, num_src, stream); break;
+        case 4096: launch_quant_i4_b<4096>(src, n, codes, scales, source, num_src, stream); break;
         default: return hipErrorInvalidValue;
         }
     } else {
@@ -315,9 +326,14 @@ hipError_t launch_quantize_i4(const float *src, size_t n, uint32_t block, uint8_
         const size_t need = (nblocks + (kQgzThreads / kWave) - 1) / (kQgzThreads / kWave);
         const unsigned grid = (unsigned)(need < (1u << 20) ? need : (1u << 20));
         hipLaunchKernelGGL(quant_i4_scalar_kernel, dim3(grid), dim3(kQgzThreads), 0, stream, src,
-                           n, block, codes, scales);
+                           n, block, codes, scales, source, num_src);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_quantize_i4(const float *src, size_t n, uint32_t block, uint8_t *codes,
+                              float *scales, bool vector_path, hipStream_t stream) {
+    return launch_quantize_i4_il(src, n, block, 0, 1, codes, scales, vector_path, stream);
 }
 
 hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,

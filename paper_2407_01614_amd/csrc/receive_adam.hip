@@ -31,6 +31,9 @@
 #ifndef ZPP_RECV_RESIDENCY
 #define ZPP_RECV_RESIDENCY 12
 #endif
+#ifndef ZPP_RECV_IL_RESIDENCY
+#define ZPP_RECV_IL_RESIDENCY 12
+#endif
 #ifndef ZPP_RECV_MAX_GRID
 #define ZPP_RECV_MAX_GRID (1u << 30)
 #endif
@@ -38,17 +41,20 @@
 namespace zpp {
 namespace {
 
+// The gradient comes from `src`: the P int4 copies as separate arrays
+// (I4Grad) or interleaved in one receive buffer (I4GradIl, zpp_i4grad.h).
+template <class GS>
 struct RecvArgs {
-    I4Grad src;
+    GS src;
     float *p, *m, *v;
     uint16_t *out;
     size_t n;
     AdamConsts c;
 };
 
-template <bool ADAMW>
-__device__ __forceinline__ void scalar_step(const RecvArgs &a, size_t i) {
-    const float g = i4grad_at(a.src, i);
+template <bool ADAMW, class GS>
+__device__ __forceinline__ void scalar_step(const RecvArgs<GS> &a, size_t i) {
+    const float g = grad_at(a.src, i);
     float p = a.p[i], m = a.m[i], v = a.v[i];
     adam_update<ADAMW>(p, m, v, g, a.c);
     a.p[i] = p;
@@ -57,8 +63,8 @@ __device__ __forceinline__ void scalar_step(const RecvArgs &a, size_t i) {
     a.out[i] = (uint16_t)bf16_rne_bits(p);
 }
 
-template <bool ADAMW>
-__global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs a) {
+template <bool ADAMW, class GS>
+__global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs<GS> a) {
     const size_t ntiles = (a.n + 255) / 256;
     const int lane = threadIdx.x;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -67,13 +73,13 @@ __global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs a) {
             // the last, partial tile: element by element
             for (int e = 0; e < 4; ++e)
                 if (i + e < a.n)
-                    scalar_step<ADAMW>(a, i + e);
+                    scalar_step<ADAMW, GS>(a, i + e);
             continue;
         }
         f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
         f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
         f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
-        const f32x4 G = i4grad_load4(a.src, i);
+        const f32x4 G = grad_load4(a.src, i);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             float p = P[e], m = M[e], v = V[e];
@@ -93,11 +99,37 @@ __global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs a) {
 }
 
 // Any alignment: one element per thread, grid-stride.
-template <bool ADAMW>
-__global__ __launch_bounds__(kThreads) void recv_adam_scalar_kernel(RecvArgs a) {
+template <bool ADAMW, class GS>
+__global__ __launch_bounds__(kThreads) void recv_adam_scalar_kernel(RecvArgs<GS> a) {
     const size_t stride = (size_t)gridDim.x * kThreads;
     for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < a.n; i += stride)
-        scalar_step<ADAMW>(a, i);
+        scalar_step<ADAMW, GS>(a, i);
+}
+
+template <class GS>
+hipError_t launch_recv(const RecvArgs<GS> &a, int residency, bool vector_path,
+                       hipStream_t stream) {
+    if (vector_path) {
+        const size_t tiles = (a.n + 255) / 256;
+        const unsigned grid = (unsigned)(tiles < ZPP_RECV_MAX_GRID ? tiles : ZPP_RECV_MAX_GRID);
+        const size_t lds = residency_lds(residency);
+        if (a.c.adamw)
+            hipLaunchKernelGGL((recv_adam_kernel<true, GS>), dim3(grid), dim3(kWave), lds, stream,
+                               a);
+        else
+            hipLaunchKernelGGL((recv_adam_kernel<false, GS>), dim3(grid), dim3(kWave), lds,
+                               stream, a);
+    } else {
+        const size_t blocks = (a.n + kThreads - 1) / kThreads;
+        const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
+        if (a.c.adamw)
+            hipLaunchKernelGGL((recv_adam_scalar_kernel<true, GS>), dim3(grid), dim3(kThreads), 0,
+                               stream, a);
+        else
+            hipLaunchKernelGGL((recv_adam_scalar_kernel<false, GS>), dim3(grid), dim3(kThreads),
+                               0, stream, a);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -119,7 +151,7 @@ hipError_t launch_receive_adam(float *p, float *m, float *v, const uint8_t *cons
                                const float *const *src_scales, uint32_t num_src, uint32_t block,
                                float scale_out, uint16_t *out, size_t n, const AdamConsts &c,
                                bool vector_path, hipStream_t stream) {
-    RecvArgs a = {};
+    RecvArgs<I4Grad> a = {};
     a.src = make_i4grad(src_codes, src_scales, num_src, block, scale_out);
     a.p = p;
     a.m = m;
@@ -127,25 +159,33 @@ hipError_t launch_receive_adam(float *p, float *m, float *v, const uint8_t *cons
     a.out = out;
     a.n = n;
     a.c = c;
-    if (vector_path) {
-        const size_t tiles = (n + 255) / 256;
-        const unsigned grid = (unsigned)(tiles < ZPP_RECV_MAX_GRID ? tiles : ZPP_RECV_MAX_GRID);
-        constexpr size_t lds = residency_lds(ZPP_RECV_RESIDENCY);
-        if (c.adamw)
-            hipLaunchKernelGGL((recv_adam_kernel<true>), dim3(grid), dim3(kWave), lds, stream, a);
-        else
-            hipLaunchKernelGGL((recv_adam_kernel<false>), dim3(grid), dim3(kWave), lds, stream, a);
-    } else {
-        const size_t blocks = (n + kThreads - 1) / kThreads;
-        const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
-        if (c.adamw)
-            hipLaunchKernelGGL((recv_adam_scalar_kernel<true>), dim3(grid), dim3(kThreads), 0,
-                               stream, a);
-        else
-            hipLaunchKernelGGL((recv_adam_scalar_kernel<false>), dim3(grid), dim3(kThreads), 0,
-                               stream, a);
-    }
-    return hipGetLastError();
+    return launch_recv(a, ZPP_RECV_RESIDENCY, vector_path, stream);
+}
+
+I4GradIl make_i4grad_il(const uint8_t *codes, const float *scales, uint32_t num_src,
+                        uint32_t block, float scale_out) {
+    I4GradIl s = {};
+    s.codes = codes;
+    s.scales = scales;
+    s.num_src = num_src;
+    s.block_shift = (uint32_t)__builtin_ctz(block);
+    s.scale_out = scale_out;
+    return s;
+}
+
+hipError_t launch_receive_adam_il(float *p, float *m, float *v, const uint8_t *codes,
+                                  const float *scales, uint32_t num_src, uint32_t block,
+                                  float scale_out, uint16_t *out, size_t n, const AdamConsts &c,
+                                  bool vector_path, hipStream_t stream) {
+    RecvArgs<I4GradIl> a = {};
+    a.src = make_i4grad_il(codes, scales, num_src, block, scale_out);
+    a.p = p;
+    a.m = m;
+    a.v = v;
+    a.out = out;
+    a.n = n;
+    a.c = c;
+    return launch_recv(a, ZPP_RECV_IL_RESIDENCY, vector_path, stream);
 }
 
 }  // namespace zpp

@@ -79,6 +79,15 @@ zpp_status wait_on(hipStream_t stream, hipEvent_t ev) {
     return e == hipSuccess ? ZPP_OK : hip_fail(e);
 }
 
+// Bytes of codes and count of scales of an interleaved receive buffer of
+// num_src int4 copies of n elements in blocks of `block`.
+size_t il_code_bytes(size_t n, uint32_t block, uint32_t num_src) {
+    return (n + block - 1) / block * num_src * (block / 2);
+}
+size_t il_scale_count(size_t n, uint32_t block, uint32_t num_src) {
+    return (n + block - 1) / block * num_src;
+}
+
 zpp_status record(hipStream_t stream, hipEvent_t ev) {
     if (!ev)
         return ZPP_OK;
@@ -467,6 +476,154 @@ ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize(
     }
     if (n) {
         const hipError_t e = zpp::launch_fused_receive(
+            master, exp_avg, exp_avg_sq, src_codes, src_scales, num_src, grad_block, scale_out,
+            primary_bf16, secondary_bf16, codes, scales, n, block, adam_consts(*hp), vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_quantize_blockwise_i4_interleaved(const float *src, size_t n,
+                                                         uint32_t block, uint32_t source,
+                                                         uint32_t num_src, uint8_t *codes,
+                                                         float *scales, hipStream_t stream,
+                                                         hipEvent_t wait_before,
+                                                         hipEvent_t done_after) {
+    if (!valid_block(block) || num_src == 0 || num_src > ZPP_MAX_SHARDS || source >= num_src)
+        return ZPP_EINVAL;
+    if (n > kMaxElems / num_src)
+        return ZPP_EINVAL;
+    if (n) {
+        if (!src || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(src, 4) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const void *ptrs[3] = {src, codes, scales};
+        const size_t bytes[3] = {4 * n, il_code_bytes(n, block, num_src),
+                                 4 * il_scale_count(n, block, num_src)};
+        if (any_overlap(ptrs, bytes, 3))
+            return ZPP_EOVERLAP;
+    }
+    zpp_status st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (n) {
+        const bool vec = aligned(src, 16) && aligned(codes, 2);
+        const hipError_t e = zpp::launch_quantize_i4_il(src, n, block, source, num_src, codes,
+                                                        scales, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_qgz_receive_adam_step_interleaved(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *codes, const float *scales,
+    uint32_t num_src, uint32_t block, float scale_out, uint16_t *primary_bf16, size_t n,
+    const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after) {
+    zpp_status st = check_hparams(hp);
+    if (st != ZPP_OK)
+        return st;
+    if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(block))
+        return ZPP_EINVAL;
+    if (n > kMaxElems / num_src || !isfinite(scale_out))
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!codes || !scales)
+        return ZPP_EINVAL;
+    if (!aligned(scales, 4))
+        return ZPP_EALIGN;
+    if (n) {
+        if (!master || !exp_avg || !exp_avg_sq || !primary_bf16)
+            return ZPP_EINVAL;
+        if (!aligned(master, 4) || !aligned(exp_avg, 4) || !aligned(exp_avg_sq, 4) ||
+            !aligned(primary_bf16, 2))
+            return ZPP_EALIGN;
+        const void *ptrs[6] = {master, exp_avg, exp_avg_sq, primary_bf16, codes, scales};
+        const size_t bytes[6] = {4 * n, 4 * n, 4 * n, 2 * n, il_code_bytes(n, block, num_src),
+                                 4 * il_scale_count(n, block, num_src)};
+        // the two inputs may share bytes with each other, not with an output
+        for (int o = 0; o < 4; ++o)
+            for (int x = o + 1; x < 6; ++x)
+                if (overlaps(ptrs[o], bytes[o], ptrs[x], bytes[x]))
+                    return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (n) {
+        const bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
+                         aligned(primary_bf16, 8) && aligned(codes, 2);
+        const hipError_t e = zpp::launch_receive_adam_il(master, exp_avg, exp_avg_sq, codes,
+                                                         scales, num_src, block, scale_out,
+                                                         primary_bf16, n, adam_consts(*hp), vec,
+                                                         stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
+ZPP_API zpp_status zpp_qgz_receive_step_refresh_quantize_interleaved(
+    float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *src_codes,
+    const float *src_scales, uint32_t num_src, uint32_t grad_block, float scale_out,
+    uint16_t *primary_bf16, uint16_t *secondary_bf16, int8_t *codes, float *scales, size_t n,
+    uint32_t block, const zpp_adam_hparams *hp, hipStream_t stream, const hipEvent_t *wait_events,
+    uint32_t num_wait, hipEvent_t done_after) {
+    zpp_status st = check_hparams(hp);
+    if (st != ZPP_OK)
+        return st;
+    if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(grad_block) ||
+        !valid_block(block))
+        return ZPP_EINVAL;
+    if (n > kMaxElems / num_src || !isfinite(scale_out))
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!src_codes || !src_scales)
+        return ZPP_EINVAL;
+    if (!aligned(src_scales, 4))
+        return ZPP_EALIGN;
+    if (n) {
+        if (!master || !exp_avg || !exp_avg_sq || !primary_bf16 || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(master, 4) || !aligned(exp_avg, 4) || !aligned(exp_avg_sq, 4) ||
+            !aligned(primary_bf16, 2) || !aligned(secondary_bf16, 2) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const size_t nblocks = (n + block - 1) / block;
+        const void *ptrs[9] = {master, exp_avg, exp_avg_sq, primary_bf16, codes, scales,
+                               secondary_bf16, src_codes, src_scales};
+        const size_t bytes[9] = {4 * n, 4 * n, 4 * n, 2 * n, n, 4 * nblocks,
+                                 secondary_bf16 ? 2 * n : 0,
+                                 il_code_bytes(n, grad_block, num_src),
+                                 4 * il_scale_count(n, grad_block, num_src)};
+        // the two inputs may share bytes with each other, not with an output
+        for (int o = 0; o < 7; ++o)
+            for (int x = o + 1; x < 9; ++x)
+                if (overlaps(ptrs[o], bytes[o], ptrs[x], bytes[x]))
+                    return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (n) {
+        const bool vec = aligned(master, 16) && aligned(exp_avg, 16) && aligned(exp_avg_sq, 16) &&
+                         aligned(primary_bf16, 8) && aligned(secondary_bf16, 8) &&
+                         aligned(codes, 4) && aligned(src_codes, 2);
+        const hipError_t e = zpp::launch_fused_receive_il(
             master, exp_avg, exp_avg_sq, src_codes, src_scales, num_src, grad_block, scale_out,
             primary_bf16, secondary_bf16, codes, scales, n, block, adam_consts(*hp), vec, stream);
         if (e != hipSuccess)

@@ -50,7 +50,7 @@ constexpr size_t residency_lds(int workgroups_per_cu) {
     return workgroups_per_cu <= 0 ? 0 : (kLdsPerCU / workgroups_per_cu) / 1024 * 1024;
 }
 static_assert(kLdsPerCU / residency_lds(11) == 11 && kLdsPerCU / residency_lds(12) == 12 &&
-                  kLdsPerCU / residency_lds(13) == 13,
+                  kLdsPerCU / residency_lds(13) == 13 && kLdsPerCU / residency_lds(14) == 14,
               "a reservation caps residency at exactly the requested count");
 
 // Streaming accesses: every byte is touched once, so loads and stores are

@@ -73,6 +73,78 @@ __device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
                  i4grad_scaled(acc[2], s.scale_out), i4grad_scaled(acc[3], s.scale_out)};
 }
 
+// The same P int4 copies interleaved in one receive buffer: for each block k
+// of B = 2^block_shift elements the sources' codes lie side by side (source
+// q's B/2 bytes at (k P + q) B/2) and so do their scales (source q's at
+// k P + q).  P = 1 is the plain layout of one copy.  A wave's 256-element
+// tile then reads all its codes within one run of P x 128 bytes (blocks of
+// 256 or fewer) instead of from P separate arrays.  The gradient is formed in
+// the same order with the same operations as from separate arrays, so the
+// results are the same bits.
+struct I4GradIl {
+    const uint8_t *codes;
+    const float *scales;
+    uint32_t num_src;
+    uint32_t block_shift;
+    float scale_out;
+};
+
+// Byte offset of element i's code of source q (element i is in the low nibble
+// when i is even).
+__device__ __forceinline__ size_t il_code_byte(const I4GradIl &s, size_t i, uint32_t q) {
+    const size_t mask = ((size_t)1 << s.block_shift) - 1;
+    return ((((i >> s.block_shift) * s.num_src + q)) << (s.block_shift - 1)) + ((i & mask) >> 1);
+}
+
+__device__ __forceinline__ float i4grad_at(const I4GradIl &s, size_t i) {
+    float acc = 0.0f;
+    const size_t k = i >> s.block_shift;
+    for (uint32_t q = 0; q < s.num_src; ++q) {
+        const uint32_t byte = s.codes[il_code_byte(s, i, q)];
+        const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
+        acc = __builtin_fmaf(i4_code(nib, 0), s.scales[k * s.num_src + q], acc);
+    }
+    return i4grad_scaled(acc, s.scale_out);
+}
+
+// The gradient of the four consecutive elements i .. i+3 (i a multiple of 4,
+// all four in range): the loads of the separate layout (a 2-byte code load
+// and a scale per source, sources eight at a time, all loads in flight before
+// the fma passes, which keep the source order), addressed in the interleaved
+// buffer: a wave's loads of one source are 128 contiguous bytes, and those of
+// all sources lie within one run of the buffer.
+__device__ __forceinline__ f32x4 i4grad_load4(const I4GradIl &s, size_t i) {
+    constexpr int kBatch = 8;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const size_t k = i >> s.block_shift;
+    const uint8_t *base = s.codes + il_code_byte(s, i, 0);
+    const size_t stride = (size_t)1 << (s.block_shift - 1);
+    const float *sbase = s.scales + k * s.num_src;
+    for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
+        uint32_t w[kBatch];
+        float sc[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            w[b] = 0u;
+            sc[b] = 0.0f;
+            if (q0 + b < s.num_src) {
+                w[b] = ld_nt(reinterpret_cast<const uint16_t *>(base + (q0 + b) * stride));
+                sc[b] = sbase[q0 + b];
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) {
+            if (q0 + b < s.num_src) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[e] = __builtin_fmaf(i4_code(w[b], e), sc[b], acc[e]);
+            }
+        }
+    }
+    return f32x4{i4grad_scaled(acc[0], s.scale_out), i4grad_scaled(acc[1], s.scale_out),
+                 i4grad_scaled(acc[2], s.scale_out), i4grad_scaled(acc[3], s.scale_out)};
+}
+
 // The fp32 gradient array the separate partition step reads, behind the same
 // interface.
 struct F32Grad {
@@ -87,5 +159,11 @@ __device__ __forceinline__ float grad_at(const I4Grad &s, size_t i) { return i4g
 __device__ __forceinline__ f32x4 grad_load4(const I4Grad &s, size_t i) {
     return i4grad_load4(s, i);
 }
+__device__ __forceinline__ float grad_at(const I4GradIl &s, size_t i) { return i4grad_at(s, i); }
+__device__ __forceinline__ f32x4 grad_load4(const I4GradIl &s, size_t i) {
+    return i4grad_load4(s, i);
+}
+
+
 
 }  // namespace zpp

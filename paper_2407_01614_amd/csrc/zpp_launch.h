@@ -57,6 +57,7 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
                                     bool vector_path, hipStream_t stream);
 
 struct I4Grad;
+struct I4GradIl;
 
 // The int4 gradient sources of the qgZ receive, gathered for a kernel argument.
 I4Grad make_i4grad(const uint8_t *const *src_codes, const float *const *src_scales,
@@ -72,6 +73,29 @@ hipError_t launch_fused_receive(float *p, float *m, float *v, const uint8_t *con
                                 uint16_t *secondary, int8_t *codes, float *scales, size_t n,
                                 uint32_t block, const AdamConsts &c, bool vector_path,
                                 hipStream_t stream);
+
+// The int4 copies interleaved in one receive buffer (layout in
+// zpp_i4grad.h), gathered for a kernel argument.
+I4GradIl make_i4grad_il(const uint8_t *codes, const float *scales, uint32_t num_src,
+                        uint32_t block, float scale_out);
+
+// The receive step and the fused pass from the interleaved receive buffer.
+hipError_t launch_receive_adam_il(float *p, float *m, float *v, const uint8_t *codes,
+                                  const float *scales, uint32_t num_src, uint32_t block,
+                                  float scale_out, uint16_t *out, size_t n, const AdamConsts &c,
+                                  bool vector_path, hipStream_t stream);
+hipError_t launch_fused_receive_il(float *p, float *m, float *v, const uint8_t *src_codes,
+                                   const float *src_scales, uint32_t num_src, uint32_t grad_block,
+                                   float scale_out, uint16_t *primary, uint16_t *secondary,
+                                   int8_t *codes, float *scales, size_t n, uint32_t block,
+                                   const AdamConsts &c, bool vector_path, hipStream_t stream);
+
+// int4 quantization of one source's n values into its slots of an
+// interleaved receive buffer of num_src sources (num_src = 1: the plain
+// layout of launch_quantize_i4).
+hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uint32_t source,
+                                 uint32_t num_src, uint8_t *codes, float *scales,
+                                 bool vector_path, hipStream_t stream);
 
 // The qgZ receive fused into the partition step: the gradient of every
 // element is the dequantize-and-reduce of the num_src int4 sources (times

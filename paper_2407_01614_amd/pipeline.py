@@ -56,10 +56,14 @@ class PartitionPipeline:
     own dequantize-and-reduce kernel writing `grad`, or, with `fuse_receive`,
     inside the partition step (`zpp_qgz_receive_adam_step`, no `grad`
     written), and with `fused` too, inside the single pass of step, refresh
-    and quantization (`zpp_qgz_receive_step_refresh_quantize`)."""
+    and quantization (`zpp_qgz_receive_step_refresh_quantize`).
+    `qgz_interleaved` keeps the int4 copies in one interleaved receive buffer
+    (`GradientExchange`), which only the fused receive reads."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
-                 qgz_sources=0, streams=3, fuse_receive=False):
+                 qgz_sources=0, streams=3, fuse_receive=False, qgz_interleaved=False):
+        if qgz_interleaved and not fuse_receive:
+            raise ValueError("an interleaved receive buffer is read by the fused receive only")
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         if streams not in (1, 3):
@@ -73,7 +77,8 @@ class PartitionPipeline:
         self.fuse_receive = fuse_receive
         # with qgz_sources > 0 every step starts with the qgZ receive: the mean
         # of that many int4 copies of this partition's gradient becomes `grad`
-        self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device)
+        self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device,
+                                          interleaved=qgz_interleaved)
                          if qgz_sources else None)
         n, s, B = wl.n, wl.shard_elems, wl.block
         K = wl.distinct_layers
@@ -311,10 +316,17 @@ class PartitionPipeline:
         wl, B = self.wl, self.wl.block
         if self._receive_fused():
             ex = self.exchange
-            self._timed("fused_receive", stream, lambda: zpp.qgz_receive_step_refresh_quantize(
-                self.master, self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales, self.primary,
-                self.secondary, self.codes, self.scales, step=t, grad_block=ex.block, block=B,
-                scale_out=1.0 / ex.num_src, stream=stream, done_after=done_after, **wl.adam))
+            if ex.interleaved:
+                call = functools.partial(zpp.qgz_receive_step_refresh_quantize_interleaved,
+                                         self.master, self.exp_avg, self.exp_avg_sq, ex.codes,
+                                         ex.scales, ex.num_src)
+            else:
+                call = functools.partial(zpp.qgz_receive_step_refresh_quantize, self.master,
+                                         self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales)
+            self._timed("fused_receive", stream, lambda: call(
+                self.primary, self.secondary, self.codes, self.scales, step=t,
+                grad_block=ex.block, block=B, scale_out=1.0 / ex.num_src, stream=stream,
+                done_after=done_after, **wl.adam))
         else:
             self._timed("fused", stream, lambda: zpp.adam_step_refresh_quantize(
                 self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary,
@@ -327,9 +339,16 @@ class PartitionPipeline:
         wl = self.wl
         if self._receive_fused():
             ex = self.exchange
-            self._timed("receive_adam", stream, lambda: zpp.qgz_receive_adam_step(
-                self.master, self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales, self.primary,
-                step=t, block=ex.block, scale_out=1.0 / ex.num_src, stream=stream, **wl.adam))
+            if ex.interleaved:
+                call = functools.partial(zpp.qgz_receive_adam_step_interleaved, self.master,
+                                         self.exp_avg, self.exp_avg_sq, ex.codes, ex.scales,
+                                         ex.num_src)
+            else:
+                call = functools.partial(zpp.qgz_receive_adam_step, self.master, self.exp_avg,
+                                         self.exp_avg_sq, ex.codes, ex.scales)
+            self._timed("receive_adam", stream, lambda: call(
+                self.primary, step=t, block=ex.block, scale_out=1.0 / ex.num_src,
+                stream=stream, **wl.adam))
         else:
             self._timed("adam", stream, lambda: zpp.adam_partition_step(
                 self.master, self.exp_avg, self.exp_avg_sq, self.grad, self.primary, step=t,
@@ -386,21 +405,37 @@ class GradientExchange:
     `num_src` sending ranks quantizes its gradient of this rank's partition to
     int4 (sources other than this rank are simulated in this GPU's memory),
     and the rank reduces the copies into the fp32 mean gradient that the
-    partition step reads."""
+    partition step reads.  With `interleaved` the copies arrive in one
+    receive buffer, block by block (the layout of include/zpp.h), which only
+    the receive fused into the partition step reads."""
 
-    def __init__(self, n, num_src, block=256, device="cuda"):
+    def __init__(self, n, num_src, block=256, device="cuda", interleaved=False):
         self.n, self.num_src, self.block = n, num_src, block
+        self.interleaved = interleaved
         nb = (n + block - 1) // block
-        self.codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device=device)
-                      for _ in range(num_src)]
-        self.scales = [torch.empty(nb, dtype=torch.float32, device=device)
-                       for _ in range(num_src)]
+        if interleaved:
+            nc, ns = zpp.interleaved_sizes(n, block, num_src)
+            self.codes = torch.zeros(nc, dtype=torch.uint8, device=device)
+            self.scales = torch.zeros(ns, dtype=torch.float32, device=device)
+        else:
+            self.codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device=device)
+                          for _ in range(num_src)]
+            self.scales = [torch.empty(nb, dtype=torch.float32, device=device)
+                           for _ in range(num_src)]
 
     def quantize(self, q, grad, stream=None, done_after=None):
-        zpp.quantize_blockwise_i4(grad, self.codes[q], self.scales[q], block=self.block,
-                                  n=self.n, stream=stream, done_after=done_after)
+        if self.interleaved:
+            zpp.quantize_blockwise_i4_interleaved(grad, self.codes, self.scales, source=q,
+                                                  num_src=self.num_src, block=self.block,
+                                                  n=self.n, stream=stream, done_after=done_after)
+        else:
+            zpp.quantize_blockwise_i4(grad, self.codes[q], self.scales[q], block=self.block,
+                                      n=self.n, stream=stream, done_after=done_after)
 
     def reduce(self, out, stream=None, wait_events=(), done_after=None):
+        if self.interleaved:
+            raise ValueError("the separate dequantize-and-reduce reads separate source arrays; "
+                             "an interleaved buffer is read by the fused receive")
         zpp.dequant_reduce_i4(self.codes, self.scales, self.n, out, block=self.block,
                               scale_out=1.0 / self.num_src, stream=stream,
                               wait_events=wait_events, done_after=done_after)

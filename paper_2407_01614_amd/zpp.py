@@ -59,6 +59,17 @@ _lib.zpp_qgz_receive_step_refresh_quantize.restype = ctypes.c_int
 _lib.zpp_qgz_receive_step_refresh_quantize.argtypes = [
     _P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P, _P, _P, _P, _sz, _u32,
     ctypes.POINTER(AdamHParams), _P, _P, _u32, _P]
+_lib.zpp_quantize_blockwise_i4_interleaved.restype = ctypes.c_int
+_lib.zpp_quantize_blockwise_i4_interleaved.argtypes = [_P, _sz, _u32, _u32, _u32, _P, _P, _P, _P,
+                                                       _P]
+_lib.zpp_qgz_receive_adam_step_interleaved.restype = ctypes.c_int
+_lib.zpp_qgz_receive_adam_step_interleaved.argtypes = [
+    _P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P, _sz, ctypes.POINTER(AdamHParams), _P, _P,
+    _u32, _P]
+_lib.zpp_qgz_receive_step_refresh_quantize_interleaved.restype = ctypes.c_int
+_lib.zpp_qgz_receive_step_refresh_quantize_interleaved.argtypes = [
+    _P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P, _P, _P, _P, _sz, _u32,
+    ctypes.POINTER(AdamHParams), _P, _P, _u32, _P]
 _lib.zpp_status_string.restype = ctypes.c_char_p
 _lib.zpp_status_string.argtypes = [ctypes.c_int]
 _lib.zpp_last_hip_error.restype = ctypes.c_int
@@ -67,7 +78,10 @@ _lib.zpp_last_hip_error.argtypes = []
 EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
            "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
            "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
-           "zpp_qgz_receive_step_refresh_quantize", "zpp_status_string", "zpp_last_hip_error")
+           "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
+           "zpp_qgz_receive_adam_step_interleaved",
+           "zpp_qgz_receive_step_refresh_quantize_interleaved", "zpp_status_string",
+           "zpp_last_hip_error")
 
 
 class ZppError(RuntimeError):
@@ -445,6 +459,99 @@ def qgz_receive_step_refresh_quantize(master, exp_avg, exp_avg_sq, src_codes, sr
         scales.data_ptr(), n, block, ctypes.byref(hp), stream_handle(stream), warr, len(waits),
         _event_handle(done_after))
     _check(st, "zpp_qgz_receive_step_refresh_quantize")
+
+
+# --------------------------------------------------------------------------
+# The qgZ receive buffer interleaved (layout in include/zpp.h)
+# --------------------------------------------------------------------------
+def interleaved_sizes(n, block, num_src):
+    """(code bytes, scale count) of an interleaved receive buffer of num_src
+    int4 copies of n elements in blocks of `block`."""
+    nb = num_blocks(n, block)
+    return nb * num_src * (block // 2), nb * num_src
+
+
+def _interleaved_inputs(codes, scales, n, block, num_src):
+    _dev(codes, _U8, "codes")
+    _dev(scales, _F32, "scales")
+    if not 1 <= num_src <= MAX_SHARDS:
+        raise ValueError("1..%d sources" % MAX_SHARDS)
+    nc, ns = interleaved_sizes(n, block, num_src)
+    if codes.numel() < nc or scales.numel() < ns:
+        raise ValueError("the interleaved buffer is too small for n = %d, %d sources" % (n, num_src))
+
+
+def quantize_blockwise_i4_interleaved(src, codes, scales, *, source, num_src, block=256, n=None,
+                                      stream=None, wait_before=None, done_after=None):
+    """zpp_quantize_blockwise_i4_interleaved: source `source` of num_src."""
+    _dev(src, _F32, "src")
+    if n is None:
+        n = src.numel()
+    if src.numel() < n:
+        raise ValueError("src holds fewer than n elements")
+    _interleaved_inputs(codes, scales, n, block, num_src)
+    st = _lib.zpp_quantize_blockwise_i4_interleaved(
+        src.data_ptr(), n, block, source, num_src, codes.data_ptr(), scales.data_ptr(),
+        stream_handle(stream), _event_handle(wait_before), _event_handle(done_after))
+    _check(st, "zpp_quantize_blockwise_i4_interleaved")
+
+
+def qgz_receive_adam_step_interleaved(master, exp_avg, exp_avg_sq, codes, scales, num_src,
+                                      primary_bf16, *, lr, beta1, beta2, eps, weight_decay,
+                                      step, adamw=True, block=256, scale_out=1.0, n=None,
+                                      stream=None, wait_events=(), done_after=None):
+    """zpp_qgz_receive_adam_step_interleaved: the receive step from one
+    interleaved buffer of num_src int4 copies."""
+    for t, name in ((master, "master"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq")):
+        _dev(t, _F32, name)
+    _dev(primary_bf16, _BF16, "primary_bf16")
+    if n is None:
+        n = master.numel()
+    if any(t.numel() < n for t in (master, exp_avg, exp_avg_sq, primary_bf16)):
+        raise ValueError("a buffer holds fewer than n elements")
+    _interleaved_inputs(codes, scales, n, block, num_src)
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    hp = AdamHParams(lr, beta1, beta2, eps, weight_decay, 1 if adamw else 0, int(step))
+    st = _lib.zpp_qgz_receive_adam_step_interleaved(
+        master.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), codes.data_ptr(),
+        scales.data_ptr(), num_src, block, scale_out, primary_bf16.data_ptr(), n,
+        ctypes.byref(hp), stream_handle(stream), warr, len(waits), _event_handle(done_after))
+    _check(st, "zpp_qgz_receive_adam_step_interleaved")
+
+
+def qgz_receive_step_refresh_quantize_interleaved(
+        master, exp_avg, exp_avg_sq, src_codes, src_scales, num_src, primary_bf16,
+        secondary_bf16, codes, scales, *, lr, beta1, beta2, eps, weight_decay, step, adamw=True,
+        grad_block=256, block=256, scale_out=1.0, n=None, stream=None, wait_events=(),
+        done_after=None):
+    """zpp_qgz_receive_step_refresh_quantize_interleaved: the single pass from
+    one interleaved buffer of num_src int4 copies."""
+    for t, name in ((master, "master"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq"),
+                    (scales, "scales")):
+        _dev(t, _F32, name)
+    _dev(primary_bf16, _BF16, "primary_bf16")
+    if secondary_bf16 is not None:
+        _dev(secondary_bf16, _BF16, "secondary_bf16")
+    _dev(codes, _I8, "codes")
+    if n is None:
+        n = master.numel()
+    bufs = [master, exp_avg, exp_avg_sq, primary_bf16, codes]
+    if secondary_bf16 is not None:
+        bufs.append(secondary_bf16)
+    if any(t.numel() < n for t in bufs) or scales.numel() < num_blocks(n, block):
+        raise ValueError("a buffer is too small for n = %d" % n)
+    _interleaved_inputs(src_codes, src_scales, n, grad_block, num_src)
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    hp = AdamHParams(lr, beta1, beta2, eps, weight_decay, 1 if adamw else 0, int(step))
+    st = _lib.zpp_qgz_receive_step_refresh_quantize_interleaved(
+        master.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), src_codes.data_ptr(),
+        src_scales.data_ptr(), num_src, grad_block, scale_out, primary_bf16.data_ptr(),
+        secondary_bf16.data_ptr() if secondary_bf16 is not None else None, codes.data_ptr(),
+        scales.data_ptr(), n, block, ctypes.byref(hp), stream_handle(stream), warr, len(waits),
+        _event_handle(done_after))
+    _check(st, "zpp_qgz_receive_step_refresh_quantize_interleaved")
 
 
 # --------------------------------------------------------------------------

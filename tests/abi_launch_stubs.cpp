@@ -56,4 +56,20 @@ hipError_t launch_receive_adam(float *, float *, float *, const uint8_t *const *
     return reached();
 }
 
+hipError_t launch_quantize_i4_il(const float *, size_t, uint32_t, uint32_t, uint32_t, uint8_t *,
+                                 float *, bool, hipStream_t) {
+    return reached();
+}
+hipError_t launch_receive_adam_il(float *, float *, float *, const uint8_t *, const float *,
+                                  uint32_t, uint32_t, float, uint16_t *, size_t, const AdamConsts &,
+                                  bool, hipStream_t) {
+    return reached();
+}
+hipError_t launch_fused_receive_il(float *, float *, float *, const uint8_t *, const float *,
+                                   uint32_t, uint32_t, float, uint16_t *, uint16_t *, int8_t *,
+                                   float *, size_t, uint32_t, const AdamConsts &, bool,
+                                   hipStream_t) {
+    return reached();
+}
+
 }  // namespace zpp

@@ -301,6 +301,61 @@ static void check_qgz_receive(void)
     free_sources(&s);
 }
 
+static void check_interleaved(void)
+{
+    zpp_adam_hparams hp = good_hp();
+    const size_t n = 1000;
+    float *p = dev(0), *m = dev(1), *v = dev(2), *x = dev(3), *sc8 = dev(7), *is = dev(9);
+    uint16_t *pr = dev(4), *se = dev(5);
+    int8_t *c8 = dev(6);
+    uint8_t *ic = dev(8);
+    for (unsigned P = 1; P <= ZPP_MAX_SHARDS; P = P < 8 ? P + 1 : P * 2) {
+        const unsigned W = P < 3 ? P : 3;
+        hipEvent_t *waits = xmalloc(W * sizeof *waits);
+        for (unsigned w = 0; w < W; ++w)
+            waits[w] = fake_event(w);
+        EXPECT_STATUS(zpp_quantize_blockwise_i4_interleaved(x, 0, 256, P - 1, P, ic, is, NULL, NULL,
+                                                            NULL),
+                      ZPP_OK);
+        EXPECT_STATUS(zpp_quantize_blockwise_i4_interleaved(x, n, 256, P, P, ic, is, NULL, NULL,
+                                                            NULL),
+                      ZPP_EINVAL);
+        EXPECT_STATUS(zpp_quantize_blockwise_i4_interleaved(x, n, 256, 0, P, (uint8_t *)dev_off(3, 8),
+                                                            is, NULL, NULL, NULL),
+                      ZPP_EOVERLAP);
+        EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, ic, is, P, 256, 0.5f, pr, 0, &hp,
+                                                            NULL, NULL, 0, NULL),
+                      ZPP_OK);
+        EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, ic, is, P, 256, 0.5f, NULL, n,
+                                                            &hp, NULL, waits, W, NULL),
+                      ZPP_EINVAL);
+        EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, (uint8_t *)dev_off(0, 16), is,
+                                                            P, 256, 0.5f, pr, n, &hp, NULL, NULL,
+                                                            0, NULL),
+                      ZPP_EOVERLAP);
+        EXPECT_STATUS(zpp_qgz_receive_step_refresh_quantize_interleaved(
+                          p, m, v, ic, is, P, 256, 0.5f, pr, se, c8, sc8, 0, 256, &hp, NULL, NULL,
+                          0, NULL),
+                      ZPP_OK);
+        EXPECT_STATUS(zpp_qgz_receive_step_refresh_quantize_interleaved(
+                          p, m, v, ic, is, P, 256, 0.5f, pr, se, NULL, sc8, n, 256, &hp, NULL,
+                          waits, W, NULL),
+                      ZPP_EINVAL);
+        EXPECT_STATUS(zpp_qgz_receive_step_refresh_quantize_interleaved(
+                          p, m, v, ic, (float *)dev_off(7, 0), P, 256, 0.5f, pr, se, c8, sc8, n,
+                          256, &hp, NULL, NULL, 0, NULL),
+                      ZPP_EOVERLAP);
+        free(waits);
+    }
+    EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, ic, is, 0, 256, 0.5f, pr, n, &hp,
+                                                        NULL, NULL, 0, NULL),
+                  ZPP_EINVAL);
+    EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, ic, is, 8, 256, 0.5f, pr,
+                                                        SIZE_MAX / 16 / 8 + 1, &hp, NULL, NULL, 0,
+                                                        NULL),
+                  ZPP_EINVAL);
+}
+
 static void check_strings(void)
 {
     const int all[] = {ZPP_OK, ZPP_EINVAL, ZPP_EALIGN, ZPP_EOVERLAP, ZPP_EHIP, 99, -1};
@@ -325,6 +380,7 @@ int main(void)
     check_refresh_and_quantize();
     check_gather();
     check_qgz_receive();
+    check_interleaved();
     check_strings();
     if (zpp_test_launches) {
         printf("%d case(s) got past validation to a kernel launch\n", zpp_test_launches);

@@ -36,7 +36,9 @@ def test_header_declares_the_four_calls():
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
                "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
                "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
-               "zpp_qgz_receive_step_refresh_quantize", "zpp_status_string",
+               "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
+               "zpp_qgz_receive_adam_step_interleaved",
+               "zpp_qgz_receive_step_refresh_quantize_interleaved", "zpp_status_string",
                "zpp_last_hip_error"):
         assert fn in names
 
@@ -328,6 +330,90 @@ def test_qgz_receive_pass_validation(zpp):
     assert receive_pass(zpp, codes=(D, A + 16)) == zpp.ZPP_EOVERLAP
     assert receive_pass(zpp, scales=(D + 0x200000, F + 8)) == zpp.ZPP_EOVERLAP
     assert receive_pass(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
+
+
+def quant_il(zpp, src=A, codes=F, scales=H, n=1000, block=256, source=3, num=8):
+    return zpp.raw.zpp_quantize_blockwise_i4_interleaved(src, n, block, source, num, codes, scales,
+                                                         None, None, None)
+
+
+def test_quantize_i4_interleaved_validation(zpp):
+    """Every case fails validation (or is a size-0 no-op): none reaches a launch."""
+    assert quant_il(zpp, n=0, src=None, codes=None, scales=None) == zpp.ZPP_OK
+    assert quant_il(zpp, num=0) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, num=65) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, source=8) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, block=100) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, n=(1 << 64) // 16 // 8 + 1) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, src=None) == zpp.ZPP_EINVAL
+    assert quant_il(zpp, src=A + 2) == zpp.ZPP_EALIGN
+    assert quant_il(zpp, scales=H + 2) == zpp.ZPP_EALIGN
+    assert quant_il(zpp, codes=A + 16) == zpp.ZPP_EOVERLAP        # codes inside src
+    assert quant_il(zpp, scales=F + 4000) == zpp.ZPP_EOVERLAP    # scales inside the codes buffer
+
+
+def receive_il(zpp, state=(A, B, C, E), codes=F, scales=H, num=8, n=1024, block=256,
+               scale_out=0.5, h=None, waits=None, nwait=0):
+    P = ctypes.c_void_p
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_qgz_receive_adam_step_interleaved(
+        state[0], state[1], state[2], codes, scales, num, block, scale_out, state[3], n,
+        ctypes.byref(h) if h is not False else None, None, warr, nwait, None)
+
+
+def test_qgz_receive_interleaved_validation(zpp):
+    """Every case fails validation (or is a size-0 no-op): none reaches a launch."""
+    assert receive_il(zpp, n=0, state=(None,) * 4) == zpp.ZPP_OK
+    assert receive_il(zpp, h=False) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, h=hp(zpp, step=0)) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, num=0) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, num=65) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, block=96) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, scale_out=float("nan")) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, n=(1 << 64) // 16 // 8 + 1) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, codes=None) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, scales=H + 2) == zpp.ZPP_EALIGN
+    assert receive_il(zpp, state=(A, None, C, E)) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, state=(A + 2, B, C, E)) == zpp.ZPP_EALIGN
+    assert receive_il(zpp, state=(A, B, C, A + 64)) == zpp.ZPP_EOVERLAP  # primary in master
+    assert receive_il(zpp, codes=A + 16) == zpp.ZPP_EOVERLAP            # codes in master
+    assert receive_il(zpp, scales=E + 8) == zpp.ZPP_EOVERLAP            # scales in primary
+    assert receive_il(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
+    assert receive_il(zpp, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
+
+
+def receive_pass_il(zpp, state=(A, B, C, E, F, G, H), codes=D, scales=D + 0x200000, num=8,
+                    n=1024, grad_block=256, block=256, scale_out=0.5, h=None, waits=None,
+                    nwait=0):
+    """state: master, exp_avg, exp_avg_sq, primary, secondary, codes, scales."""
+    P = ctypes.c_void_p
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    h = h if h is not None else hp(zpp)
+    return zpp.raw.zpp_qgz_receive_step_refresh_quantize_interleaved(
+        state[0], state[1], state[2], codes, scales, num, grad_block, scale_out, state[3],
+        state[4], state[5], state[6], n, block, ctypes.byref(h) if h is not False else None, None,
+        warr, nwait, None)
+
+
+def test_qgz_receive_pass_interleaved_validation(zpp):
+    """Every case fails validation (or is a size-0 no-op): none reaches a launch."""
+    assert receive_pass_il(zpp, n=0, state=(None,) * 7) == zpp.ZPP_OK
+    assert receive_pass_il(zpp, h=False) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, grad_block=96) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, block=32) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, num=0) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, scale_out=float("inf")) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, codes=None) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, scales=D + 2) == zpp.ZPP_EALIGN
+    assert receive_pass_il(zpp, state=(A, B, C, E, F, None, H)) == zpp.ZPP_EINVAL
+    assert receive_pass_il(zpp, state=(A, B, C, E, F, G, H + 2)) == zpp.ZPP_EALIGN
+    assert receive_pass_il(zpp, state=(A, B, C, E, F + 1, G, H)) == zpp.ZPP_EALIGN
+    assert receive_pass_il(zpp, state=(A, B, C, E, E + 64, G, H)) == zpp.ZPP_EOVERLAP
+    assert receive_pass_il(zpp, codes=A + 16) == zpp.ZPP_EOVERLAP
+    assert receive_pass_il(zpp, scales=F + 8) == zpp.ZPP_EOVERLAP
+    assert receive_pass_il(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
 
 
 def test_no_oracle_in_product_path():

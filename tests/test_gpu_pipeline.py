@@ -479,3 +479,49 @@ def test_pipeline_fused_receive_equals_separate(zpp, streams):
     for other in results[1:]:
         for i, (a, b) in enumerate(zip(other, results[0])):
             assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["step", "single-pass"])
+def test_pipeline_interleaved_receive_equals_separate(zpp, fused):
+    """The pipeline with its 8 int4 copies in one interleaved receive buffer
+    (each quantized into its slots on the device) ends two steps in the same
+    state as with the oracle's copies in separate arrays, bit for bit."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small-qgz-il", cfg_id=15, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
+                  secondary_world=4, world=4)
+    P = 8
+    srcs = [synth.gradients(wl.n, wl.cfg_id, q) for q in range(P)]
+    peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
+                                          wl.block) for j in range(wl.secondary_world - 1)]
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    results = []
+    for il in (False, True):
+        pipe = PartitionPipeline(wl, qgz_sources=P, fused=fused, fuse_receive=True,
+                                 qgz_interleaved=il)
+        pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
+        for q, x in enumerate(srcs):
+            if il:
+                pipe.exchange.quantize(q, torch.from_numpy(x).cuda())
+            else:
+                c, sc = oracle.quantize_blockwise_i4(x, wl.block)
+                pipe.exchange.codes[q].copy_(torch.from_numpy(c))
+                pipe.exchange.scales[q].copy_(torch.from_numpy(sc))
+        torch.cuda.synchronize()
+        pipe.step()
+        pipe.step()
+        pipe.wait()
+        results.append([t.cpu().numpy().copy() for t in (pipe.master, pipe.exp_avg,
+                                                         pipe.exp_avg_sq, pipe.primary,
+                                                         pipe.secondary, pipe.codes, pipe.scales,
+                                                         pipe.out)])
+        del pipe
+    for i, (a, b) in enumerate(zip(results[1], results[0])):
+        assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)
+
+
+def test_pipeline_interleaved_needs_fused_receive():
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import WORKLOADS
+    with pytest.raises(ValueError):
+        PartitionPipeline(WORKLOADS["tiny"], qgz_sources=8, qgz_interleaved=True)

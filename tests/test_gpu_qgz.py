@@ -503,3 +503,208 @@ def test_fullsize_receive_pass(zpp):
     for a, b, name in zip(outs[1], outs[0], ("master", "exp_avg", "exp_avg_sq", "primary",
                                              "secondary", "codes", "scales")):
         assert torch.equal(a, b), name
+
+
+# ===========================================================================
+# The interleaved receive buffer: the P int4 copies in one buffer, block by
+# block (layout in include/zpp.h)
+# ===========================================================================
+def interleave(quants, n, block):
+    """Lay the P separate (codes, scales) out as one interleaved receive
+    buffer: block k holds each source's block/2 code bytes side by side, and
+    source q's scale of block k is scale k P + q."""
+    P = len(quants)
+    nb = -(-n // block)
+    half = block // 2
+    codes = np.zeros((nb, P, half), np.uint8)
+    scales = np.zeros((nb, P), np.float32)
+    for q, (c, s) in enumerate(quants):
+        padded = np.zeros(nb * half, np.uint8)
+        padded[:c.size] = c
+        codes[:, q, :] = padded.reshape(nb, half)
+        scales[:, q] = s
+    return codes.ravel(), scales.ravel()
+
+
+def deinterleave(codes, scales, n, block, P):
+    nb = -(-n // block)
+    half = block // 2
+    c = codes[:nb * P * half].reshape(nb, P, half)
+    s = scales[:nb * P].reshape(nb, P)
+    return [(c[:, q, :].ravel()[:(n + 1) // 2].copy(), s[:, q].copy()) for q in range(P)]
+
+
+def zeros_u8(n):
+    return torch.zeros(n, dtype=torch.uint8, device="cuda")
+
+
+@pytest.mark.parametrize("P,n,block", [(1, 7, 256), (3, 256 * 9 + 81, 64), (8, 100001, 256),
+                                       (8, 65536 + 8, 1024), (64, 256 * 5 + 3, 128),
+                                       (5, 4096 * 3 + 500, 4096)])
+@pytest.mark.parametrize("pad", [0, 1], ids=["vector", "scalar"])
+def test_quantize_i4_interleaved_equals_plain(zpp, P, n, block, pad):
+    """Each source quantized into its slots of one interleaved buffer: taken
+    back out, every source's codes and scales are the oracle's, bit for bit."""
+    srcs = [grads(n, 150 + P, q, scale=1.0 + q) for q in range(P)]
+    nc, ns = zpp.interleaved_sizes(n, block, P)
+    codes = zeros_u8(nc)
+    scales = empty_dev(ns, np.float32, fill=-1.0)
+    for q, x in enumerate(srcs):
+        zpp.quantize_blockwise_i4_interleaved(to_dev(x, pad=pad), codes, scales, source=q,
+                                              num_src=P, block=block)
+    torch.cuda.synchronize()
+    got = deinterleave(codes.cpu().numpy(), to_host(scales, np.float32), n, block, P)
+    for q, x in enumerate(srcs):
+        rc, rs = oracle.quantize_blockwise_i4(x, block)
+        assert_bits_equal(got[q][0], rc, "codes of source %d" % q)
+        assert_bits_equal(got[q][1], rs, "scales of source %d" % q)
+
+
+def run_receive_il(zpp, quants, n, block, scale_out, state, step, hp, adamw, pad_codes=0):
+    ic, isc = interleave(quants, n, block)
+    p, m, v, b = state
+    zpp.qgz_receive_adam_step_interleaved(p, m, v, u8_dev(ic, pad=pad_codes), to_dev(isc),
+                                          len(quants), b, step=step, adamw=adamw, block=block,
+                                          scale_out=scale_out, **hp)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("P,n,block", [
+    (1, 1, 256), (8, 7, 256), (8, 256 * 9 + 81, 256), (3, 65536 + 8, 64), (8, 100001, 128),
+    (5, 256 * 33, 1024), (8, 1 << 18, 4096), (64, 256 * 5 + 3, 256), (9, 256 * 40, 512),
+    (16, 256 * 17 + 100, 64)])
+@pytest.mark.parametrize("regime", sorted(REGIMES))
+def test_receive_interleaved_equals_separate(zpp, P, n, block, regime):
+    """The receive step from one interleaved buffer leaves the same bits as
+    from the P separate arrays (same state, same sources)."""
+    hp, moments, step, adamw = REGIMES[regime]
+    quants = oracle_sources(P, n, block, 160 + P + n)
+    scale_out = float(np.float32(1.0 / P))
+    ref_state, _ = receive_state(n, 161, moments=moments)
+    got_state, _ = receive_state(n, 161, moments=moments)
+    run_receive(zpp, quants, n, block, scale_out, ref_state, step, hp, adamw)
+    run_receive_il(zpp, quants, n, block, scale_out, got_state, step, hp, adamw)
+    for a, b, name in zip(host_state(got_state), host_state(ref_state),
+                          ("master", "exp_avg", "exp_avg_sq", "primary")):
+        assert_bits_equal(a, b, "%s P=%d n=%d block %d" % (name, P, n, block))
+
+
+@pytest.mark.parametrize("pads", [(1, 0), (0, 1), (0, 3), (0, 2)],
+                         ids=["state", "codes-odd", "codes-odd-3", "codes-2"])
+def test_receive_interleaved_misaligned(zpp, pads):
+    """Misaligned state, or interleaved codes at an odd address, take the
+    any-alignment kernel; codes at a 2-byte address keep the vector kernel:
+    the same bits either way."""
+    n, block, P = 256 * 11 + 5, 128, 5
+    quants = oracle_sources(P, n, block, 162)
+    ref_state, _ = receive_state(n, 163)
+    got_state, _ = receive_state(n, 163, pad=pads[0])
+    run_receive(zpp, quants, n, block, 0.2, ref_state, 1, HP, True)
+    run_receive_il(zpp, quants, n, block, 0.2, got_state, 1, HP, True, pad_codes=pads[1])
+    for a, b in zip(host_state(got_state), host_state(ref_state)):
+        assert_bits_equal(a, b, "misaligned %s" % (pads,))
+
+
+def test_receive_interleaved_vs_oracle(zpp):
+    """The interleaved receive step against the oracle's dequantize-and-reduce
+    of the same sources followed by its Adam step."""
+    n, block, P = 256 * 21 + 17, 256, 8
+    hp = HP_LOUD
+    quants = oracle_sources(P, n, block, 164)
+    state, (p, m, v) = receive_state(n, 165, moments=True)
+    run_receive_il(zpp, quants, n, block, float(np.float32(1.0 / P)), state, 3, hp, True)
+    g = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
+                                 float(np.float32(1.0 / P)))
+    ref = oracle.adam_step(p, m, v, g, step=3, **hp)
+    assert_adam_close(host_state(state), ref, hp["lr"], "interleaved receive", prev=(p, m, v),
+                      g=g, hp=hp)
+
+
+def run_receive_pass_il(zpp, quants, n, grad_block, block, scale_out, state, secondary, step,
+                        hp, adamw, pad=0):
+    p, m, v, b = state
+    ic, isc = interleave(quants, n, grad_block)
+    sec = empty_dev(n, np.uint16, pad=pad, fill=0x7FC0) if secondary else None
+    qc = empty_dev(n, np.int8, pad=pad, fill=0)
+    qs = empty_dev((n + block - 1) // block, np.float32, fill=-1.0)
+    zpp.qgz_receive_step_refresh_quantize_interleaved(
+        p, m, v, u8_dev(ic), to_dev(isc), len(quants), b, sec, qc, qs, step=step, adamw=adamw,
+        grad_block=grad_block, block=block, scale_out=scale_out, **hp)
+    torch.cuda.synchronize()
+    return host_state(state) + ((to_host(sec, np.uint16) if secondary else None),
+                                to_host(qc, np.int8), to_host(qs, np.float32))
+
+
+@pytest.mark.parametrize("P,n,grad_block,block,secondary", [
+    (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
+    (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
+    (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
+    (16, 256 * 17 + 100, 128, 512, True)])
+@pytest.mark.parametrize("regime", sorted(REGIMES))
+def test_receive_pass_interleaved_equals_separate(zpp, P, n, grad_block, block, secondary,
+                                                  regime):
+    """The single pass from one interleaved buffer: the same bits as from the
+    P separate arrays."""
+    hp, moments, step, adamw = REGIMES[regime]
+    quants = oracle_sources(P, n, grad_block, 166 + P + n)
+    scale_out = float(np.float32(1.0 / P))
+    ref_state, _ = receive_state(n, 167, moments=moments)
+    got_state, _ = receive_state(n, 167, moments=moments)
+    ref = run_receive_pass(zpp, quants, n, grad_block, block, scale_out, ref_state, secondary,
+                           step, hp, adamw)
+    got = run_receive_pass_il(zpp, quants, n, grad_block, block, scale_out, got_state,
+                              secondary, step, hp, adamw)
+    names = ("master", "exp_avg", "exp_avg_sq", "primary", "secondary", "codes", "scales")
+    for a, b, name in zip(got, ref, names):
+        if a is None:
+            continue
+        assert_bits_equal(a, b, "%s P=%d n=%d blocks %d/%d" % (name, P, n, grad_block, block))
+
+
+def test_fullsize_receive_interleaved(zpp):
+    """The Llama-2-13B partition from 8 int4 sources, each quantized on the
+    device into separate arrays and into one interleaved buffer: the receive
+    step and the single pass leave the same bits either way (compared whole
+    on the device)."""
+    wl = WORKLOADS["llama-2-13b"]
+    n, B, P = wl.n, wl.block, 8
+    nb = (n + B - 1) // B
+    hp = f32hp(wl.adam)
+    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
+    nc, ns = zpp.interleaved_sizes(n, B, P)
+    ic = torch.zeros(nc, dtype=torch.uint8, device="cuda")
+    isc = torch.zeros(ns, dtype=torch.float32, device="cuda")
+    for q in range(P):
+        src = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, rank=q)
+        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=B)
+        zpp.quantize_blockwise_i4_interleaved(src, ic, isc, source=q, num_src=P, block=B)
+        torch.cuda.synchronize()
+        del src
+    p0 = synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER)
+    for single in (False, True):
+        outs = []
+        for il in (False, True):
+            p, m, v = p0.clone(), torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+            prim = torch.empty(n, dtype=torch.int16, device="cuda")
+            sec = torch.empty(n, dtype=torch.int16, device="cuda")
+            qc = torch.empty(n, dtype=torch.int8, device="cuda")
+            qs = torch.empty(nb, dtype=torch.float32, device="cuda")
+            if single and il:
+                zpp.qgz_receive_step_refresh_quantize_interleaved(
+                    p, m, v, ic, isc, P, prim, sec, qc, qs, step=1, scale_out=1.0 / P, **hp)
+            elif single:
+                zpp.qgz_receive_step_refresh_quantize(p, m, v, codes, scales, prim, sec, qc, qs,
+                                                      step=1, scale_out=1.0 / P, **hp)
+            elif il:
+                zpp.qgz_receive_adam_step_interleaved(p, m, v, ic, isc, P, prim, step=1,
+                                                      scale_out=1.0 / P, **hp)
+            else:
+                zpp.qgz_receive_adam_step(p, m, v, codes, scales, prim, step=1,
+                                          scale_out=1.0 / P, **hp)
+            torch.cuda.synchronize()
+            outs.append([p, m, v, prim] + ([sec, qc, qs] if single else []))
+        for a, b in zip(*outs):
+            assert torch.equal(a, b), "interleaved %s differs" % ("pass" if single else "step")
+        del outs
+        torch.cuda.empty_cache()
