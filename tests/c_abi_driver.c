@@ -11,7 +11,10 @@
  * copies, against the dequantize-and-reduce followed by the step and against
  * the oracle, and the single receive pass that also writes the secondary
  * and its int8 quantization (zpp_qgz_receive_step_refresh_quantize) against
- * the same sequence and the oracle's quantization.  Also checks a few
+ * the same sequence and the oracle's quantization.  The same two receives
+ * from one interleaved receive buffer (the int4 copies block by block, as
+ * include/zpp.h lays them out), each copy written into its slots by
+ * zpp_quantize_blockwise_i4_interleaved.  Also checks a few
  * validation errors of the ABI.
  *
  * Test infrastructure: built by the repository's build step, run by
@@ -117,6 +120,12 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     const size_t nb = (n + B - 1) / B, nbytes = (n + 1) / 2;
     const float scale_out = 1.0f / NSRC;
     float *x = malloc(n * 4);
+    const size_t half = B / 2, il_bytes = nb * NSRC * half, il_count = nb * NSRC;
+    uint8_t *hil_c = calloc(il_bytes, 1);
+    float *hil_s = calloc(il_count, 4);
+    uint8_t *dil_c = dev_alloc(il_bytes);
+    float *dil_s = dev_alloc(il_count * 4);
+    float *dx[NSRC];
     uint8_t *hc[NSRC];
     float *hs[NSRC];
     const uint8_t *dc[NSRC];
@@ -129,6 +138,14 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         hc[q] = malloc(nbytes);
         hs[q] = malloc(nb * 4);
         orc_quantize_blockwise_i4(x, n, B, hc[q], hs[q]);
+        /* the interleaved layout built on the host from the oracle's copy */
+        for (size_t k = 0; k < nb; k++) {
+            const size_t len = nbytes - k * half < half ? nbytes - k * half : half;
+            memcpy(hil_c + (k * NSRC + q) * half, hc[q] + k * half, len);
+            hil_s[k * NSRC + q] = hs[q][k];
+        }
+        dx[q] = dev_alloc(n * 4);
+        HIP_OK(hipMemcpy(dx[q], x, n * 4, hipMemcpyHostToDevice));
         uint8_t *c = dev_alloc(nbytes);
         float *sc = dev_alloc(nb * 4);
         HIP_OK(hipMemcpyAsync(c, hc[q], nbytes, hipMemcpyHostToDevice, up));
@@ -139,11 +156,18 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     hipEvent_t uploaded, done;
     HIP_OK(hipEventCreateWithFlags(&uploaded, hipEventDisableTiming));
     HIP_OK(hipEventCreateWithFlags(&done, hipEventDisableTiming));
+    /* each copy quantized on the device into its slots of one interleaved buffer */
+    HIP_OK(hipMemsetAsync(dil_c, 0, il_bytes, up));
+    for (unsigned q = 0; q < NSRC; q++)
+        EXPECT(zpp_quantize_blockwise_i4_interleaved(dx[q], n, B, q, NSRC, dil_c, dil_s, up, NULL,
+                                                     NULL) == ZPP_OK,
+               "interleaved int4 quantization of source %u", q);
     HIP_OK(hipEventRecord(uploaded, up));
-    /* state 0: reduce then step; 1: the receive step; 2: the single pass */
-    float *d[3][3];
-    uint16_t *dprim[3];
-    for (int k = 0; k < 3; k++) {
+    /* state 0: reduce then step; 1: the receive step; 2: the single pass;
+     * 3 and 4: the same two from the interleaved buffer */
+    float *d[5][3];
+    uint16_t *dprim[5];
+    for (int k = 0; k < 5; k++) {
         for (int a = 0; a < 3; a++) {
             d[k][a] = dev_alloc(n * 4);
             if (a == 0)
@@ -157,6 +181,9 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     uint16_t *dsec = dev_alloc(n * 2);
     int8_t *dq8 = dev_alloc(n);
     float *ds8 = dev_alloc(nb * 4);
+    uint16_t *dsec_il = dev_alloc(n * 2);
+    int8_t *dq8_il = dev_alloc(n);
+    float *ds8_il = dev_alloc(nb * 4);
     HIP_OK(hipDeviceSynchronize());
     /* the two-call sequence, then the fused call, both ordered after the upload */
     EXPECT(zpp_dequant_reduce_i4(dc, ds, NSRC, n, B, scale_out, dgrad, st, &uploaded, 1, NULL) ==
@@ -170,17 +197,35 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
            "fused receive step");
     EXPECT(zpp_qgz_receive_step_refresh_quantize(d[2][0], d[2][1], d[2][2], dc, ds, NSRC, B,
                                                  scale_out, dprim[2], dsec, dq8, ds8, n, B, hp,
-                                                 st, &uploaded, 1, done) == ZPP_OK,
+                                                 st, &uploaded, 1, NULL) == ZPP_OK,
            "single receive pass");
+    EXPECT(zpp_qgz_receive_adam_step_interleaved(d[3][0], d[3][1], d[3][2], dil_c, dil_s, NSRC,
+                                                 B, scale_out, dprim[3], n, hp, st, &uploaded, 1,
+                                                 NULL) == ZPP_OK,
+           "receive step from the interleaved buffer");
+    EXPECT(zpp_qgz_receive_step_refresh_quantize_interleaved(
+               d[4][0], d[4][1], d[4][2], dil_c, dil_s, NSRC, B, scale_out, dprim[4], dsec_il,
+               dq8_il, ds8_il, n, B, hp, st, &uploaded, 1, done) == ZPP_OK,
+           "single receive pass from the interleaved buffer");
     HIP_OK(hipEventSynchronize(done));
-    float *h[3][3], *hg = malloc(n * 4), *rg = malloc(n * 4), *hs8 = malloc(nb * 4),
+    float *h[5][3], *hg = malloc(n * 4), *rg = malloc(n * 4), *hs8 = malloc(nb * 4),
           *rs8 = malloc(nb * 4);
-    uint16_t *hp16[3], *hsec = malloc(n * 2);
-    int8_t *hq8 = malloc(n), *rq8 = malloc(n);
+    uint16_t *hp16[5], *hsec = malloc(n * 2), *hsec_il = malloc(n * 2);
+    int8_t *hq8 = malloc(n), *rq8 = malloc(n), *hq8_il = malloc(n);
+    float *hs8_il = malloc(nb * 4);
+    uint8_t *gil_c = malloc(il_bytes);
+    float *gil_s = malloc(il_count * 4);
+    HIP_OK(hipMemcpy(gil_c, dil_c, il_bytes, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(gil_s, dil_s, il_count * 4, hipMemcpyDeviceToHost));
+    EXPECT(memcmp(gil_c, hil_c, il_bytes) == 0, "interleaved codes differ from the oracle's");
+    EXPECT(memcmp(gil_s, hil_s, il_count * 4) == 0, "interleaved scales differ from the oracle's");
+    HIP_OK(hipMemcpy(hsec_il, dsec_il, n * 2, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hq8_il, dq8_il, n, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(hs8_il, ds8_il, nb * 4, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(hsec, dsec, n * 2, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(hq8, dq8, n, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(hs8, ds8, nb * 4, hipMemcpyDeviceToHost));
-    for (int k = 0; k < 3; k++) {
+    for (int k = 0; k < 5; k++) {
         for (int a = 0; a < 3; a++) {
             h[k][a] = malloc(n * 4);
             HIP_OK(hipMemcpy(h[k][a], d[k][a], n * 4, hipMemcpyDeviceToHost));
@@ -189,13 +234,16 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         HIP_OK(hipMemcpy(hp16[k], dprim[k], n * 2, hipMemcpyDeviceToHost));
     }
     HIP_OK(hipMemcpy(hg, dgrad, n * 4, hipMemcpyDeviceToHost));
-    for (int k = 1; k < 3; k++) {
+    for (int k = 1; k < 5; k++) {
         for (int a = 0; a < 3; a++)
             EXPECT(memcmp(h[0][a], h[k][a], n * 4) == 0, "receive %d: state array %d differs", k,
                    a);
         EXPECT(memcmp(hp16[0], hp16[k], n * 2) == 0, "receive %d: primary differs", k);
     }
     EXPECT(memcmp(hsec, hp16[0], n * 2) == 0, "single receive pass: secondary differs");
+    EXPECT(memcmp(hsec_il, hp16[0], n * 2) == 0, "interleaved single pass: secondary differs");
+    EXPECT(memcmp(hq8_il, hq8, n) == 0, "interleaved single pass: codes differ");
+    EXPECT(memcmp(hs8_il, hs8, nb * 4) == 0, "interleaved single pass: scales differ");
     orc_quantize_blockwise_i8(hp16[0], n, B, rq8, rs8);
     EXPECT(memcmp(hq8, rq8, n) == 0, "single receive pass: codes differ from the oracle's");
     EXPECT(memcmp(hs8, rs8, nb * 4) == 0, "single receive pass: scales differ from the oracle's");
@@ -211,8 +259,9 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
     for (size_t i = 0; i < n; i++)
         if ((e = rel_err(h[1][0][i], rp[i], hp->lr)) > ep) ep = e;
     EXPECT(ep <= 1e-5, "fused receive master rel err %g", ep);
-    printf("qgz receive step and single pass: %u sources, bit-identical to reduce + step, "
-           "codes and scales equal to the oracle's, master rel err %.3g\n",
+    printf("qgz receive step and single pass: %u sources, separate or interleaved, "
+           "bit-identical to reduce + step, codes and scales equal to the oracle's, "
+           "master rel err %.3g\n",
            NSRC, ep);
     HIP_OK(hipStreamDestroy(up));
     HIP_OK(hipStreamDestroy(st));

@@ -2,8 +2,9 @@
 the repository's build step) runs one iteration of the path with hipMalloc'd
 buffers, three streams and caller-owned events, and checks it against the
 oracle's C library; then the qgZ receive fused into the partition step,
-against the dequantize-and-reduce followed by the step.  It runs as a child
-process of the test runner."""
+against the dequantize-and-reduce followed by the step, from separate int4
+arrays and from one interleaved receive buffer.  It runs as a child process
+of the test runner."""
 import os
 import subprocess
 import sys

@@ -117,22 +117,31 @@ def test_iteration_in_a_hip_graph(zpp, fused):
         h.hipGraphDestroy(graph)
 
 
+@pytest.mark.parametrize("interleaved", [False, True], ids=["separate", "interleaved"])
 @pytest.mark.parametrize("single_pass", [False, True], ids=["step", "single-pass"])
-def test_receive_iteration_in_a_hip_graph(zpp, single_pass):
+def test_receive_iteration_in_a_hip_graph(zpp, single_pass, interleaved):
     """An iteration that opens with the qgZ receive fused into the partition
     step (int4 gradient copies -> Adam), then the refresh, the quantization
     (or all three in the single receive pass) and the gather, on one stream,
     captured into a HIP graph and replayed three times with eager work in
     between: every replay equals the same iteration run eagerly from the same
-    state, bit for bit."""
+    state, bit for bit.  `interleaved`: the int4 copies in one interleaved
+    receive buffer, each written into its slots by the int4 quantizer."""
     n, B, P, P2 = (1 << 20) + 256, 256, 4, 2
     hp = dict(lr=float(np.float32(1e-4)), beta1=float(np.float32(0.9)),
               beta2=float(np.float32(0.95)), eps=float(np.float32(1e-8)),
               weight_decay=float(np.float32(0.1)))
     p0 = torch.from_numpy(synth.master_weights(n, 111)).cuda()
     src_c, src_s = [], []
+    if interleaved:
+        nc, ns = zpp.interleaved_sizes(n, B, P)
+        il_c = torch.zeros(nc, dtype=torch.uint8, device="cuda")
+        il_s = torch.zeros(ns, dtype=torch.float32, device="cuda")
     for q in range(P):
         g = synth.device_normal_f32(n, synth.GRAD_STD, 111, synth.KIND_GRAD, rank=q)
+        if interleaved:
+            zpp.quantize_blockwise_i4_interleaved(g, il_c, il_s, source=q, num_src=P, block=B)
+            continue
         c = torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda")
         s = torch.empty((n + B - 1) // B, dtype=torch.float32, device="cuda")
         zpp.quantize_blockwise_i4(g, c, s, block=B)
@@ -153,14 +162,25 @@ def test_receive_iteration_in_a_hip_graph(zpp, single_pass):
     stream = torch.cuda.Stream()
 
     def iteration(st):
-        if single_pass:
+        if single_pass and interleaved:
+            zpp.qgz_receive_step_refresh_quantize_interleaved(
+                st["p"], st["m"], st["v"], il_c, il_s, P, st["prim"], st["sec"], st["codes"],
+                st["scales"], step=1, grad_block=B, block=B, scale_out=1.0 / P, stream=stream,
+                **hp)
+        elif single_pass:
             zpp.qgz_receive_step_refresh_quantize(
                 st["p"], st["m"], st["v"], src_c, src_s, st["prim"], st["sec"], st["codes"],
                 st["scales"], step=1, grad_block=B, block=B, scale_out=1.0 / P, stream=stream,
                 **hp)
-        else:
-            zpp.qgz_receive_adam_step(st["p"], st["m"], st["v"], src_c, src_s, st["prim"],
-                                      step=1, block=B, scale_out=1.0 / P, stream=stream, **hp)
+        if not single_pass:
+            if interleaved:
+                zpp.qgz_receive_adam_step_interleaved(st["p"], st["m"], st["v"], il_c, il_s, P,
+                                                      st["prim"], step=1, block=B,
+                                                      scale_out=1.0 / P, stream=stream, **hp)
+            else:
+                zpp.qgz_receive_adam_step(st["p"], st["m"], st["v"], src_c, src_s, st["prim"],
+                                          step=1, block=B, scale_out=1.0 / P, stream=stream,
+                                          **hp)
             zpp.refresh_secondary(st["sec"], st["prim"], stream=stream)
             zpp.quantize_blockwise_i8(st["sec"], st["codes"], st["scales"], block=B,
                                       stream=stream)
