@@ -22,8 +22,8 @@ three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
 timing only), the qgZ gradient side, the step preceded by the qgZ receive
 (as its own kernel, fused into the partition step, and inside the single
-pass of step, refresh and quantization; the last two also with the eight
-int4 copies interleaved in one receive buffer), and, for context,
+pass of step, refresh and quantization; all three also with the eight int4
+copies interleaved in one receive buffer), and, for context,
 PyTorch's fused AdamW on a partition of the same size.  The
 CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
@@ -418,6 +418,10 @@ def main():
         pipe.exchange.quantize(q, g)
         del g
     torch.cuda.synchronize()
+    pipe.fuse_receive = False
+    ilr_ms, ilr_times, ilr_kb, ilr_step_bytes = run(False, "event", True)
+    ilr_gbps = ilr_step_bytes / (ilr_ms * 1e-3) / 1e9
+    pipe.fuse_receive = True
     il_ms, il_times, il_kb, il_step_bytes = run(False, "event", True)
     il_gbps = il_step_bytes / (il_ms * 1e-3) / 1e9
     ilf_ms, ilf_times, ilf_kb, ilf_step_bytes = run(True, "event", True)
@@ -494,6 +498,10 @@ def main():
             "ms_per_step": round(ff_ms, 4), "GB/s": round(ff_gbps, 1),
             "frac_of_peak": round(ff_gbps / HBM_PEAK_GBPS, 4),
             "kernels": kernel_table(ff_kb, ff_times)},
+        "step_with_qgz_receive_interleaved": {
+            "ms_per_step": round(ilr_ms, 4), "GB/s": round(ilr_gbps, 1),
+            "frac_of_peak": round(ilr_gbps / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(ilr_kb, ilr_times)},
         "step_with_fused_qgz_receive_interleaved": {
             "ms_per_step": round(il_ms, 4), "GB/s": round(il_gbps, 1),
             "frac_of_peak": round(il_gbps / HBM_PEAK_GBPS, 4),

@@ -320,6 +320,21 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4_interleaved(const float *src, size_
                                                          hipEvent_t wait_before,
                                                          hipEvent_t done_after);
 
+/* zpp_dequant_reduce_i4 with its num_src int4 copies in one interleaved
+ * receive buffer (layout above): the same arithmetic in the same order, so
+ * the same bits.  codes, scales: DEVICE pointers to the interleaved buffer,
+ * B = block.  n <= SIZE_MAX / 16 / num_src.  out: float[n], which must not
+ * overlap the buffer (ZPP_EOVERLAP).  Order on `stream`: wait for every
+ * event of wait_events[0..num_wait), reduce, record `done_after`.
+ * Alignment: out and scales 4 bytes (ZPP_EALIGN); 16-byte out and 2-byte
+ * codes select the vector kernel. */
+ZPP_API zpp_status zpp_dequant_reduce_i4_interleaved(const uint8_t *codes, const float *scales,
+                                                     uint32_t num_src, size_t n, uint32_t block,
+                                                     float scale_out, float *out,
+                                                     hipStream_t stream,
+                                                     const hipEvent_t *wait_events,
+                                                     uint32_t num_wait, hipEvent_t done_after);
+
 /* zpp_qgz_receive_adam_step with its num_src int4 copies in one interleaved
  * receive buffer (layout above): the same arithmetic in the same order, so
  * the same bits.  codes, scales: DEVICE pointers to the interleaved buffer,

@@ -14,10 +14,15 @@
 // sources' pointers travel by value in the kernel arguments; a lane
 // accumulates its elements over the sources in order, one fma each.
 //
+// The dequant-reduce also reads the P copies from one interleaved receive
+// buffer (layout in zpp_i4grad.h): the gradient source of the receive
+// kernels forms each float4, so the bits are those of the separate arrays.
+//
 // Both kernels keep every wave's loads and stores contiguous: on this GPU,
 // non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
 // lane at a 32- or 64-byte stride) run two to three times slower.
 #include "zpp_device.h"
+#include "zpp_i4grad.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
 
@@ -29,6 +34,9 @@
 #endif
 #ifndef ZPP_QGZ_REDUCE_GROUPS
 #define ZPP_QGZ_REDUCE_GROUPS 2
+#endif
+#ifndef ZPP_QGZ_REDUCE_IL_GROUPS
+#define ZPP_QGZ_REDUCE_IL_GROUPS 2
 #endif
 #ifndef ZPP_QGZ_MAX_GRID
 #define ZPP_QGZ_MAX_GRID (1u << 30)
@@ -293,6 +301,51 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_scalar_kernel(ReduceArg
     }
 }
 
+// The reduction from a gradient source of zpp_i4grad.h: a lane holds G
+// groups of 4 consecutive elements at 256 t + 4 l of its wave's tile, as
+// above; each group is the source's gradient of those four elements, stored
+// as one float4 (1 KiB contiguous per wave store).  Partial tiles go element
+// by element.
+template <class GS, int G>
+__global__ __launch_bounds__(kQgzThreads) void reduce_gs_kernel(GS gs, size_t n,
+                                                               float *__restrict__ out) {
+    constexpr int kWaves = kQgzThreads / kWave;
+    constexpr size_t C = 256 * G;
+    const size_t ntiles = (n + C - 1) / C;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    for (size_t tile = (size_t)blockIdx.x * kWaves + wave; tile < ntiles;
+         tile += (size_t)gridDim.x * kWaves) {
+        const size_t base = tile * C + (size_t)lane * 4;
+        if (tile * C + C <= n) {
+            f32x4 r[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                r[g] = grad_load4(gs, base + (size_t)g * 256);
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                st_nt(reinterpret_cast<f32x4 *>(out + base + (size_t)g * 256), r[g]);
+        } else {
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                for (int e = 0; e < 4; ++e) {
+                    const size_t i = base + (size_t)g * 256 + e;
+                    if (i < n)
+                        out[i] = grad_at(gs, i);
+                }
+        }
+    }
+}
+
+// Any alignment: one element per thread.
+template <class GS>
+__global__ __launch_bounds__(kQgzThreads) void reduce_gs_scalar_kernel(GS gs, size_t n,
+                                                                      float *__restrict__ out) {
+    for (size_t i = (size_t)blockIdx.x * kQgzThreads + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * kQgzThreads)
+        out[i] = grad_at(gs, i);
+}
+
 template <int B>
 void launch_quant_i4_b(const float *src, size_t n, uint8_t *codes, float *scales,
                        uint32_t q_src, uint32_t num_src, hipStream_t stream) {
@@ -362,6 +415,27 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
         const size_t need = (n + kQgzThreads - 1) / kQgzThreads;
         const unsigned grid = (unsigned)(need < (1u << 20) ? need : (1u << 20));
         hipLaunchKernelGGL(reduce_i4_scalar_kernel, dim3(grid), dim3(kQgzThreads), 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_dequant_reduce_i4_il(const uint8_t *codes, const float *scales, uint32_t num_src,
+                                       size_t n, uint32_t block, float scale_out, float *out,
+                                       bool vector_path, hipStream_t stream) {
+    const I4GradIl gs = make_i4grad_il(codes, scales, num_src, block, scale_out);
+    if (vector_path) {
+        constexpr size_t C = 256 * ZPP_QGZ_REDUCE_IL_GROUPS;
+        const size_t ntiles = (n + C - 1) / C;
+        const size_t waves = kQgzThreads / kWave;
+        const size_t need = (ntiles + waves - 1) / waves;
+        const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
+        hipLaunchKernelGGL((reduce_gs_kernel<I4GradIl, ZPP_QGZ_REDUCE_IL_GROUPS>), dim3(grid),
+                           dim3(kQgzThreads), 0, stream, gs, n, out);
+    } else {
+        const size_t need = (n + kQgzThreads - 1) / kQgzThreads;
+        const unsigned grid = (unsigned)(need < (1u << 20) ? need : (1u << 20));
+        hipLaunchKernelGGL(reduce_gs_scalar_kernel<I4GradIl>, dim3(grid), dim3(kQgzThreads), 0,
+                           stream, gs, n, out);
     }
     return hipGetLastError();
 }

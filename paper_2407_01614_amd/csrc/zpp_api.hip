@@ -518,6 +518,49 @@ ZPP_API zpp_status zpp_quantize_blockwise_i4_interleaved(const float *src, size_
     return record(stream, done_after);
 }
 
+ZPP_API zpp_status zpp_dequant_reduce_i4_interleaved(const uint8_t *codes, const float *scales,
+                                                     uint32_t num_src, size_t n, uint32_t block,
+                                                     float scale_out, float *out,
+                                                     hipStream_t stream,
+                                                     const hipEvent_t *wait_events,
+                                                     uint32_t num_wait, hipEvent_t done_after) {
+    if (num_src == 0 || num_src > ZPP_MAX_SHARDS || !valid_block(block))
+        return ZPP_EINVAL;
+    if (n > kMaxElems / num_src || !isfinite(scale_out))
+        return ZPP_EINVAL;
+    if (num_wait > ZPP_MAX_WAIT_EVENTS || (num_wait && !wait_events))
+        return ZPP_EINVAL;
+    for (uint32_t w = 0; w < num_wait; ++w)
+        if (!wait_events[w])
+            return ZPP_EINVAL;
+    if (!codes || !scales)
+        return ZPP_EINVAL;
+    if (!aligned(scales, 4))
+        return ZPP_EALIGN;
+    if (n) {
+        if (!out)
+            return ZPP_EINVAL;
+        if (!aligned(out, 4))
+            return ZPP_EALIGN;
+        if (overlaps(out, 4 * n, codes, il_code_bytes(n, block, num_src)) ||
+            overlaps(out, 4 * n, scales, 4 * il_scale_count(n, block, num_src)))
+            return ZPP_EOVERLAP;
+    }
+    for (uint32_t w = 0; w < num_wait; ++w) {
+        const zpp_status st = wait_on(stream, wait_events[w]);
+        if (st != ZPP_OK)
+            return st;
+    }
+    if (n) {
+        const bool vec = aligned(out, 16) && aligned(codes, 2);
+        const hipError_t e = zpp::launch_dequant_reduce_i4_il(codes, scales, num_src, n, block,
+                                                              scale_out, out, vec, stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
 ZPP_API zpp_status zpp_qgz_receive_adam_step_interleaved(
     float *master, float *exp_avg, float *exp_avg_sq, const uint8_t *codes, const float *scales,
     uint32_t num_src, uint32_t block, float scale_out, uint16_t *primary_bf16, size_t n,

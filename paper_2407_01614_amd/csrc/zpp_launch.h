@@ -90,6 +90,11 @@ hipError_t launch_fused_receive_il(float *p, float *m, float *v, const uint8_t *
                                    int8_t *codes, float *scales, size_t n, uint32_t block,
                                    const AdamConsts &c, bool vector_path, hipStream_t stream);
 
+// The dequant-reduce from the interleaved receive buffer.
+hipError_t launch_dequant_reduce_i4_il(const uint8_t *codes, const float *scales, uint32_t num_src,
+                                       size_t n, uint32_t block, float scale_out, float *out,
+                                       bool vector_path, hipStream_t stream);
+
 // int4 quantization of one source's n values into its slots of an
 // interleaved receive buffer of num_src sources (num_src = 1: the plain
 // layout of launch_quantize_i4).

@@ -58,12 +58,10 @@ class PartitionPipeline:
     written), and with `fused` too, inside the single pass of step, refresh
     and quantization (`zpp_qgz_receive_step_refresh_quantize`).
     `qgz_interleaved` keeps the int4 copies in one interleaved receive buffer
-    (`GradientExchange`), which only the fused receive reads."""
+    (`GradientExchange`), read by the `..._interleaved` entry points."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
                  qgz_sources=0, streams=3, fuse_receive=False, qgz_interleaved=False):
-        if qgz_interleaved and not fuse_receive:
-            raise ValueError("an interleaved receive buffer is read by the fused receive only")
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         if streams not in (1, 3):
@@ -406,8 +404,7 @@ class GradientExchange:
     int4 (sources other than this rank are simulated in this GPU's memory),
     and the rank reduces the copies into the fp32 mean gradient that the
     partition step reads.  With `interleaved` the copies arrive in one
-    receive buffer, block by block (the layout of include/zpp.h), which only
-    the receive fused into the partition step reads."""
+    receive buffer, block by block (the layout of include/zpp.h)."""
 
     def __init__(self, n, num_src, block=256, device="cuda", interleaved=False):
         self.n, self.num_src, self.block = n, num_src, block
@@ -434,8 +431,11 @@ class GradientExchange:
 
     def reduce(self, out, stream=None, wait_events=(), done_after=None):
         if self.interleaved:
-            raise ValueError("the separate dequantize-and-reduce reads separate source arrays; "
-                             "an interleaved buffer is read by the fused receive")
+            zpp.dequant_reduce_i4_interleaved(self.codes, self.scales, self.num_src, self.n, out,
+                                              block=self.block, scale_out=1.0 / self.num_src,
+                                              stream=stream, wait_events=wait_events,
+                                              done_after=done_after)
+            return
         zpp.dequant_reduce_i4(self.codes, self.scales, self.n, out, block=self.block,
                               scale_out=1.0 / self.num_src, stream=stream,
                               wait_events=wait_events, done_after=done_after)

@@ -62,6 +62,9 @@ _lib.zpp_qgz_receive_step_refresh_quantize.argtypes = [
 _lib.zpp_quantize_blockwise_i4_interleaved.restype = ctypes.c_int
 _lib.zpp_quantize_blockwise_i4_interleaved.argtypes = [_P, _sz, _u32, _u32, _u32, _P, _P, _P, _P,
                                                        _P]
+_lib.zpp_dequant_reduce_i4_interleaved.restype = ctypes.c_int
+_lib.zpp_dequant_reduce_i4_interleaved.argtypes = [_P, _P, _u32, _sz, _u32, ctypes.c_float, _P,
+                                                   _P, _P, _u32, _P]
 _lib.zpp_qgz_receive_adam_step_interleaved.restype = ctypes.c_int
 _lib.zpp_qgz_receive_adam_step_interleaved.argtypes = [
     _P, _P, _P, _P, _P, _u32, _u32, ctypes.c_float, _P, _sz, ctypes.POINTER(AdamHParams), _P, _P,
@@ -79,7 +82,7 @@ EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_ref
            "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
            "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
            "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
-           "zpp_qgz_receive_adam_step_interleaved",
+           "zpp_dequant_reduce_i4_interleaved", "zpp_qgz_receive_adam_step_interleaved",
            "zpp_qgz_receive_step_refresh_quantize_interleaved", "zpp_status_string",
            "zpp_last_hip_error")
 
@@ -494,6 +497,22 @@ def quantize_blockwise_i4_interleaved(src, codes, scales, *, source, num_src, bl
         src.data_ptr(), n, block, source, num_src, codes.data_ptr(), scales.data_ptr(),
         stream_handle(stream), _event_handle(wait_before), _event_handle(done_after))
     _check(st, "zpp_quantize_blockwise_i4_interleaved")
+
+
+def dequant_reduce_i4_interleaved(codes, scales, num_src, n, out, *, block=256, scale_out=1.0,
+                                  stream=None, wait_events=(), done_after=None):
+    """zpp_dequant_reduce_i4_interleaved: the num_src int4 copies of one
+    interleaved receive buffer reduced into out[:n]."""
+    _interleaved_inputs(codes, scales, n, block, num_src)
+    _dev(out, _F32, "out")
+    if out.numel() < n:
+        raise ValueError("out holds fewer than n elements")
+    waits = [_event_handle(e) for e in wait_events]
+    warr = (_P * len(waits))(*waits) if waits else None
+    st = _lib.zpp_dequant_reduce_i4_interleaved(
+        codes.data_ptr(), scales.data_ptr(), num_src, n, block, scale_out, out.data_ptr(),
+        stream_handle(stream), warr, len(waits), _event_handle(done_after))
+    _check(st, "zpp_dequant_reduce_i4_interleaved")
 
 
 def qgz_receive_adam_step_interleaved(master, exp_avg, exp_avg_sq, codes, scales, num_src,

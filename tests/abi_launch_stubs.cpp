@@ -60,6 +60,10 @@ hipError_t launch_quantize_i4_il(const float *, size_t, uint32_t, uint32_t, uint
                                  float *, bool, hipStream_t) {
     return reached();
 }
+hipError_t launch_dequant_reduce_i4_il(const uint8_t *, const float *, uint32_t, size_t, uint32_t,
+                                       float, float *, bool, hipStream_t) {
+    return reached();
+}
 hipError_t launch_receive_adam_il(float *, float *, float *, const uint8_t *, const float *,
                                   uint32_t, uint32_t, float, uint16_t *, size_t, const AdamConsts &,
                                   bool, hipStream_t) {

@@ -323,6 +323,16 @@ static void check_interleaved(void)
         EXPECT_STATUS(zpp_quantize_blockwise_i4_interleaved(x, n, 256, 0, P, (uint8_t *)dev_off(3, 8),
                                                             is, NULL, NULL, NULL),
                       ZPP_EOVERLAP);
+        EXPECT_STATUS(zpp_dequant_reduce_i4_interleaved(ic, is, P, 0, 256, 0.5f, NULL, NULL, NULL,
+                                                        0, NULL),
+                      ZPP_OK);
+        EXPECT_STATUS(zpp_dequant_reduce_i4_interleaved(ic, is, P, n, 256, 0.5f, NULL, NULL, waits,
+                                                        W, NULL),
+                      ZPP_EINVAL);
+        EXPECT_STATUS(zpp_dequant_reduce_i4_interleaved(ic, is, P, n, 256, 0.5f,
+                                                        (float *)dev_off(9, 0), NULL, NULL, 0,
+                                                        NULL),
+                      ZPP_EOVERLAP);
         EXPECT_STATUS(zpp_qgz_receive_adam_step_interleaved(p, m, v, ic, is, P, 256, 0.5f, pr, 0, &hp,
                                                             NULL, NULL, 0, NULL),
                       ZPP_OK);

@@ -177,7 +177,7 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         }
         dprim[k] = dev_alloc(n * 2);
     }
-    float *dgrad = dev_alloc(n * 4);
+    float *dgrad = dev_alloc(n * 4), *dgrad_il = dev_alloc(n * 4);
     uint16_t *dsec = dev_alloc(n * 2);
     int8_t *dq8 = dev_alloc(n);
     float *ds8 = dev_alloc(nb * 4);
@@ -199,6 +199,9 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
                                                  scale_out, dprim[2], dsec, dq8, ds8, n, B, hp,
                                                  st, &uploaded, 1, NULL) == ZPP_OK,
            "single receive pass");
+    EXPECT(zpp_dequant_reduce_i4_interleaved(dil_c, dil_s, NSRC, n, B, scale_out, dgrad_il, st,
+                                             &uploaded, 1, NULL) == ZPP_OK,
+           "dequant-reduce from the interleaved buffer");
     EXPECT(zpp_qgz_receive_adam_step_interleaved(d[3][0], d[3][1], d[3][2], dil_c, dil_s, NSRC,
                                                  B, scale_out, dprim[3], n, hp, st, &uploaded, 1,
                                                  NULL) == ZPP_OK,
@@ -234,6 +237,9 @@ static void check_receive(size_t n, const float *p0, const zpp_adam_hparams *hp)
         HIP_OK(hipMemcpy(hp16[k], dprim[k], n * 2, hipMemcpyDeviceToHost));
     }
     HIP_OK(hipMemcpy(hg, dgrad, n * 4, hipMemcpyDeviceToHost));
+    float *hg_il = malloc(n * 4);
+    HIP_OK(hipMemcpy(hg_il, dgrad_il, n * 4, hipMemcpyDeviceToHost));
+    EXPECT(memcmp(hg_il, hg, n * 4) == 0, "interleaved dequant-reduce differs");
     for (int k = 1; k < 5; k++) {
         for (int a = 0; a < 3; a++)
             EXPECT(memcmp(h[0][a], h[k][a], n * 4) == 0, "receive %d: state array %d differs", k,

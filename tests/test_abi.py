@@ -31,13 +31,13 @@ def declared_functions():
     return sorted(set(re.findall(r"ZPP_API\s+[\w\s\*]*?\b(zpp_\w+)\s*\(", text)))
 
 
-def test_header_declares_the_four_calls():
+def test_header_declares_every_entry_point():
     names = declared_functions()
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
                "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
                "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
                "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
-               "zpp_qgz_receive_adam_step_interleaved",
+               "zpp_dequant_reduce_i4_interleaved", "zpp_qgz_receive_adam_step_interleaved",
                "zpp_qgz_receive_step_refresh_quantize_interleaved", "zpp_status_string",
                "zpp_last_hip_error"):
         assert fn in names
@@ -350,6 +350,34 @@ def test_quantize_i4_interleaved_validation(zpp):
     assert quant_il(zpp, scales=H + 2) == zpp.ZPP_EALIGN
     assert quant_il(zpp, codes=A + 16) == zpp.ZPP_EOVERLAP        # codes inside src
     assert quant_il(zpp, scales=F + 4000) == zpp.ZPP_EOVERLAP    # scales inside the codes buffer
+
+
+def reduce_il(zpp, codes=F, scales=H, num=8, n=1024, block=256, scale_out=0.5, out=A,
+              waits=None, nwait=0):
+    P = ctypes.c_void_p
+    warr = (P * max(nwait, 1))(*(waits or [])) if waits is not None else None
+    return zpp.raw.zpp_dequant_reduce_i4_interleaved(codes, scales, num, n, block, scale_out, out,
+                                                     None, warr, nwait, None)
+
+
+def test_dequant_reduce_i4_interleaved_validation(zpp):
+    """Every case fails validation (or is a size-0 no-op): none reaches a launch."""
+    assert reduce_il(zpp, n=0, out=None) == zpp.ZPP_OK
+    assert reduce_il(zpp, num=0) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, num=65) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, block=96) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, scale_out=float("nan")) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, n=(1 << 64) // 16 // 8 + 1) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, codes=None) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, scales=None) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, out=None) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, scales=H + 2) == zpp.ZPP_EALIGN
+    assert reduce_il(zpp, out=A + 2) == zpp.ZPP_EALIGN
+    assert reduce_il(zpp, out=F + 1024) == zpp.ZPP_EOVERLAP      # out inside the codes
+    assert reduce_il(zpp, out=H - 16) == zpp.ZPP_EOVERLAP        # out runs into the scales
+    assert reduce_il(zpp, nwait=1, waits=None) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, nwait=2, waits=[A, None]) == zpp.ZPP_EINVAL
+    assert reduce_il(zpp, nwait=65, waits=[A] * 65) == zpp.ZPP_EINVAL
 
 
 def receive_il(zpp, state=(A, B, C, E), codes=F, scales=H, num=8, n=1024, block=256,

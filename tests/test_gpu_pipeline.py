@@ -481,11 +481,14 @@ def test_pipeline_fused_receive_equals_separate(zpp, streams):
             assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)
 
 
-@pytest.mark.parametrize("fused", [False, True], ids=["step", "single-pass"])
-def test_pipeline_interleaved_receive_equals_separate(zpp, fused):
+@pytest.mark.parametrize("fused,fuse", [(False, False), (True, False), (False, True),
+                                        (True, True)],
+                         ids=["reduce-step", "reduce-fused", "receive-step", "single-pass"])
+def test_pipeline_interleaved_receive_equals_separate(zpp, fused, fuse):
     """The pipeline with its 8 int4 copies in one interleaved receive buffer
     (each quantized into its slots on the device) ends two steps in the same
-    state as with the oracle's copies in separate arrays, bit for bit."""
+    state as with the oracle's copies in separate arrays, bit for bit, with
+    the receive as its own dequantize-and-reduce kernel or fused."""
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import Workload
     wl = Workload(name="small-qgz-il", cfg_id=15, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
@@ -497,7 +500,7 @@ def test_pipeline_interleaved_receive_equals_separate(zpp, fused):
     p0 = synth.master_weights(wl.n, wl.cfg_id)
     results = []
     for il in (False, True):
-        pipe = PartitionPipeline(wl, qgz_sources=P, fused=fused, fuse_receive=True,
+        pipe = PartitionPipeline(wl, qgz_sources=P, fused=fused, fuse_receive=fuse,
                                  qgz_interleaved=il)
         pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
         for q, x in enumerate(srcs):
@@ -519,9 +522,3 @@ def test_pipeline_interleaved_receive_equals_separate(zpp, fused):
     for i, (a, b) in enumerate(zip(results[1], results[0])):
         assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "output %d" % i)
 
-
-def test_pipeline_interleaved_needs_fused_receive():
-    from paper_2407_01614_amd.pipeline import PartitionPipeline
-    from paper_2407_01614_amd.workloads import WORKLOADS
-    with pytest.raises(ValueError):
-        PartitionPipeline(WORKLOADS["tiny"], qgz_sources=8, qgz_interleaved=True)

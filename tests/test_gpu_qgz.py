@@ -708,3 +708,99 @@ def test_fullsize_receive_interleaved(zpp):
             assert torch.equal(a, b), "interleaved %s differs" % ("pass" if single else "step")
         del outs
         torch.cuda.empty_cache()
+
+
+def run_reduce_il(zpp, quants, n, block, scale_out, pad_out=0, pad_codes=0):
+    ic, isc = interleave(quants, n, block)
+    out = empty_dev(n, np.float32, pad=pad_out, fill=-7.0)
+    zpp.dequant_reduce_i4_interleaved(u8_dev(ic, pad=pad_codes), to_dev(isc), len(quants), n,
+                                      out, block=block, scale_out=scale_out)
+    torch.cuda.synchronize()
+    return to_host(out, np.float32)
+
+
+@pytest.mark.parametrize("P,n,block", [
+    (1, 1, 256), (2, 7, 64), (8, 9, 256), (3, 256 * 5 + 3, 128), (8, 65536 + 8, 256),
+    (8, 100001, 1024), (64, 256 * 5 + 3, 256), (5, 4096 * 3 + 500, 4096), (16, 512 * 9, 64)])
+def test_dequant_reduce_interleaved_vs_oracle(zpp, P, n, block):
+    """The dequant-reduce from one interleaved receive buffer against the
+    oracle's reduction of the same P copies (separate arrays), bit for bit."""
+    quants = oracle_sources(P, n, block, 170 + n)
+    for scale_out in (1.0, float(np.float32(1.0 / P))):
+        got = run_reduce_il(zpp, quants, n, block, scale_out)
+        ref = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
+                                       scale_out)
+        assert_bits_equal(got, ref, "P=%d n=%d block %d scale_out=%g" % (P, n, block, scale_out))
+
+
+@pytest.mark.parametrize("pads", [(1, 0), (0, 1), (0, 2)], ids=["out", "codes-odd", "codes-2"])
+def test_dequant_reduce_interleaved_misaligned(zpp, pads):
+    """A misaligned output or codes at an odd address take the any-alignment
+    kernel; codes at a 2-byte address keep the vector kernel: the oracle's
+    bits either way."""
+    n, block, P = 256 * 11 + 5, 128, 5
+    quants = oracle_sources(P, n, block, 171)
+    got = run_reduce_il(zpp, quants, n, block, 0.2, *pads)
+    ref = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
+                                   float(np.float32(0.2)))
+    assert_bits_equal(got, ref, "misaligned %s" % (pads,))
+
+
+def test_dequant_reduce_interleaved_special_scales(zpp):
+    """NaN, Inf, zero and subnormal source scales reach the output as the
+    oracle's reduction has them."""
+    n, block, P = 256 * 8, 256, 4
+    quants = oracle_sources(P, n, block, 172)
+    quants[1][1][2] = np.nan
+    quants[2][1][3] = np.inf
+    quants[3][1][4] = 0.0
+    quants[0][1][5] = 1e-40
+    got = run_reduce_il(zpp, quants, n, block, 1.0)
+    ref = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block, 1.0)
+    assert_bits_equal(got, ref, "special scales")
+
+
+def test_fullsize_reduce_interleaved(zpp):
+    """The Llama-2-13B partition from 8 int4 sources quantized on the device
+    into separate arrays and into one interleaved buffer: the two reductions
+    are equal bit for bit, and sampled blocks (the partial last one among
+    them) equal the oracle's quantization and reduction of the same sources."""
+    wl = WORKLOADS["llama-2-13b"]
+    n, B, P = wl.n, wl.block, 8
+    nb = (n + B - 1) // B
+    g = np.random.default_rng(173)
+    kb = np.unique(np.concatenate([g.integers(0, nb - 1, size=512), [0, nb - 2]]))
+    eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
+    lo = (nb - 1) * B
+    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
+    nc, ns = zpp.interleaved_sizes(n, B, P)
+    ic = torch.zeros(nc, dtype=torch.uint8, device="cuda")
+    isc = torch.zeros(ns, dtype=torch.float32, device="cuda")
+    hsrc, tails = [], []
+    for q in range(P):
+        src = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, rank=q)
+        hsrc.append(src.index_select(0, eidx).cpu().numpy())
+        tails.append(src[lo:].cpu().numpy())
+        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=B)
+        zpp.quantize_blockwise_i4_interleaved(src, ic, isc, source=q, num_src=P, block=B)
+        torch.cuda.synchronize()
+        del src
+    outs = []
+    for il in (False, True):
+        out = torch.empty(n, dtype=torch.float32, device="cuda")
+        if il:
+            zpp.dequant_reduce_i4_interleaved(ic, isc, P, n, out, block=B, scale_out=0.125)
+        else:
+            zpp.dequant_reduce_i4(codes, scales, n, out, block=B, scale_out=0.125)
+        torch.cuda.synchronize()
+        outs.append(out)
+    assert torch.equal(outs[0], outs[1])
+    rq = [oracle.quantize_blockwise_i4(h, B) for h in hsrc]
+    ref = oracle.dequant_reduce_i4([c for c, _ in rq], [s for _, s in rq], kb.size * B, B, 0.125)
+    assert_bits_equal(outs[1].index_select(0, eidx).cpu().numpy(), ref, "sampled mean")
+    rt = [oracle.quantize_blockwise_i4(t, B) for t in tails]
+    reft = oracle.dequant_reduce_i4([c for c, _ in rt], [s for _, s in rt], n - lo, B, 0.125)
+    assert_bits_equal(outs[1][lo:].cpu().numpy(), reft, "tail mean")
+    del outs, codes, scales, ic, isc
+    torch.cuda.empty_cache()
