@@ -23,7 +23,9 @@ event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
 timing only), the qgZ gradient side, the step preceded by the qgZ receive
 (as its own kernel, fused into the partition step, and inside the single
 pass of step, refresh and quantization; all three also with the eight int4
-copies interleaved in one receive buffer), and, for context,
+copies interleaved in one receive buffer), the forward AllGather(L, P) with
+qwZ as one GPU carries it (the layer from all P ranks' int8 primary slices),
+and, for context,
 PyTorch's fused AdamW on a partition of the same size.  The
 CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
@@ -131,6 +133,50 @@ def qgz_measure(pipe, wl, reps, num_src=8):
     res["sources"] = num_src
     del ex, out
     return res
+
+
+def forward_gather_measure(wl, reps):
+    """The forward AllGather(L, P) with qwZ, as far as one GPU carries it:
+    the layer assembled from all P ranks' int8-quantized primary slices (P =
+    the workload's data-parallel world, slices of ceil(N/P) rounded up to the
+    block), by the same dequant-gather kernel over P shards (64 at most per
+    call; a larger world takes several calls, each writing its part of the
+    layer).  The exchange that brings the slices from the other nodes needs
+    more GPUs.  Timed with events over `reps` launches."""
+    import torch
+    from paper_2407_01614_amd import synth, zpp
+    from paper_2407_01614_amd.workloads import bytes_gather, secondary_elems
+    P, N, B = wl.world, wl.layer_elems, wl.block
+    s = secondary_elems(N, P, B)
+    codes = [synth.device_random_codes(s, wl.cfg_id, rank=1000 + j) for j in range(P)]
+    scales = [synth.device_random_scales(s // B, wl.cfg_id, rank=1000 + j) for j in range(P)]
+    out = torch.empty(N, dtype=torch.int16, device="cuda")
+    stream = torch.cuda.Stream()
+    G = zpp.MAX_SHARDS
+
+    def once():
+        for g0 in range(0, P, G):
+            part = min(N - g0 * s, min(G, P - g0) * s)
+            if part > 0:
+                zpp.dequant_gather_layer(codes[g0:g0 + G], scales[g0:g0 + G], s, part,
+                                         out[g0 * s:], block=B, stream=stream)
+
+    once()
+    evs = []
+    for _ in range(reps):
+        a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+        a.record(stream)
+        once()
+        b.record(stream)
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    mean = sum(a.elapsed_ms(b) for a, b in evs) / len(evs)
+    nbytes = bytes_gather(s, P, N, B)
+    gbps = nbytes / (mean * 1e-3) / 1e9
+    del codes, scales, out
+    return {"ranks": P, "slice_elems": s, "layer_elems": N, "launches_per_gather": -(-P // G),
+            "bytes": nbytes, "mean_us": round(mean * 1e3, 2), "GB/s": round(gbps, 1),
+            "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def torch_adamw_context(wl, reps):
@@ -517,6 +563,8 @@ def main():
                 "clocks": clocks},
     }
     del pipe
+    torch.cuda.empty_cache()
+    line["forward_gather_qwz"] = forward_gather_measure(wl, args.steps)
     torch.cuda.empty_cache()
     if args.cpu_sample > 0:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample, steps=args.cpu_steps)

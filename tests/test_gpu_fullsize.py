@@ -20,7 +20,7 @@ import torch
 import oracle
 from paper_2407_01614_amd import synth
 from paper_2407_01614_amd.pipeline import PartitionPipeline
-from paper_2407_01614_amd.workloads import WORKLOADS
+from paper_2407_01614_amd.workloads import WORKLOADS, secondary_elems
 from parity import ChunkedAdam, assert_adam_close, assert_bits_equal
 
 pytestmark = pytest.mark.gpu
@@ -143,6 +143,38 @@ def test_fullsize_gather(zpp, wl):
             [hc[j]], [hs[j]], s, B, min(s, N - j * s)), range(P2)))
     assert_bits_equal(out.cpu().numpy().view(np.uint16), np.concatenate(ref), "whole layer")
     assert not bool(((out & 0x7FFF) > 0x7F80).any()), "NaN in the gathered layer"
+
+
+@pytest.mark.parametrize("name", ["llama-2-13b", "falcon-40b"])
+def test_fullsize_forward_gather(zpp, name):
+    """The forward AllGather(L, P) with qwZ as one GPU carries it, in the
+    calls the benchmark times: the layer from all P ranks' int8 slices (64
+    slices with a padded last one for Llama-2-13B; 128 for Falcon-40B, two
+    calls of 64 each writing its half), the whole layer against the oracle,
+    bit for bit."""
+    wl = WORKLOADS[name]
+    N, P, B = wl.layer_elems, wl.world, wl.block
+    s = oracle.secondary_shard_elems(N, P, B)
+    assert s == secondary_elems(N, P, B)
+    codes = [synth.device_random_codes(s, wl.cfg_id, rank=1000 + j) for j in range(P)]
+    scales = [synth.device_random_scales(s // B, wl.cfg_id, rank=1000 + j) for j in range(P)]
+    out = torch.full((N,), 0x5A5A, dtype=torch.int16, device="cuda")
+    G = zpp.MAX_SHARDS
+    torch.cuda.synchronize()
+    for g0 in range(0, P, G):
+        part = min(N - g0 * s, min(G, P - g0) * s)
+        zpp.dequant_gather_layer(codes[g0:g0 + G], scales[g0:g0 + G], s, part, out[g0 * s:],
+                                 block=B)
+    torch.cuda.synchronize()
+    hc = [c.cpu().numpy() for c in codes]
+    hs = [x.cpu().numpy() for x in scales]
+    del codes, scales
+    with pool() as ex:
+        ref = list(ex.map(lambda j: oracle.dequant_gather_layer(
+            [hc[j]], [hs[j]], s, B, min(s, N - j * s)), range(P)))
+    assert_bits_equal(out.cpu().numpy().view(np.uint16), np.concatenate(ref), "whole layer")
+    del out
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("streams", [1, 3])
