@@ -20,7 +20,9 @@
 // at the Llama-2-13B partition (9-20 within 1%), 1127-1145 us uncapped.  With
 // the qgZ receive in place of the fp32 gradient (8 int4 sources) the cap is
 // ZPP_FUSED_RECV_RESIDENCY: 1111 us with 13, 1118 with 14, 1150 with 12, 1216
-// with 11, 1142 uncapped.
+// with 11, 1142 uncapped.  From one interleaved receive buffer
+// (ZPP_FUSED_RECV_IL_RESIDENCY): 1054 us with 14, 1062 with 16, 1075 with 12,
+// 1097 uncapped, against 1096 us from separate arrays in the same run.
 #include "zpp_adam.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"

@@ -23,6 +23,11 @@
 // 1027 us uncapped.  Scales loaded as wave-uniform scalar loads (possible for
 // blocks of 256 or more) took 1112-1251 us: the scalar cache's latency is not
 // hidden the way the vector loads' is.
+//
+// The same kernel reads the P copies from one interleaved receive buffer
+// (I4GradIl, zpp_i4grad.h: a wave's codes of all sources within one
+// contiguous run): 938 us with ZPP_RECV_IL_RESIDENCY = 12 (14: 949, 16: 955,
+// uncapped 978) against 981 us from separate arrays in the same run.
 #include "zpp_adam.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"
