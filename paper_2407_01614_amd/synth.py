@@ -104,6 +104,14 @@ def device_random_codes(n, cfg, rank=0, device="cuda"):
                          generator=_device_gen(cfg, KIND_CODES, rank, 0, device))
 
 
+def device_random_packed_i4(nbytes, cfg, rank=0, device="cuda"):
+    """Arbitrary bytes, i.e. pairs of 4-bit two's-complement codes (every
+    nibble from -8 to 7), drawn on the device."""
+    torch = torch_mod()
+    return torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device=device,
+                         generator=_device_gen(cfg, KIND_CODES, rank, 1, device))
+
+
 def device_random_scales(nblocks, cfg, rank=0, lo=1e-5, hi=1e-3, device="cuda"):
     """Positive float32 scales, log-uniform in [lo, hi], drawn on the device."""
     torch = torch_mod()

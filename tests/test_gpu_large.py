@@ -119,7 +119,8 @@ def test_gather_past_4g(zpp):
 @pytest.mark.parametrize("single_pass", [False, True], ids=["step", "single-pass"])
 def test_receive_adam_past_4g(zpp, single_pass):
     """The qgZ receive fused into the partition step over more than 2^32
-    elements from 2 int4 sources: sampled whole blocks (around 2^32 and the
+    elements from 2 int4 sources (arbitrary packed codes and scales from the
+    input generator): sampled whole blocks (around 2^32 and the
     ragged tail included) against the oracle's dequantize-and-reduce followed
     by its Adam step.  The single pass also writes the secondary (equal to the
     primary everywhere) and its int8 quantization (the oracle's quantization
@@ -128,14 +129,10 @@ def test_receive_adam_past_4g(zpp, single_pass):
     nb = (n + B - 1) // B
     hp = {k: float(np.float32(v)) for k, v in
           dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1).items()}
-    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
-    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
-    for q in range(P):
-        src = synth.device_normal_f32(n, synth.GRAD_STD, 104, synth.KIND_GRAD, rank=q)
-        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=B)
-        torch.cuda.synchronize()
-        del src
-    torch.cuda.empty_cache()
+    # the int4 copies as the exchange would deliver them: arbitrary packed
+    # codes and scales drawn by the input generator
+    codes = [synth.device_random_packed_i4((n + 1) // 2, 104, rank=q) for q in range(P)]
+    scales = [synth.device_random_scales(nb, 104, rank=q, lo=1e-5, hi=2e-4) for q in range(P)]
     p = synth.device_normal_f32(n, synth.WEIGHT_STD, 104, synth.KIND_MASTER)
     m = torch.zeros(n, device="cuda")
     v = torch.zeros(n, device="cuda")

@@ -317,23 +317,20 @@ def test_receive_adam_special_scales(zpp):
 
 
 def test_fullsize_receive_adam(zpp):
-    """The Llama-2-13B partition from 8 int4 sources, in the configuration the
-    benchmark times: the whole state after the fused receive equals the
-    reduce-then-step sequence (compared on the device), and the whole
-    gradient the sequence formed equals the oracle's."""
+    """The Llama-2-13B partition from 8 int4 sources (arbitrary packed codes
+    and scales drawn by the input generator, every nibble from -8 to 7): the
+    whole state after the fused receive equals the reduce-then-step sequence
+    (compared on the device), and the whole gradient the sequence formed
+    equals the oracle's reduction of the same copies."""
     import os
     from concurrent.futures import ThreadPoolExecutor
     wl = WORKLOADS["llama-2-13b"]
     n, block, P = wl.n, wl.block, 8
     nb = (n + block - 1) // block
     hp = f32hp(wl.adam)
-    codes = [torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda") for _ in range(P)]
-    scales = [torch.empty(nb, dtype=torch.float32, device="cuda") for _ in range(P)]
-    for q in range(P):
-        src = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD, rank=q)
-        zpp.quantize_blockwise_i4(src, codes[q], scales[q], block=block)
-        torch.cuda.synchronize()
-        del src
+    codes = [synth.device_random_packed_i4((n + 1) // 2, wl.cfg_id, rank=q) for q in range(P)]
+    scales = [synth.device_random_scales(nb, wl.cfg_id, rank=q, lo=1e-5, hi=2e-4)
+              for q in range(P)]
     p0 = synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER)
     states = []
     for _ in range(2):
