@@ -267,9 +267,9 @@ def _chunks(n, parts, align):
 
 def cpu_baseline(wl, frac, threads=1, steps=1):
     """Time the CPU oracle (as it stands) on a `frac` sample of the workload
-    for `steps` consecutive steps: Adam on frac*n (step t = 1, 2, ..., each
-    from the state the previous one left), refresh and quantization of
-    frac*n, gather of a frac*N layer from P' shards.  With threads > 1 each
+    for `steps` consecutive steps: Adam on frac*n (all n at frac = 1; step
+    t = 1, 2, ..., each from the state the previous one left), refresh and
+    quantization of frac*n, gather of a frac*N layer from P' shards.  With threads > 1 each
     op's elements are split into block-aligned ranges, and the same oracle
     calls run on the ranges from a pool of that many threads (the calls
     release the GIL).  Inputs come from the same seeded generators;
@@ -281,7 +281,9 @@ def cpu_baseline(wl, frac, threads=1, steps=1):
     from paper_2407_01614_amd.workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_gather,
                                                 bytes_quant, secondary_elems)
     B = wl.block
-    n = max(B, int(wl.n * frac) // B * B)
+    # the whole partition at full size (short last block included), else a
+    # whole number of blocks
+    n = wl.n if frac >= 1 else max(B, int(wl.n * frac) // B * B)
     N = max(B * wl.secondary_world, int(wl.layer_elems * frac))
     s = secondary_elems(N, wl.secondary_world, B)
     p = synth.master_weights(n, wl.cfg_id)

@@ -3,12 +3,13 @@
 The full Llama-2-13B rank partition (203,372,880 elements) and layer
 (317,204,480 elements over 8 shards), and the padded Falcon-7B layer, run
 through the same entry points with the same sizes as the benchmark, so the
-kernels and grids are the ones it times.  The quantization and the gather
-are compared with the oracle over the whole arrays (the oracle runs on
-block-aligned ranges from a pool of host threads); the optimizer step over a
-sample of elements it computes one by one, plus properties that hold at any
-size on everything.  Inputs are drawn on the device by the seeded
-generators and copied to the host before any kernel touches them.
+kernels and grids are the ones it times.  The optimizer step, the
+quantization and the gather are compared with the oracle over the whole
+arrays (the oracle runs on block-aligned ranges from a pool of host
+threads), every element of every array, plus properties that hold at any
+size; the fused kernel is compared on sampled quantization blocks.  Inputs
+are drawn on the device by the seeded generators and copied to the host
+before any kernel touches them.
 """
 import os
 from concurrent.futures import ThreadPoolExecutor

@@ -304,7 +304,7 @@ def test_iterations_with_buffer_reuse(zpp):
         assert (d == 0).mean() > 0.99, "iteration %d" % t
     got = (to_host(tp, np.float32), to_host(tm, np.float32), to_host(tv, np.float32),
            to_host(prim, np.uint16))
-    assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "after 3 iterations", steps=3,
+    assert_adam_close(got, (rp, rm, rv, rb), hp["lr"], "after 3 iterations",
                       m_tau=tau_m)
     same = assert_downstream(to_host(prim, np.uint16), rb, to_host(codes, np.int8),
                              to_host(scales, np.float32), rc, rs, B, "last iteration")
@@ -345,11 +345,28 @@ def test_pipeline_modes_agree(zpp):
     for key, res in results.items():
         for i, (a, b) in enumerate(zip(res, ref)):
             assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "%s output %d" % (key, i))
-    # the peers' part of the gathered layer against the oracle
+    # every output of the reference mode against the oracle: the Adam state
+    # after three steps (the same gradient each step), the secondary, the
+    # codes and scales (the oracle's quantization of the GPU's primary:
+    # identical inputs) and the whole gathered layer
+    hp = f32hp(wl.adam)
     s, B = wl.shard_elems, wl.block
-    expect = oracle.dequant_gather_layer([q[0] for q in peers], [q[1] for q in peers], s, B,
-                                         wl.layer_elems - s)
-    assert_bits_equal(ref[7].view(np.uint16)[s:], expect, "peer shards")
+    rp, rm, rv = p0, np.zeros(wl.n, np.float32), np.zeros(wl.n, np.float32)
+    mt = MomentTolerance()
+    for t in range(1, 4):
+        tau_m = mt.step((rp, rm, rv), g0, hp)
+        rp, rm, rv, rb = oracle.adam_step(rp, rm, rv, g0, step=t, **hp)
+    gp, gm, gv, gb, gsec, gc, gs, gout = ref
+    assert_adam_close((gp, gm, gv, gb.view(np.uint16)), (rp, rm, rv, rb), hp["lr"],
+                      "reference mode after 3 steps", m_tau=tau_m)
+    assert_bits_equal(gsec.view(np.uint16), gb.view(np.uint16), "secondary = primary")
+    rc, rs = oracle.quantize_blockwise_i8(gb.view(np.uint16), B)
+    assert_bits_equal(gc, rc, "codes")
+    assert_bits_equal(gs, rs, "scales")
+    expect = oracle.dequant_gather_layer([rc[:s]] + [q[0] for q in peers],
+                                         [rs[:s // B]] + [q[1] for q in peers], s, B,
+                                         wl.layer_elems)
+    assert_bits_equal(gout.view(np.uint16), expect, "gathered layer")
 
 
 @pytest.mark.parametrize("layers", [4, 5])
@@ -433,7 +450,7 @@ def test_pipeline_with_qgz_receive(zpp):
     r2 = oracle.adam_step(r1[0], r1[1], r1[2], g, step=2, **hp)
     got = (to_host(pipe.master, np.float32), to_host(pipe.exp_avg, np.float32),
            to_host(pipe.exp_avg_sq, np.float32), to_host(pipe.primary, np.uint16))
-    assert_adam_close(got, r2, hp["lr"], "after 2 steps", steps=2, m_tau=tau_m)
+    assert_adam_close(got, r2, hp["lr"], "after 2 steps", m_tau=tau_m)
 
 
 @pytest.mark.parametrize("streams", [1, 3])
