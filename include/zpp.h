@@ -119,7 +119,7 @@ ZPP_API zpp_status zpp_refresh_secondary(uint16_t *secondary_bf16, const uint16_
  *       correctly rounded), code = rint(x * inv) (ties to even) in
  *       [-127, 127]; when a < 2^-100, x and a are first multiplied by 2^64.
  * src_bf16: uint16_t[n].  codes: int8_t[n] out.  scales: float[ceil(n/block)]
- * out.  block: a power of two in [64, 4096], else ZPP_EINVAL.
+ * out.  block: a multiple of 64 in [64, 4096], else ZPP_EINVAL.
  * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
  * No two of the three ranges may overlap (ZPP_EOVERLAP).  Alignment: src 2,
  * scales 4 (ZPP_EALIGN); src 16 and codes 8 bytes select the vector kernel. */
@@ -138,7 +138,7 @@ ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n,
  * master, exp_avg, exp_avg_sq: float[n] in place; grad: float[n];
  * primary_bf16: uint16_t[n] out; secondary_bf16: uint16_t[n] out, or NULL to
  * keep no bf16 secondary copy; codes: int8_t[n] out; scales:
- * float[ceil(n/block)] out.  block: a power of two in [64, 4096].  hp as for
+ * float[ceil(n/block)] out.  block: a multiple of 64 in [64, 4096].  hp as for
  * zpp_adam_partition_step.
  * Order on `stream`: wait `wait_before`, run, record `done_after` (the event
  * a gather of the codes waits on).
@@ -170,7 +170,7 @@ ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg,
  *   read during the call only.  num_shards in [1, ZPP_MAX_SHARDS]; every
  *   pointer non-NULL.  out_bf16: uint16_t[layer_elems] out.
  * shard_elems >= 1, layer_elems <= num_shards * shard_elems (layer_elems 0
- *   is a no-op), block a power of two in [64, 4096] (ZPP_EINVAL otherwise).
+ *   is a no-op), block a multiple of 64 in [64, 4096] (ZPP_EINVAL otherwise).
  * Order on `stream`: wait for every event of wait_events[0..num_wait) on the
  * device (the paper's fix: no gather before the copies it reads are
  * complete), gather, record `done_after` (lets the next refresh of these
@@ -200,7 +200,7 @@ ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
  * Packing: two codes per byte, element 2i in the low nibble, 2i+1 in the high
  * nibble, 4-bit two's complement; an odd n leaves the last high nibble 0.
  * src: float[n].  codes: uint8_t[ceil(n/2)] out.  scales:
- * float[ceil(n/block)] out.  block: a power of two in [64, 4096].
+ * float[ceil(n/block)] out.  block: a multiple of 64 in [64, 4096].
  * Order on `stream`: wait `wait_before`, quantize, record `done_after`.
  * No two ranges may overlap (ZPP_EOVERLAP).  Alignment: src and scales 4
  * bytes (ZPP_EALIGN); 16-byte src and 2-byte codes select the vector kernel. */
@@ -243,8 +243,8 @@ ZPP_API zpp_status zpp_dequant_reduce_i4(const uint8_t *const *src_codes,
  * master, exp_avg, exp_avg_sq: float[n] in place.  src_codes, src_scales:
  * HOST arrays of num_src DEVICE pointers (uint8_t[ceil(n/2)], packed as
  * zpp_quantize_blockwise_i4 writes them, and float[ceil(n/block)] each),
- * read during the call only; num_src in [1, ZPP_MAX_SHARDS].  block: a power
- * of two in [64, 4096].  scale_out finite (1/num_src for the data-parallel
+ * read during the call only; num_src in [1, ZPP_MAX_SHARDS].  block: a
+ * multiple of 64 in [64, 4096].  scale_out finite (1/num_src for the data-parallel
  * mean).  primary_bf16: uint16_t[n] out.  hp as for zpp_adam_partition_step.
  * Order on `stream`: wait for every event of wait_events[0..num_wait) (the
  * exchange that delivered the sources), step, record `done_after`.
@@ -272,10 +272,10 @@ ZPP_API zpp_status zpp_qgz_receive_adam_step(float *master, float *exp_avg, floa
  * 33 B + num_src * (0.5 B + 4/grad_block B) + 4/block B.
  * master, exp_avg, exp_avg_sq: float[n] in place.  src_codes, src_scales,
  * num_src, scale_out: as for zpp_qgz_receive_adam_step, with int4 blocks of
- * grad_block (a power of two in [64, 4096]).  primary_bf16: uint16_t[n] out;
+ * grad_block (a multiple of 64 in [64, 4096]).  primary_bf16: uint16_t[n] out;
  * secondary_bf16: uint16_t[n] out, or NULL to keep no bf16 secondary copy;
  * codes: int8_t[n] out; scales: float[ceil(n/block)] out, int8 blocks of
- * block (a power of two in [64, 4096]).  hp as for zpp_adam_partition_step.
+ * block (a multiple of 64 in [64, 4096]).  hp as for zpp_adam_partition_step.
  * Order on `stream`: wait for every event of wait_events[0..num_wait),
  * run, record `done_after` (the event a gather of the codes waits on).
  * No two outputs may overlap, nor any output a source range (ZPP_EOVERLAP).

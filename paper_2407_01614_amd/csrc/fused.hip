@@ -15,7 +15,9 @@
 // the 4 elements [chunk + 256 w + 4 l, +4) for w < C / 256.  The bf16 of the
 // updated weights stays in registers (two per 4 elements) until the block's
 // absmax is known; a 256-block is exactly one wave, so its absmax is a
-// six-step cross-lane reduction.  Residency is capped at ZPP_FUSED_RESIDENCY
+// six-step cross-lane reduction.  A block that is not a power of two (any
+// multiple of 64 up to 4096) takes one wave per block (fused_any_kernel).
+// Residency is capped at ZPP_FUSED_RESIDENCY
 // workgroups per CU, as for the optimizer step: 1031-1046 us with 12 resident
 // at the Llama-2-13B partition (9-20 within 1%), 1127-1145 us uncapped.  With
 // the qgZ receive in place of the fp32 gradient (8 int4 sources) the cap is
@@ -139,6 +141,90 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a, GS gs) {
     }
 }
 
+// A block B = 64 b that is not a power of two: one wave per block; lane l
+// holds the 4 elements [k B + 256 w + 4 l, +4) for w < B / 256 (lanes past
+// the block's end hold nothing), so the absmax is a reduction over the whole
+// wave.  Otherwise as fused_kernel, with the same results as the three
+// separate kernels.
+template <bool ADAMW, class GS>
+__global__ __launch_bounds__(kWave) void fused_any_kernel(FusedArgs a, GS gs, uint32_t block) {
+    constexpr int kMaxW = 4096 / 256;  // float4 groups per lane of the largest block
+    const int lane = threadIdx.x;
+    const size_t nblocks = (a.n + block - 1) / block;
+    for (size_t k = blockIdx.x; k < nblocks; k += gridDim.x) {
+        const size_t base = k * block;
+        u32x2 pk[kMaxW];
+        u16x2 m2 = {0, 0};
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) {
+            const uint32_t off = (uint32_t)w * 256 + (uint32_t)lane * 4;
+            const size_t i = base + off;
+            pk[w] = u32x2{0u, 0u};
+            if (off < block && i + 4 <= a.n) {
+                f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
+                f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
+                f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
+                const f32x4 G = grad_load4(gs, i);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float p = P[e], m = M[e], v = V[e];
+                    adam_update<ADAMW>(p, m, v, G[e], a.c);
+                    P[e] = p;
+                    M[e] = m;
+                    V[e] = v;
+                }
+                st_nt(reinterpret_cast<f32x4 *>(a.p + i), P);
+                st_nt(reinterpret_cast<f32x4 *>(a.m + i), M);
+                st_nt(reinterpret_cast<f32x4 *>(a.v + i), V);
+                pk[w] = u32x2{pack_bf16x2(P.x, P.y), pack_bf16x2(P.z, P.w)};
+                st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk[w]);
+                if (a.secondary)
+                    st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk[w]);
+            } else if (off < block) {
+                // the partition's last elements: one by one
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    h[e] = 0u;
+                    if (i + e < a.n) {
+                        float p = a.p[i + e], m = a.m[i + e], v = a.v[i + e];
+                        adam_update<ADAMW>(p, m, v, grad_at(gs, i + e), a.c);
+                        a.p[i + e] = p;
+                        a.m[i + e] = m;
+                        a.v[i + e] = v;
+                        h[e] = bf16_rne_bits(p);
+                        a.primary[i + e] = (uint16_t)h[e];
+                        if (a.secondary)
+                            a.secondary[i + e] = (uint16_t)h[e];
+                    }
+                }
+                pk[w] = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+            }
+            m2 = __builtin_elementwise_max(
+                m2, __builtin_elementwise_max(absbits2(pk[w].x), absbits2(pk[w].y)));
+        }
+        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+        for (int off = kWave / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const BlockQuant q = block_params(mx);
+#pragma unroll
+        for (int w = 0; w < kMaxW; ++w) {
+            const uint32_t off = (uint32_t)w * 256 + (uint32_t)lane * 4;
+            const size_t i = base + off;
+            const uint32_t c4 = quant_word(pk[w].x, pk[w].y, q);
+            if (off < block && i + 4 <= a.n) {
+                st_nt(reinterpret_cast<uint32_t *>(a.codes + i), c4);
+            } else if (off < block) {
+                for (int e = 0; e < 4 && i + e < a.n; ++e)
+                    a.codes[i + e] = (int8_t)((c4 >> (8 * e)) & 0xFFu);
+            }
+        }
+        if (lane == 0)
+            a.scales[k] = q.scale;
+    }
+}
+
 // Workgroups per CU for each gradient source.
 template <class GS> constexpr int fused_residency();
 template <> constexpr int fused_residency<F32Grad>() { return ZPP_FUSED_RESIDENCY; }
@@ -170,7 +256,18 @@ hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
     case 1024: launch_fused_b<1024>(a, gs, stream); break;
     case 2048: launch_fused_b<2048>(a, gs, stream); break;
     case 4096: launch_fused_b<4096>(a, gs, stream); break;
-    default: return hipErrorInvalidValue;
+    default: {
+        const size_t nblocks = (a.n + block - 1) / block;
+        const unsigned grid =
+            (unsigned)(nblocks < ZPP_FUSED_MAX_GRID ? nblocks : ZPP_FUSED_MAX_GRID);
+        constexpr size_t lds = residency_lds(fused_residency<GS>());
+        if (a.c.adamw)
+            hipLaunchKernelGGL((fused_any_kernel<true, GS>), dim3(grid), dim3(kWave), lds, stream,
+                               a, gs, block);
+        else
+            hipLaunchKernelGGL((fused_any_kernel<false, GS>), dim3(grid), dim3(kWave), lds,
+                               stream, a, gs, block);
+    }
     }
     return hipGetLastError();
 }

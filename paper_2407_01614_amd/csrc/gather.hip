@@ -36,7 +36,7 @@ struct GatherArgs {
     uint16_t *out;
     size_t shard_elems;
     size_t layer_elems;
-    uint32_t block_shift;  // log2(block)
+    BlockDiv block;
 };
 
 __device__ __forceinline__ float code_f32(uint32_t w, int byte) {
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_vec_kernel(GatherArgs a
             for (int u = 0; u < U; ++u) {
                 const size_t i = base + (size_t)u * kRow;
                 c[u] = ld_nt(reinterpret_cast<const u32x2 *>(codes + i));
-                s[u] = scales[i >> a.block_shift];
+                s[u] = scales[block_of(a.block, i)];
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_vec_kernel(GatherArgs a
             for (int u = 0; u < U; ++u) {
                 const size_t i0 = base + (size_t)u * kRow;
                 for (size_t i = i0; i < i0 + 8 && i < valid; ++i) {
-                    const float x = (float)codes[i] * scales[i >> a.block_shift];
+                    const float x = (float)codes[i] * scales[block_of(a.block, i)];
                     out[i] = (uint16_t)bf16_rne_bits(x);
                 }
             }
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void gather_scalar_kernel(GatherArgs a) {
     const float *scales = a.shards.scales[j];
     const size_t stride = (size_t)gridDim.x * kThreads;
     for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < valid; i += stride) {
-        const float x = (float)codes[i] * scales[i >> a.block_shift];
+        const float x = (float)codes[i] * scales[block_of(a.block, i)];
         a.out[lo + i] = (uint16_t)bf16_rne_bits(x);
     }
 }
@@ -158,7 +158,7 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
     a.out = out;
     a.shard_elems = shard_elems;
     a.layer_elems = layer_elems;
-    a.block_shift = (uint32_t)__builtin_ctz(block);
+    a.block = make_block_div(block);
     const size_t per_shard = shard_elems < layer_elems ? shard_elems : layer_elems;
     if (vector_path) {
         constexpr size_t kTile = (size_t)kGatherThreads * 8 * ZPP_GATHER_UNROLL;

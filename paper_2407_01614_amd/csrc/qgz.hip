@@ -18,6 +18,9 @@
 // buffer (layout in zpp_i4grad.h): the gradient source of the receive
 // kernels forms each float4, so the bits are those of the separate arrays.
 //
+// Blocks may be any multiple of 64 up to 4096; the quantizer takes one wave
+// per block for those that are not powers of two.
+//
 // Both kernels keep every wave's loads and stores contiguous: on this GPU,
 // non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
 // lane at a 32- or 64-byte stride) run two to three times slower.
@@ -107,6 +110,12 @@ __device__ __forceinline__ size_t i4_out_byte(size_t i, uint32_t shift, uint32_t
     return (((i >> shift) * P + q) << (shift - 1)) + ((i & (((size_t)1 << shift) - 1)) >> 1);
 }
 
+// The same for element i of block k of any block size B.
+__device__ __forceinline__ size_t i4_out_byte_any(size_t i, size_t k, uint32_t B, uint32_t q,
+                                                  uint32_t P) {
+    return (k * P + q) * (B / 2) + ((i - k * B) >> 1);
+}
+
 template <int B, int U>
 __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
     const float *__restrict__ src, size_t n, uint8_t *__restrict__ codes,
@@ -170,12 +179,66 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
     }
 }
 
+// Vector path for a block B = 64 b that is not a power of two: one wave per
+// block; lane l holds the groups of 4 values [k B + 256 g + 4 l, +4) for
+// g < B / 256 (lanes past the block's end hold nothing), so the absmax is a
+// reduction over the whole wave; each group's 4 codes are one 16-bit store.
+__global__ __launch_bounds__(kQgzThreads) void quant_i4_any_kernel(
+    const float *__restrict__ src, size_t n, uint32_t block, uint8_t *__restrict__ codes,
+    float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
+    constexpr int kMaxG = 4096 / 256;  // groups per lane of the largest block
+    const size_t nblocks = (n + block - 1) / block;
+    const int lane = threadIdx.x & (kWave - 1);
+    const size_t wave0 = (size_t)blockIdx.x * (kQgzThreads / kWave) + threadIdx.x / kWave;
+    const size_t nwaves = (size_t)gridDim.x * (kQgzThreads / kWave);
+    for (size_t k = wave0; k < nblocks; k += nwaves) {
+        const size_t lo = k * block;
+        f32x4 x[kMaxG];
+        uint32_t mx = 0;
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g) {
+            const uint32_t off = (uint32_t)g * 256 + (uint32_t)lane * 4;
+            const size_t i = lo + off;
+            x[g] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (off < block && i + 4 <= n) {
+                x[g] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
+            } else if (off < block) {
+                float h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    h[e] = (i + e < n) ? src[i + e] : 0.0f;
+                x[g] = f32x4{h[0], h[1], h[2], h[3]};
+            }
+            mx = max(mx, abs_bits_max4(x[g]));
+        }
+#pragma unroll
+        for (int off = kWave / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const I4Quant q = i4_params(mx);
+#pragma unroll
+        for (int g = 0; g < kMaxG; ++g) {
+            const uint32_t off = (uint32_t)g * 256 + (uint32_t)lane * 4;
+            const size_t i = lo + off;
+            if (off < block && i < n) {
+                const uint32_t h = i4_half(x[g], q);
+                const size_t byte0 = i4_out_byte_any(i, k, block, q_src, num_src);
+                // the second byte holds elements i + 2 and i + 3
+                if (i + 2 < n)
+                    st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
+                else
+                    codes[byte0] = (uint8_t)h;
+            }
+        }
+        if (lane == 0)
+            scales[k * num_src + q_src] = q.scale;
+    }
+}
+
 // Any alignment: one wave per block, lanes stride through it; each code
 // byte is written by the lane that owns its even element.
 __global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(
     const float *__restrict__ src, size_t n, uint32_t block, uint8_t *__restrict__ codes,
     float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
-    const uint32_t shift = __builtin_ctz(block);
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
     const size_t wave0 = (size_t)blockIdx.x * (kQgzThreads / kWave) + threadIdx.x / kWave;
@@ -194,7 +257,7 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_scalar_kernel(
             const float x0 = src[i];
             const float x1 = (i + 1 < hi) ? src[i + 1] : 0.0f;
             const uint32_t h = i4_half(f32x4{x0, x1, 0.0f, 0.0f}, q);
-            codes[i4_out_byte(i, shift, q_src, num_src)] = (uint8_t)(h & 0xFFu);
+            codes[i4_out_byte_any(i, k, block, q_src, num_src)] = (uint8_t)(h & 0xFFu);
         }
         if (lane == 0)
             scales[k * num_src + q_src] = q.scale;
@@ -206,7 +269,7 @@ struct ReduceArgs {
     const float *scales[kMaxShards];
     uint32_t num_src;
     size_t n;
-    uint32_t block_shift;
+    BlockDiv block;
     float scale_out;
     float *out;
 };
@@ -255,7 +318,7 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_kernel(ReduceArgs a) {
                                 w[j][g] |= (uint32_t)a.codes[q][i / 2 + 1] << 8;
                         }
                         if (i < a.n)
-                            s[j][g] = a.scales[q][i >> a.block_shift];
+                            s[j][g] = a.scales[q][block_of(a.block, i)];
                     }
                 }
             }
@@ -295,7 +358,7 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_scalar_kernel(ReduceArg
         for (uint32_t q = 0; q < a.num_src; ++q) {
             const uint32_t byte = a.codes[q][i / 2];
             const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
-            acc = __builtin_fmaf(i4_code(nib, 0), a.scales[q][i >> a.block_shift], acc);
+            acc = __builtin_fmaf(i4_code(nib, 0), a.scales[q][block_of(a.block, i)], acc);
         }
         a.out[i] = acc * a.scale_out;
     }
@@ -372,7 +435,14 @@ hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uin
         case 1024: launch_quant_i4_b<1024>(src, n, codes, scales, source, num_src, stream); break;
         case 2048: launch_quant_i4_b<2048>(src, n, codes, scales, source, num_src, stream); break;
         case 4096: launch_quant_i4_b<4096>(src, n, codes, scales, source, num_src, stream); break;
-        default: return hipErrorInvalidValue;
+        default: {
+            const size_t nblocks = (n + block - 1) / block;
+            const size_t waves = kQgzThreads / kWave;
+            const size_t need = (nblocks + waves - 1) / waves;
+            const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
+            hipLaunchKernelGGL(quant_i4_any_kernel, dim3(grid), dim3(kQgzThreads), 0, stream, src,
+                               n, block, codes, scales, source, num_src);
+        }
         }
     } else {
         const size_t nblocks = (n + block - 1) / block;
@@ -400,7 +470,7 @@ hipError_t launch_dequant_reduce_i4(const uint8_t *const *src_codes,
     }
     a.num_src = num_src;
     a.n = n;
-    a.block_shift = (uint32_t)__builtin_ctz(block);
+    a.block = make_block_div(block);
     a.scale_out = scale_out;
     a.out = out;
     if (vector_path) {

@@ -9,7 +9,8 @@
 // NaN), reduced across the L lanes with cross-lane xor shuffles; no LDS
 // traffic and no float compares are needed.  Every lane then derives the
 // block's scale and inverse itself (two correctly rounded divisions per 8
-// elements) and writes its 8 codes as one 8-byte store.
+// elements) and writes its 8 codes as one 8-byte store.  Blocks that are
+// not powers of two (any multiple of 64 up to 4096) take one wave per block.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
@@ -103,8 +104,68 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
     }
 }
 
-// Any alignment, any power-of-two block: one wave per quant block, lanes
-// stride through it element by element.
+// Vector path for a block B = 64 b that is not a power of two: one wave per
+// block; lane l holds the 8 elements [k B + 8 (64 v + l), +8) for v < B / 512
+// (lanes past the block's end hold nothing), so the absmax is a reduction
+// over the whole wave.
+__global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
+    const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
+    float *__restrict__ scales) {
+    constexpr int kMaxV = 4096 / (8 * kWave);  // vectors per lane of the largest block
+    const size_t nblocks = (n + block - 1) / block;
+    const int lane = threadIdx.x & (kWave - 1);
+    const size_t wave0 = (size_t)blockIdx.x * (kQuantThreads / kWave) + threadIdx.x / kWave;
+    const size_t nwaves = (size_t)gridDim.x * (kQuantThreads / kWave);
+    for (size_t k = wave0; k < nblocks; k += nwaves) {
+        const size_t lo = k * block;
+        u32x4 x[kMaxV];
+        u16x2 m2 = {0, 0};
+#pragma unroll
+        for (int v = 0; v < kMaxV; ++v) {
+            const uint32_t off = (uint32_t)(v * kWave + lane) * 8;
+            const size_t i = lo + off;
+            x[v] = u32x4{0u, 0u, 0u, 0u};
+            if (off < block && i + 8 <= n) {
+                x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
+            } else if (off < block) {
+                uint32_t h[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    h[e] = (i + e < n) ? (uint32_t)src[i + e] : 0u;
+                x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                             h[6] | (h[7] << 16)};
+            }
+            m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
+                     __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
+                     __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
+        }
+        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+        for (int off = kWave / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const BlockQuant q = block_params(mx);
+#pragma unroll
+        for (int v = 0; v < kMaxV; ++v) {
+            const uint32_t off = (uint32_t)(v * kWave + lane) * 8;
+            const size_t i = lo + off;
+            u32x2 c;
+            c.x = quant_word(x[v].x, x[v].y, q);
+            c.y = quant_word(x[v].z, x[v].w, q);
+            if (off < block && i + 8 <= n) {
+                st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
+            } else if (off < block) {
+                for (int e = 0; e < 8 && i + e < n; ++e)
+                    codes[i + e] =
+                        (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
+            }
+        }
+        if (lane == 0)
+            scales[k] = q.scale;
+    }
+}
+
+// Any alignment, any block: one wave per quant block, lanes stride through it
+// element by element.
 __global__ __launch_bounds__(kThreads) void quant_scalar_kernel(
     const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
     float *__restrict__ scales) {
@@ -153,7 +214,15 @@ hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t
         case 1024: launch_vec<1024>(src, n, codes, scales, stream); break;
         case 2048: launch_vec<2048>(src, n, codes, scales, stream); break;
         case 4096: launch_vec<4096>(src, n, codes, scales, stream); break;
-        default: return hipErrorInvalidValue;
+        default: {
+            const size_t nblocks = (n + block - 1) / block;
+            constexpr size_t kWaves = kQuantThreads / kWave;
+            const size_t need = (nblocks + kWaves - 1) / kWaves;
+            const unsigned grid =
+                (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
+            hipLaunchKernelGGL(quant_any_kernel, dim3(grid), dim3(kQuantThreads), 0, stream, src,
+                               n, block, codes, scales);
+        }
         }
     } else {
         const size_t nblocks = (n + block - 1) / block;

@@ -147,7 +147,7 @@ I4Grad make_i4grad(const uint8_t *const *src_codes, const float *const *src_scal
         s.scales[q] = src_scales[q];
     }
     s.num_src = num_src;
-    s.block_shift = (uint32_t)__builtin_ctz(block);
+    s.block = make_block_div(block);
     s.scale_out = scale_out;
     return s;
 }
@@ -173,7 +173,7 @@ I4GradIl make_i4grad_il(const uint8_t *codes, const float *scales, uint32_t num_
     s.codes = codes;
     s.scales = scales;
     s.num_src = num_src;
-    s.block_shift = (uint32_t)__builtin_ctz(block);
+    s.block = make_block_div(block);
     s.scale_out = scale_out;
     return s;
 }

@@ -25,9 +25,8 @@ bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes) {
     return a0 < b0 + bbytes && b0 < a0 + abytes;
 }
 
-bool valid_block(uint32_t block) {
-    return block >= 64 && block <= 4096 && (block & (block - 1)) == 0;
-}
+// Any multiple of 64 from 64 to 4096.
+bool valid_block(uint32_t block) { return block >= 64 && block <= 4096 && block % 64 == 0; }
 
 // Largest element count whose byte ranges (up to 16 B per element) cannot
 // overflow a size_t.

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "zpp_launch.h"
+
 namespace zpp {
 
 #ifndef ZPP_THREADS
@@ -35,6 +37,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Block index of element i (BlockDiv, zpp_launch.h): the branch is uniform
+// across a launch.
+__device__ __forceinline__ size_t block_of(const BlockDiv &d, size_t i) {
+    return d.magic ? (size_t)__umul64hi((unsigned long long)(i >> 6), d.magic) : i >> d.shift;
+}
 
 // Residency cap.  The streaming kernels that keep many HBM streams open at
 // once (the optimizer step: four arrays read, four written) run faster with

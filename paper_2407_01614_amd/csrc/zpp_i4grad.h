@@ -15,9 +15,9 @@ namespace zpp {
 
 struct I4Grad {
     const uint8_t *codes[kMaxShards];  // packed int4, element 2i in the low nibble
-    const float *scales[kMaxShards];   // one per block of 2^block_shift elements
+    const float *scales[kMaxShards];   // one per block
     uint32_t num_src;
-    uint32_t block_shift;
+    BlockDiv block;
     float scale_out;
 };
 
@@ -35,7 +35,7 @@ __device__ __forceinline__ float i4grad_at(const I4Grad &s, size_t i) {
     for (uint32_t q = 0; q < s.num_src; ++q) {
         const uint32_t byte = s.codes[q][i / 2];
         const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
-        acc = __builtin_fmaf(i4_code(nib, 0), s.scales[q][i >> s.block_shift], acc);
+        acc = __builtin_fmaf(i4_code(nib, 0), s.scales[q][block_of(s.block, i)], acc);
     }
     return i4grad_scaled(acc, s.scale_out);
 }
@@ -47,6 +47,7 @@ __device__ __forceinline__ float i4grad_at(const I4Grad &s, size_t i) {
 __device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
     constexpr int kBatch = 8;
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const size_t k = block_of(s.block, i);
     for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
         uint32_t w[kBatch];
         float sc[kBatch];
@@ -57,7 +58,7 @@ __device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
             sc[j] = 0.0f;
             if (q < s.num_src) {
                 w[j] = ld_nt(reinterpret_cast<const uint16_t *>(s.codes[q] + i / 2));
-                sc[j] = s.scales[q][i >> s.block_shift];
+                sc[j] = s.scales[q][k];
             }
         }
 #pragma unroll
@@ -74,7 +75,7 @@ __device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
 }
 
 // The same P int4 copies interleaved in one receive buffer: for each block k
-// of B = 2^block_shift elements the sources' codes lie side by side (source
+// of B elements the sources' codes lie side by side (source
 // q's B/2 bytes at (k P + q) B/2) and so do their scales (source q's at
 // k P + q).  P = 1 is the plain layout of one copy.  A wave's 256-element
 // tile then reads all its codes within one run of P x 128 bytes (blocks of
@@ -85,22 +86,23 @@ struct I4GradIl {
     const uint8_t *codes;
     const float *scales;
     uint32_t num_src;
-    uint32_t block_shift;
+    BlockDiv block;
     float scale_out;
 };
 
-// Byte offset of element i's code of source q (element i is in the low nibble
-// when i is even).
-__device__ __forceinline__ size_t il_code_byte(const I4GradIl &s, size_t i, uint32_t q) {
-    const size_t mask = ((size_t)1 << s.block_shift) - 1;
-    return ((((i >> s.block_shift) * s.num_src + q)) << (s.block_shift - 1)) + ((i & mask) >> 1);
+// Byte offset of element i's code of source q, element i in block k (element
+// i is in the low nibble when i is even).
+__device__ __forceinline__ size_t il_code_byte(const I4GradIl &s, size_t i, size_t k,
+                                               uint32_t q) {
+    const size_t B = s.block.block;
+    return (k * s.num_src + q) * (B / 2) + ((i - k * B) >> 1);
 }
 
 __device__ __forceinline__ float i4grad_at(const I4GradIl &s, size_t i) {
     float acc = 0.0f;
-    const size_t k = i >> s.block_shift;
+    const size_t k = block_of(s.block, i);
     for (uint32_t q = 0; q < s.num_src; ++q) {
-        const uint32_t byte = s.codes[il_code_byte(s, i, q)];
+        const uint32_t byte = s.codes[il_code_byte(s, i, k, q)];
         const uint32_t nib = (i % 2 == 0) ? (byte & 0xFu) : (byte >> 4);
         acc = __builtin_fmaf(i4_code(nib, 0), s.scales[k * s.num_src + q], acc);
     }
@@ -116,9 +118,9 @@ __device__ __forceinline__ float i4grad_at(const I4GradIl &s, size_t i) {
 __device__ __forceinline__ f32x4 i4grad_load4(const I4GradIl &s, size_t i) {
     constexpr int kBatch = 8;
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    const size_t k = i >> s.block_shift;
-    const uint8_t *base = s.codes + il_code_byte(s, i, 0);
-    const size_t stride = (size_t)1 << (s.block_shift - 1);
+    const size_t k = block_of(s.block, i);
+    const uint8_t *base = s.codes + il_code_byte(s, i, k, 0);
+    const size_t stride = s.block.block / 2;
     const float *sbase = s.scales + k * s.num_src;
     for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
         uint32_t w[kBatch];

@@ -8,6 +8,34 @@
 
 namespace zpp {
 
+// Index of the block of `block` elements that holds element i, for any block
+// B = 64 b with b = 1 .. 64: a shift when B is a power of two, otherwise
+// floor((i >> 6) / b) as the high half of the 64 x 64-bit product of i >> 6
+// and magic = ceil(2^64 / b).  That quotient is exact for every i < 2^64:
+// with x = i >> 6 = q b + r (x < 2^58, r < b) the product is
+// 2^64 (q + r / b) + x e / b with e = magic b - 2^64 < b <= 64, and
+// x e < 2^64 keeps r / b + x e / (b 2^64) below 1.
+struct BlockDiv {
+    uint64_t magic;  // 0 when the block is a power of two
+    uint32_t shift;  // log2(block) when it is
+    uint32_t block;
+};
+
+inline BlockDiv make_block_div(uint32_t block) {
+    BlockDiv d;
+    d.block = block;
+    if ((block & (block - 1)) == 0) {
+        d.magic = 0;
+        d.shift = (uint32_t)__builtin_ctz(block);
+    } else {
+        // block / 64 is not a power of two, so 2^64 / b is not an integer
+        // and its ceiling is floor((2^64 - 1) / b) + 1
+        d.magic = UINT64_MAX / (block / 64) + 1;
+        d.shift = 0;
+    }
+    return d;
+}
+
 struct AdamConsts {
     float lr_wd;      // lr * weight_decay (decoupled decay)
     float wd;         // weight_decay (L2 form)

@@ -178,7 +178,7 @@ def test_refresh_validation(zpp):
 
 def test_quant_validation(zpp):
     q = zpp.raw.zpp_quantize_blockwise_i8
-    for blk in (0, 32, 100, 192, 8192):
+    for blk in (0, 32, 100, 200, 4160, 8192):  # not a multiple of 64 in [64, 4096]
         assert q(A, 1024, blk, B, C, None, None, None) == zpp.ZPP_EINVAL, blk
     assert q(None, 0, 256, None, None, None, None, None) == zpp.ZPP_OK
     assert q(None, 0, 3, None, None, None, None, None) == zpp.ZPP_EINVAL

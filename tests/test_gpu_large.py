@@ -65,8 +65,9 @@ def test_adam_past_4g(zpp):
     torch.cuda.empty_cache()
 
 
-def test_quantize_past_4g(zpp):
-    n, B = BIG, 256
+@pytest.mark.parametrize("B", [256, 320])
+def test_quantize_past_4g(zpp, B):
+    n = BIG
     nb = (n + B - 1) // B
     x = synth.device_bf16_weights(n, 102)
     codes = torch.empty(n, dtype=torch.int8, device="cuda")
@@ -89,10 +90,13 @@ def test_quantize_past_4g(zpp):
     torch.cuda.empty_cache()
 
 
-def test_gather_past_4g(zpp):
-    """A layer of more than 2^32 elements from 2 shards of 2^31 + 2^20."""
-    B, P2 = 256, 2
-    s = (1 << 31) + (1 << 20)
+@pytest.mark.parametrize("B,P2,s", [(256, 2, (1 << 31) + (1 << 20)),
+                                    (192, 1, ((1 << 32) + 4099 + 191) // 192 * 192)],
+                         ids=["2-shards", "one-shard-block-192"])
+def test_gather_past_4g(zpp, B, P2, s):
+    """A layer of more than 2^32 elements from 2 shards of 2^31 + 2^20, or
+    from one shard past 2^32 in blocks that are not a power of two (block
+    indices past 2^32 / 192 through the quotient of the block size)."""
     N = P2 * s - 777
     codes = [synth.device_random_codes(s, 103, rank=j) for j in range(P2)]
     scales = [synth.device_random_scales(s // B, 103, rank=j) for j in range(P2)]
@@ -101,16 +105,19 @@ def test_gather_past_4g(zpp):
     torch.cuda.synchronize()
     g = np.random.default_rng(4)
     per = s // B
-    kb = np.unique(np.concatenate([g.integers(0, 2 * per - 1, size=1024), [per - 1, per]]))
+    kb = np.unique(np.concatenate([g.integers(0, P2 * per - 1, size=1024),
+                                   [per - 1, min(per, P2 * per - 2)],
+                                   [(1 << 32) // B - 1, (1 << 32) // B]]))
+    kb = kb[kb < P2 * per - 8]
     hc = np.concatenate([codes[k // per][(k % per) * B:(k % per + 1) * B].cpu().numpy() for k in kb])
     hs = np.array([scales[k // per][k % per].item() for k in kb], np.float32)
     ref = oracle.dequant_blockwise_i8(hc, hs, B)
     eidx = torch.from_numpy((kb[:, None] * B + np.arange(B)[None, :]).ravel()).cuda()
     assert_bits_equal(out.index_select(0, eidx).cpu().numpy().view(np.uint16), ref, "sampled")
-    # the end of the layer: the last 4 blocks of shard 1 reach past N
-    start = 2 * s - 4 * B
-    tail_ref = oracle.dequant_gather_layer([codes[1][-(4 * B):].cpu().numpy()],
-                                           [scales[1][-4:].cpu().numpy()], 4 * B, B, N - start)
+    # the end of the layer: the last 8 blocks of the last shard reach past N
+    start = P2 * s - 8 * B
+    tail_ref = oracle.dequant_gather_layer([codes[-1][-(8 * B):].cpu().numpy()],
+                                           [scales[-1][-8:].cpu().numpy()], 8 * B, B, N - start)
     assert_bits_equal(out[start:].cpu().numpy().view(np.uint16), tail_ref, "tail")
     del codes, scales, out
     torch.cuda.empty_cache()

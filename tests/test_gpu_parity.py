@@ -229,7 +229,7 @@ def test_quant_tiny_secondary_shards(zpp):
                            "shard %d" % j)
 
 
-@pytest.mark.parametrize("block", [64, 128, 256, 512, 1024, 2048, 4096])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 960, 1024, 2048, 4032, 4096])
 @pytest.mark.parametrize("n", [1, 7, 8, 63, 255, 256, 257, 256 * 5 + 80, 100000, 1 << 17])
 def test_quant_blocks_and_ragged(zpp, block, n):
     x = synth.bf16_weights(n, 52, n + block)
@@ -268,7 +268,7 @@ def special_blocks(block):
     return bits
 
 
-@pytest.mark.parametrize("block", [64, 256, 4096])
+@pytest.mark.parametrize("block", [64, 192, 256, 4032, 4096])
 @pytest.mark.parametrize("pad", [0, 1], ids=["vector", "scalar"])
 def test_quant_special_blocks(zpp, block, pad):
     x = special_blocks(block)
@@ -317,6 +317,9 @@ def test_gather_tiny_layer(zpp):
     (64, 64 * 1024 - 1, 128),    # the largest secondary group
     (5, 5 * 2048 - 2048, 512),   # last shard entirely padding
     (2, 2 * 4096, 4096),
+    (8, 8 * 8192 - 1152, 192),   # blocks that are not powers of two
+    (3, 3 * 5000 - 77, 320),
+    (2, 2 * 4032 - 4031, 4032),
 ])
 @pytest.mark.parametrize("pad_out", [0, 1], ids=["vector", "scalar"])
 def test_gather_shapes(zpp, P2, N, block, pad_out):
@@ -427,7 +430,7 @@ def assert_fused_matches_oracle(got, p, m, v, g, hp, step, block, what):
     assert_bits_equal(gsc[same], rs[same], what + " scales")
 
 
-@pytest.mark.parametrize("block", [64, 128, 256, 512, 4096])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 4032, 4096])
 @pytest.mark.parametrize("n", [1, 255, 256, 4099, 256 * 40 + 80, 65536 + 64 + 3])
 def test_fused_vs_oracle(zpp, block, n):
     hp = f32hp(HP_TINY)
@@ -440,11 +443,12 @@ def test_fused_vs_oracle(zpp, block, n):
 
 @pytest.mark.parametrize("secondary", [True, False], ids=["with-secondary", "no-secondary"])
 @pytest.mark.parametrize("pad", [0, 1], ids=["fused", "scalar"])
-def test_fused_equals_separate_calls(zpp, secondary, pad):
+@pytest.mark.parametrize("block", [256, 320])
+def test_fused_equals_separate_calls(zpp, secondary, pad, block):
     """The fused entry gives, bit for bit, what the three separate calls give
     on the same inputs (both on the GPU), on both of its paths."""
     hp = f32hp(HP_LOUD)
-    n, block = 256 * 300 + 17, 256
+    n = 256 * 300 + 17
     p = synth.master_weights(n, 71)
     g = synth.gradients(n, 71)
     m, v = synth.moments(n, 71)

@@ -46,7 +46,7 @@ def grads(n, cfg, rank=0, scale=1.0):
     return synth.gradients(n, cfg, rank) * np.float32(scale)
 
 
-@pytest.mark.parametrize("block", [64, 128, 256, 512, 2048, 4096])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 2048, 4032, 4096])
 @pytest.mark.parametrize("n", [1, 2, 7, 8, 9, 255, 256, 257, 256 * 9 + 81, 100001, 1 << 18])
 def test_quant_i4_vs_oracle(zpp, block, n):
     x = grads(n, 80, n + block)
@@ -83,7 +83,7 @@ def i4_special(block):
     return np.concatenate(parts)
 
 
-@pytest.mark.parametrize("block", [64, 256, 1024])
+@pytest.mark.parametrize("block", [64, 192, 256, 1024])
 @pytest.mark.parametrize("pad", [0, 1], ids=["vector", "scalar"])
 def test_quant_i4_special_blocks(zpp, block, pad):
     x = i4_special(block)
@@ -117,6 +117,17 @@ def test_dequant_reduce_i4_vs_oracle(zpp, P, n):
         ref = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
                                        scale_out)
         assert_bits_equal(got, ref, "P=%d n=%d scale_out=%g" % (P, n, scale_out))
+
+
+@pytest.mark.parametrize("P,n,block", [(8, 192 * 37 + 5, 192), (3, 320 * 11 + 7, 320),
+                                       (5, 4032 * 3 + 33, 4032)])
+@pytest.mark.parametrize("pad_out", [0, 1], ids=["vector", "scalar"])
+def test_dequant_reduce_i4_blocks_not_powers_of_two(zpp, P, n, block, pad_out):
+    quants = oracle_sources(P, n, block, 85 + n)
+    got = run_reduce_i4(zpp, quants, n, block, float(np.float32(1.0 / P)), pad_out=pad_out)
+    ref = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], n, block,
+                                   float(np.float32(1.0 / P)))
+    assert_bits_equal(got, ref, "P=%d n=%d block=%d" % (P, n, block))
 
 
 @pytest.mark.parametrize("pads", [(1, 0), (0, 1)], ids=["out", "codes"])
@@ -260,7 +271,7 @@ REGIMES = {"workload": (HP, False, 1, True), "loud-adamw": (HP_LOUD, True, 3, Tr
 @pytest.mark.parametrize("P,n,block", [
     (1, 1, 256), (8, 7, 256), (8, 256, 256), (8, 256 * 9 + 81, 256), (3, 65536 + 8, 64),
     (8, 100001, 128), (5, 256 * 33, 1024), (8, 1 << 18, 4096), (64, 256 * 5 + 3, 256),
-    (9, 256 * 40, 512)])
+    (9, 256 * 40, 512), (8, 192 * 37 + 5, 192), (3, 320 * 11 + 7, 320)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_adam_equals_reduce_then_step(zpp, P, n, block, regime):
     """Bit for bit the dequantize-and-reduce followed by the partition step
@@ -403,7 +414,8 @@ def run_receive_pass(zpp, quants, n, grad_block, block, scale_out, state, second
 @pytest.mark.parametrize("P,n,grad_block,block,secondary", [
     (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
     (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
-    (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False)])
+    (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
+    (8, 192 * 37 + 5, 192, 320, True), (3, 320 * 11 + 7, 320, 192, False)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_pass_equals_three_calls(zpp, P, n, grad_block, block, secondary, regime):
     """Bit for bit the receive step, then the refresh and the quantization of
@@ -537,7 +549,8 @@ def zeros_u8(n):
 
 @pytest.mark.parametrize("P,n,block", [(1, 7, 256), (3, 256 * 9 + 81, 64), (8, 100001, 256),
                                        (8, 65536 + 8, 1024), (64, 256 * 5 + 3, 128),
-                                       (5, 4096 * 3 + 500, 4096)])
+                                       (5, 4096 * 3 + 500, 4096), (8, 192 * 9 + 81, 192),
+                                       (3, 320 * 5 + 3, 320)])
 @pytest.mark.parametrize("pad", [0, 1], ids=["vector", "scalar"])
 def test_quantize_i4_interleaved_equals_plain(zpp, P, n, block, pad):
     """Each source quantized into its slots of one interleaved buffer: taken
@@ -569,7 +582,7 @@ def run_receive_il(zpp, quants, n, block, scale_out, state, step, hp, adamw, pad
 @pytest.mark.parametrize("P,n,block", [
     (1, 1, 256), (8, 7, 256), (8, 256 * 9 + 81, 256), (3, 65536 + 8, 64), (8, 100001, 128),
     (5, 256 * 33, 1024), (8, 1 << 18, 4096), (64, 256 * 5 + 3, 256), (9, 256 * 40, 512),
-    (16, 256 * 17 + 100, 64)])
+    (16, 256 * 17 + 100, 64), (8, 192 * 9 + 81, 192), (3, 320 * 11 + 7, 320)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_interleaved_equals_separate(zpp, P, n, block, regime):
     """The receive step from one interleaved buffer leaves the same bits as
@@ -636,7 +649,7 @@ def run_receive_pass_il(zpp, quants, n, grad_block, block, scale_out, state, sec
     (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
     (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
     (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
-    (16, 256 * 17 + 100, 128, 512, True)])
+    (16, 256 * 17 + 100, 128, 512, True), (8, 192 * 37 + 5, 192, 320, True)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_pass_interleaved_equals_separate(zpp, P, n, grad_block, block, secondary,
                                                   regime):
@@ -718,7 +731,8 @@ def run_reduce_il(zpp, quants, n, block, scale_out, pad_out=0, pad_codes=0):
 
 @pytest.mark.parametrize("P,n,block", [
     (1, 1, 256), (2, 7, 64), (8, 9, 256), (3, 256 * 5 + 3, 128), (8, 65536 + 8, 256),
-    (8, 100001, 1024), (64, 256 * 5 + 3, 256), (5, 4096 * 3 + 500, 4096), (16, 512 * 9, 64)])
+    (8, 100001, 1024), (64, 256 * 5 + 3, 256), (5, 4096 * 3 + 500, 4096), (16, 512 * 9, 64),
+    (8, 320 * 9 + 81, 320), (3, 192 * 5 + 3, 192)])
 def test_dequant_reduce_interleaved_vs_oracle(zpp, P, n, block):
     """The dequant-reduce from one interleaved receive buffer against the
     oracle's reduction of the same P copies (separate arrays), bit for bit."""

@@ -328,7 +328,7 @@ def check_quant_integer_blocks(orc):
     scale must be 2^e exactly and the codes must be the k, at every exponent
     bf16 can hold the block exactly (subnormal blocks included)."""
     rng = np.random.default_rng(5)
-    for block in (64, 256, 4096):
+    for block in (64, 192, 256, 320, 4096):
         exps = list(range(-133, 121, 7)) + [-126, -107, -100, -99, 0, 120]
         q = np.concatenate([int_block(rng, block) for _ in exps])
         x = np.concatenate([q[i * block:(i + 1) * block].astype(np.float64) * 2.0 ** e
@@ -447,7 +447,7 @@ def check_quant_block_boundaries(orc):
     """Block k scaled by 2^k: each block's scale is its own, so an off-by-one
     in the block index shows up as a wrong scale or code."""
     rng = np.random.default_rng(9)
-    for block in (64, 128, 256, 512):
+    for block in (64, 128, 192, 256, 320, 512, 4032):
         nb = 9
         q = np.concatenate([int_block(rng, block) for _ in range(nb)])
         q = q[:nb * block - 17]  # short last block (still contains its own extreme?)
