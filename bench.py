@@ -21,13 +21,14 @@ next step's Adam), the fused step + refresh + quantize kernel in place of the
 three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
 timing only), the qgZ gradient side, the step preceded by the qgZ receive
-(as its own kernel, fused into the partition step, and inside the single
-pass of step, refresh and quantization; all three also with the eight int4
-copies interleaved in one receive buffer), the forward AllGather(L, P) with
-qwZ as one GPU carries it (the layer from all P ranks' int8 primary slices),
-and, for context,
-PyTorch's fused AdamW on a partition of the same size.  The
-CPU baseline times the plain CPU oracle on a bounded sample of the same
+of eight int4 copies delivered into one interleaved receive buffer (as its
+own kernel, fused into the partition step, and inside the single pass of
+step, refresh and quantization), the forward AllGather(L, P) with qwZ as one
+GPU carries it (the P ranks' bf16 primary slices int8-quantized, then the
+layer gathered from them), the HBM ceilings of this GPU (read-only,
+write-only and copy streams, each kernel reported as a fraction of the copy)
+and, for context, PyTorch's fused AdamW on a partition of the same size.
+The CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload llama-2-13b]
@@ -85,7 +86,10 @@ def measured_traffic(path, workload, kernel, sources):
     return round(entry["bytes_per_launch"])
 
 
-def kernel_table(kb, times):
+def kernel_table(kb, times, copy_gbps=None):
+    """Per kernel: algorithmic bytes, launch durations, GB/s, the fraction of
+    the HBM peak and, given the copy ceiling measured in the same run, the
+    fraction of that."""
     out = {}
     for k in kb:
         ts = sorted(times[k])
@@ -94,65 +98,55 @@ def kernel_table(kb, times):
         out[k] = {"bytes": kb[k], "mean_us": round(mean * 1e3, 2),
                   "median_us": round(ts[len(ts) // 2] * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
                   "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+        if copy_gbps:
+            out[k]["frac_of_copy_ceiling"] = round(gbps / copy_gbps, 4)
     return out
 
 
-def qgz_measure(pipe, wl, reps, num_src=8):
-    """The qgZ gradient side at this workload's partition: one sending rank's
-    int4 quantization of n fp32 gradient values, and the mean of `num_src`
-    int4 copies back into fp32 (the gradient the partition step reads); each
-    timed with events on its stream over `reps` launches."""
+def forward_slices(wl, stream):
+    """The forward AllGather(L, P) with qwZ up to the exchange: a layer of
+    N bf16 weights ~ N(0, 0.02) split into the P ranks' primary slices of
+    s = ceil(N/P) rounded up to the block (the last zero-padded), each slice
+    quantized by zpp_quantize_blockwise_i8 as its rank does before the
+    exchange.  Returns s, the weights, the codes and the scales."""
     import torch
-    from paper_2407_01614_amd import zpp
-    from paper_2407_01614_amd.pipeline import GradientExchange
-    from paper_2407_01614_amd.workloads import bytes_quant_i4, bytes_reduce_i4
-    ex = GradientExchange(wl.n, num_src, wl.block)
-    stream = pipe.compute
-    for q in range(num_src):
-        ex.quantize(q, pipe.grad, stream=stream)
-    out = torch.empty(wl.n, dtype=torch.float32, device="cuda")
-    res = {}
-    for name, fn, nbytes in (
-            ("quant_i4", lambda: ex.quantize(0, pipe.grad, stream=stream),
-             bytes_quant_i4(wl.n, wl.block)),
-            ("dequant_reduce_i4", lambda: ex.reduce(out, stream=stream),
-             bytes_reduce_i4(wl.n, num_src, wl.block))):
-        fn()
-        evs = []
-        for _ in range(reps):
-            a, b = zpp.Event(timing=True), zpp.Event(timing=True)
-            a.record(stream)
-            fn()
-            b.record(stream)
-            evs.append((a, b))
-        torch.cuda.synchronize()
-        ts = sorted(a.elapsed_ms(b) for a, b in evs)
-        mean = sum(ts) / len(ts)
-        gbps = nbytes / (mean * 1e-3) / 1e9
-        res[name] = {"bytes": nbytes, "mean_us": round(mean * 1e3, 2),
-                     "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
-    res["sources"] = num_src
-    del ex, out
-    return res
+    from paper_2407_01614_amd import synth, zpp
+    from paper_2407_01614_amd.workloads import secondary_elems
+    P, N, B = wl.world, wl.layer_elems, wl.block
+    s = secondary_elems(N, P, B)
+    w = synth.device_bf16_weights(P * s, wl.cfg_id, rank=1000)
+    w[N:] = 0
+    codes = [torch.empty(s, dtype=torch.int8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(s // B, dtype=torch.float32, device="cuda") for _ in range(P)]
+    for j in range(P):
+        zpp.quantize_blockwise_i8(w[j * s:(j + 1) * s], codes[j], scales[j], block=B,
+                                  stream=stream)
+    return s, w, codes, scales
 
 
 def forward_gather_measure(wl, reps):
     """The forward AllGather(L, P) with qwZ, as far as one GPU carries it:
-    the layer assembled from all P ranks' int8-quantized primary slices (P =
-    the workload's data-parallel world, slices of ceil(N/P) rounded up to the
-    block), by the same dequant-gather kernel over P shards (64 at most per
+    the P ranks' primary slices of a layer, int8-quantized each by the
+    library (forward_slices, not timed), then the layer assembled from all P
+    slices by the same dequant-gather kernel over P shards (64 at most per
     call; a larger world takes several calls, each writing its part of the
     layer).  The exchange that brings the slices from the other nodes needs
-    more GPUs.  Timed with events over `reps` launches."""
+    more GPUs.  Timed with events over `reps` launches; the quantization of
+    one slice, what each rank does before the exchange, is timed too."""
     import torch
-    from paper_2407_01614_amd import synth, zpp
-    from paper_2407_01614_amd.workloads import bytes_gather, secondary_elems
+    from paper_2407_01614_amd import zpp
+    from paper_2407_01614_amd.workloads import bytes_gather, bytes_quant
     P, N, B = wl.world, wl.layer_elems, wl.block
-    s = secondary_elems(N, P, B)
-    codes = [synth.device_random_codes(s, wl.cfg_id, rank=1000 + j) for j in range(P)]
-    scales = [synth.device_random_scales(s // B, wl.cfg_id, rank=1000 + j) for j in range(P)]
-    out = torch.empty(N, dtype=torch.int16, device="cuda")
     stream = torch.cuda.Stream()
+    s, w, codes, scales = forward_slices(wl, stream)
+    qevs = []
+    for _ in range(reps):
+        a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+        a.record(stream)
+        zpp.quantize_blockwise_i8(w[:s], codes[0], scales[0], block=B, stream=stream)
+        b.record(stream)
+        qevs.append((a, b))
+    out = torch.empty(N, dtype=torch.int16, device="cuda")
     G = zpp.MAX_SHARDS
     groups = []
     for g0 in range(0, P, G):
@@ -185,12 +179,15 @@ def forward_gather_measure(wl, reps):
         evs.append((a, b))
     torch.cuda.synchronize()
     mean = sum(a.elapsed_ms(b) for a, b in evs) / len(evs)
+    qmean = sum(a.elapsed_ms(b) for a, b in qevs) / len(qevs)
     nbytes = bytes_gather(s, P, N, B)
     gbps = nbytes / (mean * 1e-3) / 1e9
-    del codes, scales, out
+    del w, codes, scales, out
     return {"ranks": P, "slice_elems": s, "layer_elems": N, "launches_per_gather": -(-P // G),
+            "codes": "each slice int8-quantized by the library from bf16 weights ~ N(0, 0.02)",
             "bytes": nbytes, "mean_us": round(mean * 1e3, 2), "GB/s": round(gbps, 1),
-            "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+            "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
+            "quantize_one_slice": {"bytes": bytes_quant(s, B), "mean_us": round(qmean * 1e3, 2)}}
 
 
 def torch_adamw_context(wl, reps):
@@ -231,18 +228,47 @@ def torch_adamw_context(wl, reps):
             "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
-def copy_reference(reps=20):
-    """Two plain copies of 1 GiB on this GPU, for scale: the runtime's
-    device-to-device memcpy, and this library's refresh kernel (a bf16 copy)."""
+CEILING_LIB = os.path.join(ROOT, "paper_2407_01614_amd", "libzpp_ceiling.so")
+
+
+def ceilings(reps=20):
+    """The HBM ceilings of this GPU, measured in this run on 1 GiB streams
+    (include/zpp_ceiling.h: 16-byte non-temporal accesses in the launch
+    shapes that stream fastest): read-only, write-only and copy; beside
+    them the runtime's device-to-device memcpy and this library's refresh
+    kernel (a bf16 copy) on the same 1 GiB.  GB/s counts bytes read plus
+    bytes written.  The kernels of the path all read and write, so the copy
+    is the ceiling they are compared with (frac_of_copy_ceiling)."""
     import torch
     from paper_2407_01614_amd import zpp
-    n = 1 << 29  # bf16 elements: 1 GiB
-    src = torch.ones(n, dtype=torch.int16, device="cuda")
+    if not os.path.exists(CEILING_LIB):
+        raise RuntimeError("%s is not built: run __graft_entry__.build()" % CEILING_LIB)
+    lib = ctypes.CDLL(CEILING_LIB)
+    for fn in ("zppc_read_stream", "zppc_write_stream", "zppc_copy_stream"):
+        getattr(lib, fn).restype = ctypes.c_int
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 2, dtype=torch.int16, device="cuda")
     dst = torch.empty_like(src)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(zpp.stream_handle(stream))
+    vp = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError("ceiling stream launch failed: hipError %d" % rc)
+
+    streams = (
+        ("read_only", nbytes, lambda: check(lib.zppc_read_stream(vp(src), ctypes.c_size_t(nbytes),
+                                                                 vp(sink), sh))),
+        ("write_only", nbytes, lambda: check(lib.zppc_write_stream(
+            vp(dst), ctypes.c_size_t(nbytes), ctypes.c_uint32(0x3F803F80), sh))),
+        ("copy", 2 * nbytes, lambda: check(lib.zppc_copy_stream(vp(dst), vp(src),
+                                                                ctypes.c_size_t(nbytes), sh))),
+        ("hipMemcpyAsync_d2d", 2 * nbytes, lambda: dst.copy_(src)),
+        ("refresh_kernel", 2 * nbytes, lambda: zpp.refresh_secondary(dst, src, stream=stream)))
     res = {}
-    for name, fn in (("hipMemcpyAsync_d2d", lambda: dst.copy_(src)),
-                     ("refresh_kernel", lambda: zpp.refresh_secondary(dst, src, stream=stream))):
+    for name, moved, fn in streams:
         fn()
         evs = []
         for _ in range(reps):
@@ -253,9 +279,11 @@ def copy_reference(reps=20):
             evs.append((a, b))
         torch.cuda.synchronize()
         mean = sum(a.elapsed_ms(b) for a, b in evs) / reps
-        res[name] = round(2.0 * 2 * n / (mean * 1e-3) / 1e9, 1)
-    del src, dst
-    res["unit"] = "GB/s (1 GiB read + 1 GiB written)"
+        gbps = moved / (mean * 1e-3) / 1e9
+        res[name] = {"GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    assert int(sink.item()) == 0
+    del src, dst, sink
+    res["bytes"] = "1 GiB read and/or 1 GiB written; GB/s = bytes read + bytes written"
     return res
 
 
@@ -409,9 +437,9 @@ def main():
         """W warm-up steps, then K timed steps exactly as the path runs them;
         the kernels named in `live` carry a timing-event pair (events without
         the system-scope fence, which cost the stream next to nothing) in
-        those K steps.  With `timing`, K more steps follow with a pair around
-        every kernel on that kernel's own stream (the pipeline then runs each
-        kernel alone), for the per-kernel table."""
+        those K steps.  With `timing`, K more steps follow with such a pair
+        around every kernel on that kernel's own stream (the pipeline then
+        runs each kernel alone), for the per-kernel table."""
         pipe.fused, pipe.sync, pipe.overlap, pipe.timing = fused, sync, overlap, None
         pipe.streams = streams
         for _ in range(args.warmup):
@@ -430,7 +458,7 @@ def main():
         pipe.timing = None
         times = None
         if timing:
-            pipe.enable_timing()
+            pipe.enable_timing(system_fence=False)
             for _ in range(args.steps):
                 pipe.step()
             pipe.wait()
@@ -449,36 +477,24 @@ def main():
     sync_ab = {}
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
-    qgz = qgz_measure(pipe, wl, args.steps)
-    copy_ref = copy_reference()
+    ceil = ceilings()
+    copy_gbps = ceil["copy"]["GB/s"]
     torch_ctx = torch_adamw_context(wl, args.steps)
-    # the whole iteration seen by the rank: qgZ receive (8 int4 sources ->
-    # mean gradient) feeding the step
+    # the whole iteration seen by the rank with qgZ: the int4 quantization of
+    # its own gradient (the send), the receive of 8 int4 copies of its
+    # partition's gradient delivered into one interleaved receive buffer
+    # (their mean) feeding the step, as its own kernel, fused into the
+    # partition step, and inside the single pass of step, refresh and
+    # quantization
     from paper_2407_01614_amd import synth as _synth
     from paper_2407_01614_amd.pipeline import GradientExchange
-    pipe.exchange = GradientExchange(wl.n, 8, wl.block)
-    for q in range(8):
-        g = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id, _synth.KIND_GRAD, rank=q)
-        pipe.exchange.quantize(q, g)
-        del g
-    torch.cuda.synchronize()
-    qgz_ms, qgz_times, qgz_kb, qgz_step_bytes = run(False, "event", True)
-    qgz_gbps = qgz_step_bytes / (qgz_ms * 1e-3) / 1e9
-    # the same, with the receive fused into the partition step, and into the
-    # single pass of step, refresh and quantization
-    pipe.fuse_receive = True
-    fr_ms, fr_times, fr_kb, fr_step_bytes = run(False, "event", True)
-    fr_gbps = fr_step_bytes / (fr_ms * 1e-3) / 1e9
-    ff_ms, ff_times, ff_kb, ff_step_bytes = run(True, "event", True)
-    ff_gbps = ff_step_bytes / (ff_ms * 1e-3) / 1e9
-    # both again with the 8 copies interleaved in one receive buffer
-    pipe.exchange = None
-    torch.cuda.empty_cache()
     pipe.exchange = GradientExchange(wl.n, 8, wl.block, interleaved=True)
-    for q in range(8):
+    for q in range(1, 8):
         g = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id, _synth.KIND_GRAD, rank=q)
         pipe.exchange.quantize(q, g)
         del g
+    pipe.send_grad = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id,
+                                              _synth.KIND_GRAD, rank=0)
     torch.cuda.synchronize()
     pipe.fuse_receive = False
     ilr_ms, ilr_times, ilr_kb, ilr_step_bytes = run(False, "event", True)
@@ -490,9 +506,14 @@ def main():
     ilf_gbps = ilf_step_bytes / (ilf_ms * 1e-3) / 1e9
     pipe.fuse_receive = False
     pipe.exchange = None
+    pipe.send_grad = None
+    qgz_kernels = kernel_table(ilr_kb, ilr_times, copy_gbps)
+    qgz = {"sources": 8, "from": "step_with_qgz_receive (timed inside its steps)",
+           "quant_i4": qgz_kernels["quant_i4"],
+           "dequant_reduce_i4_interleaved": qgz_kernels["reduce_i4"]}
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    kernels = kernel_table(kb, times)
-    fused_kernels = kernel_table(fused_kb, fused_times)
+    kernels = kernel_table(kb, times, copy_gbps)
+    fused_kernels = kernel_table(fused_kb, fused_times, copy_gbps)
     fused_gbps = fused_step_bytes / (fused_ms * 1e-3) / 1e9
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
     sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
@@ -543,35 +564,23 @@ def main():
             "ms_per_step": round(fused_ms, 4), "GB/s": round(fused_gbps, 1),
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
         "sync_ab_ms_per_step": sync_ab,
-        "copy_reference": copy_ref,
+        "ceilings": ceil,
         "torch_fused_adamw_context": dict(
             torch_ctx, speedup_of_partition_step=round(
                 torch_ctx["ms_per_step"] / (kernels["adam"]["mean_us"] * 1e-3), 3)),
         "qgz_gradient_side": qgz,
         "step_with_qgz_receive": {
-            "ms_per_step": round(qgz_ms, 4), "GB/s": round(qgz_gbps, 1),
-            "frac_of_peak": round(qgz_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(qgz_kb, qgz_times)},
-        "step_with_fused_qgz_receive": {
-            "ms_per_step": round(fr_ms, 4), "GB/s": round(fr_gbps, 1),
-            "frac_of_peak": round(fr_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(fr_kb, fr_times)},
-        "step_with_qgz_receive_single_pass": {
-            "ms_per_step": round(ff_ms, 4), "GB/s": round(ff_gbps, 1),
-            "frac_of_peak": round(ff_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(ff_kb, ff_times)},
-        "step_with_qgz_receive_interleaved": {
             "ms_per_step": round(ilr_ms, 4), "GB/s": round(ilr_gbps, 1),
             "frac_of_peak": round(ilr_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(ilr_kb, ilr_times)},
-        "step_with_fused_qgz_receive_interleaved": {
+            "kernels": kernel_table(ilr_kb, ilr_times, copy_gbps)},
+        "step_with_fused_qgz_receive": {
             "ms_per_step": round(il_ms, 4), "GB/s": round(il_gbps, 1),
             "frac_of_peak": round(il_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(il_kb, il_times)},
-        "step_with_qgz_receive_single_pass_interleaved": {
+            "kernels": kernel_table(il_kb, il_times, copy_gbps)},
+        "step_with_qgz_receive_single_pass": {
             "ms_per_step": round(ilf_ms, 4), "GB/s": round(ilf_gbps, 1),
             "frac_of_peak": round(ilf_gbps / HBM_PEAK_GBPS, 4),
-            "kernels": kernel_table(ilf_kb, ilf_times)},
+            "kernels": kernel_table(ilf_kb, ilf_times, copy_gbps)},
         "device": torch.cuda.get_device_properties(0).gcnArchName,
         "gpu": {"name": torch.cuda.get_device_name(0),
                 "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,

@@ -11,6 +11,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzpp.so")
+# the plain HBM streams that bench.py times beside the kernels (not the path)
+CEILING_LIB = os.path.join(PKG, "libzpp_ceiling.so")
+CEILING_SOURCES = ["ceiling.hip"]
 
 SOURCES = ["zpp_api.hip", "adam.hip", "refresh.hip", "quant.hip", "gather.hip", "fused.hip",
            "qgz.hip", "receive_adam.hip"]
@@ -41,11 +44,11 @@ def hipcc():
     return "hipcc"
 
 
-def build(out=LIB, defines=(), verbose=False):
-    """Compile every HIP source of the package into one shared library."""
+def build(out=LIB, defines=(), verbose=False, sources=SOURCES):
+    """Compile the HIP sources of the path into one shared library."""
     tmp = out + ".tmp%d" % os.getpid()
     cmd = [hipcc(), *HIPCC_FLAGS, *["-D" + d for d in defines], "-I", INCLUDE, "-I", CSRC,
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+           *[os.path.join(CSRC, s) for s in sources], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -61,5 +64,11 @@ def build(out=LIB, defines=(), verbose=False):
     return out
 
 
+def build_ceiling(verbose=False):
+    """Compile the measurement streams into libzpp_ceiling.so."""
+    return build(out=CEILING_LIB, verbose=verbose, sources=CEILING_SOURCES)
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_ceiling(verbose=True))

@@ -37,7 +37,8 @@ import torch
 from . import synth
 from . import zpp
 from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_fused_receive,
-                        bytes_gather, bytes_quant, bytes_receive_adam, bytes_reduce_i4)
+                        bytes_gather, bytes_quant, bytes_quant_i4, bytes_receive_adam,
+                        bytes_reduce_i4)
 
 
 SYNC_MODES = ("event", "host", "none")
@@ -58,7 +59,12 @@ class PartitionPipeline:
     written), and with `fused` too, inside the single pass of step, refresh
     and quantization (`zpp_qgz_receive_step_refresh_quantize`).
     `qgz_interleaved` keeps the int4 copies in one interleaved receive buffer
-    (`GradientExchange`), read by the `..._interleaved` entry points."""
+    (`GradientExchange`), read by the `..._interleaved` entry points.  With
+    an exchange, setting `send_grad` (an fp32 tensor of n: this rank's own
+    gradient of its partition, from the backward pass) opens every step with
+    its int4 quantization into source slot 0 of the exchange, the copy this
+    rank contributes to its own partition; the other slots stand for the
+    copies the exchange delivers from the other ranks."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
                  qgz_sources=0, streams=3, fuse_receive=False, qgz_interleaved=False):
@@ -108,6 +114,7 @@ class PartitionPipeline:
         self.ev_refresh = zpp.Event()
         self.ev_quant = zpp.Event()
         self.ev_gather = zpp.Event()
+        self.send_grad = None
         self.step_count = 0
         self.timing = None
         self._timing_fence = True
@@ -238,6 +245,7 @@ class PartitionPipeline:
                 zpp.stream_wait(self.compute, self.ev_gather)
             else:
                 zpp.stream_wait(self.compute, self.ev_refresh)
+        self._send(self.compute)
         if self._receive_apart():
             self._timed("reduce_i4", self.compute,
                         lambda: self.exchange.reduce(self.grad, stream=self.compute))
@@ -290,6 +298,7 @@ class PartitionPipeline:
             # work (the quantization, then the gather) into this stream
             zpp.stream_wait(cs, self.ev_quant)
             zpp.stream_wait(cs, self.ev_gather)
+        self._send(cs)
         if self._receive_apart():
             self._timed("reduce_i4", cs, lambda: self.exchange.reduce(self.grad, stream=cs))
         if self.fused:
@@ -301,6 +310,16 @@ class PartitionPipeline:
             self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
                 self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
         self._gathers(cs)
+
+    def _sends(self):
+        return self.exchange is not None and self.send_grad is not None
+
+    def _send(self, stream):
+        """The qgZ send of this rank's own gradient: its int4 quantization
+        into source slot 0, ahead of the receive on the same stream."""
+        if self._sends():
+            self._timed("quant_i4", stream, lambda: self.exchange.quantize(
+                0, self.send_grad, stream=stream))
 
     def _receive_fused(self):
         return self.exchange is not None and self.fuse_receive
@@ -373,6 +392,8 @@ class PartitionPipeline:
         wl = self.wl
         gather = float(bytes_gather(wl.shard_elems, wl.secondary_world, wl.layer_elems, wl.block))
         out = {}
+        if self._sends():
+            out["quant_i4"] = float(bytes_quant_i4(wl.n, self.exchange.block))
         if self._receive_apart():
             out["reduce_i4"] = float(bytes_reduce_i4(wl.n, self.exchange.num_src, wl.block))
         if self.fused and self._receive_fused():

@@ -454,3 +454,36 @@ def test_no_oracle_in_product_path():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle|liboracle|zpp_oracle|orc_",
                                      text, re.M), f
+
+
+CEILING_HEADER = os.path.join(ROOT, "include", "zpp_ceiling.h")
+CEILING_LIB = os.path.join(ROOT, "paper_2407_01614_amd", "libzpp_ceiling.so")
+
+
+def test_ceiling_library_exports_and_rejects():
+    """The measurement streams (libzpp_ceiling.so): every function its header
+    declares is exported, and bad sizes, alignments or overlaps are
+    rejected (hipErrorInvalidValue) before anything is enqueued."""
+    if not os.path.exists(CEILING_LIB):
+        from paper_2407_01614_amd import build
+        build.build_ceiling()
+    decl = set(re.findall(r"ZPPC_API\s+int\s+(zppc_\w+)\s*\(", open(CEILING_HEADER).read()))
+    assert decl == {"zppc_read_stream", "zppc_write_stream", "zppc_copy_stream"}
+    out = subprocess.run(["nm", "-D", "--defined-only", CEILING_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    assert {s for s in exported if "zpp" in s.lower()} == decl
+    lib = ctypes.CDLL(CEILING_LIB)
+    for fn in decl:
+        getattr(lib, fn).restype = ctypes.c_int
+    EINVAL = 1  # hipErrorInvalidValue
+    big = ctypes.c_size_t(1 << 30)
+    assert lib.zppc_read_stream(None, big, ctypes.c_void_p(A), None) == EINVAL
+    assert lib.zppc_read_stream(ctypes.c_void_p(A), big, None, None) == EINVAL
+    assert lib.zppc_read_stream(ctypes.c_void_p(A), ctypes.c_size_t(4000), ctypes.c_void_p(B),
+                                None) == EINVAL
+    assert lib.zppc_write_stream(ctypes.c_void_p(A + 8), big, ctypes.c_uint32(0), None) == EINVAL
+    assert lib.zppc_write_stream(ctypes.c_void_p(A), ctypes.c_size_t(0), ctypes.c_uint32(0),
+                                 None) == EINVAL
+    assert lib.zppc_copy_stream(ctypes.c_void_p(A), ctypes.c_void_p(A + 4096), big, None) == EINVAL
+    assert lib.zppc_copy_stream(ctypes.c_void_p(A), None, big, None) == EINVAL

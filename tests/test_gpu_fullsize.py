@@ -148,32 +148,46 @@ def test_fullsize_gather(zpp, wl):
 
 @pytest.mark.parametrize("name", ["llama-2-13b", "falcon-40b"])
 def test_fullsize_forward_gather(zpp, name):
-    """The forward AllGather(L, P) with qwZ as one GPU carries it, in the
-    calls the benchmark times: the layer from all P ranks' int8 slices (64
-    slices with a padded last one for Llama-2-13B; 128 for Falcon-40B, two
-    calls of 64 each writing its half), the whole layer against the oracle,
-    bit for bit."""
+    """The forward AllGather(L, P) with qwZ as one GPU carries it, end to end
+    in the calls the benchmark times: a layer of bf16 weights split into the
+    P ranks' primary slices (64 with a padded last one for Llama-2-13B; 128
+    for Falcon-40B, gathered in two calls of 64 each writing its half), each
+    slice int8-quantized by the library, then the layer gathered from all
+    slices.  Against the oracle's quantization of the same slices and its
+    gather of them, bit for bit: every code, every scale, the whole layer."""
     wl = WORKLOADS[name]
     N, P, B = wl.layer_elems, wl.world, wl.block
     s = oracle.secondary_shard_elems(N, P, B)
     assert s == secondary_elems(N, P, B)
-    codes = [synth.device_random_codes(s, wl.cfg_id, rank=1000 + j) for j in range(P)]
-    scales = [synth.device_random_scales(s // B, wl.cfg_id, rank=1000 + j) for j in range(P)]
+    w = synth.device_bf16_weights(P * s, wl.cfg_id, rank=1000)
+    w[N:] = 0  # the padding of the last slice
+    codes = [torch.empty(s, dtype=torch.int8, device="cuda") for _ in range(P)]
+    scales = [torch.empty(s // B, dtype=torch.float32, device="cuda") for _ in range(P)]
     out = torch.full((N,), 0x5A5A, dtype=torch.int16, device="cuda")
-    G = zpp.MAX_SHARDS
+    wh = w.cpu().numpy().view(np.uint16)
     torch.cuda.synchronize()
+    for j in range(P):
+        zpp.quantize_blockwise_i8(w[j * s:(j + 1) * s], codes[j], scales[j], block=B)
+    G = zpp.MAX_SHARDS
     for g0 in range(0, P, G):
         part = min(N - g0 * s, min(G, P - g0) * s)
+        if part <= 0:
+            continue  # a group of slices that holds only padding
         zpp.dequant_gather_layer(codes[g0:g0 + G], scales[g0:g0 + G], s, part, out[g0 * s:],
                                  block=B)
     torch.cuda.synchronize()
     hc = [c.cpu().numpy() for c in codes]
     hs = [x.cpu().numpy() for x in scales]
-    del codes, scales
+    del w, codes, scales
     with pool() as ex:
-        ref = list(ex.map(lambda j: oracle.dequant_gather_layer(
-            [hc[j]], [hs[j]], s, B, min(s, N - j * s)), range(P)))
-    assert_bits_equal(out.cpu().numpy().view(np.uint16), np.concatenate(ref), "whole layer")
+        ref = list(ex.map(lambda j: oracle.quantize_blockwise_i8(wh[j * s:(j + 1) * s], B),
+                          range(P)))
+        for j in range(P):
+            assert_bits_equal(hc[j], ref[j][0], "codes of slice %d" % j)
+            assert_bits_equal(hs[j], ref[j][1], "scales of slice %d" % j)
+        layer = list(ex.map(lambda j: oracle.dequant_gather_layer(
+            [ref[j][0]], [ref[j][1]], s, B, max(0, min(s, N - j * s))), range(P)))
+    assert_bits_equal(out.cpu().numpy().view(np.uint16), np.concatenate(layer), "whole layer")
     del out
     torch.cuda.empty_cache()
 

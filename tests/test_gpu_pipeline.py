@@ -454,6 +454,70 @@ def test_pipeline_with_qgz_receive(zpp):
 
 
 @pytest.mark.parametrize("streams", [1, 3])
+@pytest.mark.parametrize("fuse", [False, True], ids=["reduce", "fused-receive"])
+def test_pipeline_with_qgz_send(zpp, streams, fuse):
+    """Each step opens with the int4 quantization of this rank's own gradient
+    into source slot 0 of an interleaved receive buffer whose other 7 slots
+    hold the oracle's quantizations of the other ranks' gradients; the slot
+    equals the oracle's quantization, and two steps follow the oracle's Adam
+    on the oracle's mean of the 8 copies (the separate reduce's gradient
+    bit for bit)."""
+    from paper_2407_01614_amd.pipeline import PartitionPipeline
+    from paper_2407_01614_amd.workloads import Workload
+    wl = Workload(name="small-qgz-send", cfg_id=15, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
+                  secondary_world=4, world=4)
+    P, B = 8, wl.block
+    srcs = [synth.gradients(wl.n, wl.cfg_id, q) for q in range(P)]
+    quants = [oracle.quantize_blockwise_i4(x, B) for x in srcs]
+    pipe = PartitionPipeline(wl, qgz_sources=P, qgz_interleaved=True, streams=streams,
+                             fuse_receive=fuse)
+    peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
+                                          B) for j in range(wl.secondary_world - 1)]
+    p0 = synth.master_weights(wl.n, wl.cfg_id)
+    pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
+    for q in range(1, P):
+        pipe.exchange.quantize(q, to_dev(srcs[q]))
+    nb = -(-wl.n // B)
+    # slot 0 (poisoned here) is written by the send of every step
+    pipe.exchange.codes.view(nb, P, B // 2)[:, 0, :].fill_(0x77)
+    pipe.exchange.scales.view(nb, P)[:, 0].fill_(float("nan"))
+    pipe.send_grad = to_dev(srcs[0])
+    torch.cuda.synchronize()
+    assert "quant_i4" in pipe.kernel_bytes()
+    pipe.step()
+    pipe.step()
+    pipe.wait()
+    got = deinterleave(pipe.exchange.codes.cpu().numpy(), to_host(pipe.exchange.scales,
+                                                                  np.float32), wl.n, B, P)
+    for q in range(P):
+        assert_bits_equal(got[q][0], quants[q][0], "codes of source %d" % q)
+        assert_bits_equal(got[q][1], quants[q][1], "scales of source %d" % q)
+    mean = float(np.float32(1.0 / P))
+    g = oracle.dequant_reduce_i4([c for c, _ in quants], [s for _, s in quants], wl.n, B, mean)
+    if not fuse:
+        assert_bits_equal(to_host(pipe.grad, np.float32), g, "reduced gradient")
+    hp = f32hp(wl.adam)
+    z = np.zeros(wl.n, np.float32)
+    mt = MomentTolerance()
+    mt.step((p0, z, z), g, hp)
+    r1 = oracle.adam_step(p0, z, z, g, step=1, **hp)
+    tau_m = mt.step(r1[:3], g, hp)
+    r2 = oracle.adam_step(r1[0], r1[1], r1[2], g, step=2, **hp)
+    got = (to_host(pipe.master, np.float32), to_host(pipe.exp_avg, np.float32),
+           to_host(pipe.exp_avg_sq, np.float32), to_host(pipe.primary, np.uint16))
+    assert_adam_close(got, r2, hp["lr"], "after 2 steps", m_tau=tau_m)
+
+
+def deinterleave(codes, scales, n, block, P):
+    """The P sources' (codes, scales) out of an interleaved receive buffer."""
+    nb = -(-n // block)
+    half = block // 2
+    c = codes[:nb * P * half].reshape(nb, P, half)
+    s = scales[:nb * P].reshape(nb, P)
+    return [(c[:, q, :].ravel()[:(n + 1) // 2].copy(), s[:, q].copy()) for q in range(P)]
+
+
+@pytest.mark.parametrize("streams", [1, 3])
 def test_pipeline_fused_receive_equals_separate(zpp, streams):
     """The qgZ receive fused into the partition step (no gradient buffer
     written), alone or inside the single pass of step, refresh and
