@@ -20,7 +20,8 @@ streams ordered by events (with and without one step's gather overlapping the
 next step's Adam), the fused step + refresh + quantize kernel in place of the
 three separate ones, the time per step with the gather ordered by a device
 event wait (the fix), by a host-side wait, or not at all (stock hpZ, racy:
-timing only), the qgZ gradient side, the step preceded by the qgZ receive
+timing only), the step with the refresh and its quantization as one pass,
+the qgZ gradient side, the step preceded by the qgZ receive
 of eight int4 copies delivered into one interleaved receive buffer (as its
 own kernel, fused into the partition step, and inside the single pass of
 step, refresh and quantization), the forward AllGather(L, P) with qwZ as one
@@ -474,6 +475,10 @@ def main():
     ms_per_step, times, kb, step_bytes, live_times = run(False, "event", True, live={"adam"})
     three_ms = run(False, "event", False, overlap=True, streams=3)[0]
     fused_ms, fused_times, fused_kb, fused_step_bytes = run(True, "event", True)
+    # the refresh and its quantization as one pass (zpp_refresh_quantize_i8)
+    pipe.fuse_copy = True
+    fc_ms, fc_times, fc_kb, fc_step_bytes = run(False, "event", True)
+    pipe.fuse_copy = False
     sync_ab = {}
     for mode in ("event", "host", "none"):
         sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
@@ -563,6 +568,11 @@ def main():
         "fused_step_refresh_quant": {
             "ms_per_step": round(fused_ms, 4), "GB/s": round(fused_gbps, 1),
             "frac_of_peak": round(fused_gbps / HBM_PEAK_GBPS, 4), "kernels": fused_kernels},
+        "step_with_fused_refresh_quant": {
+            "ms_per_step": round(fc_ms, 4),
+            "GB/s": round(fc_step_bytes / (fc_ms * 1e-3) / 1e9, 1),
+            "frac_of_peak": round(fc_step_bytes / (fc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "kernels": kernel_table(fc_kb, fc_times, copy_gbps)},
         "sync_ab_ms_per_step": sync_ab,
         "ceilings": ceil,
         "torch_fused_adamw_context": dict(

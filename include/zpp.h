@@ -127,6 +127,26 @@ ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n,
                                              int8_t *codes, float *scales, hipStream_t stream,
                                              hipEvent_t wait_before, hipEvent_t done_after);
 
+/* The secondary refresh and its qwZ quantization in one pass: the same
+ * results, bit for bit, as zpp_refresh_secondary(secondary_bf16, src_bf16, n)
+ * followed by zpp_quantize_blockwise_i8(secondary_bf16, n, block, codes,
+ * scales) (Algorithm 1: the D2D copy of the local rank's weights into
+ * L_{i,second}; Background: qwZ quantizes them before the gather), reading
+ * src_bf16 once: 5.016 instead of 7.016 bytes of HBM traffic per element for
+ * block 256.  secondary_bf16: uint16_t[n] out; src_bf16: uint16_t[n];
+ * codes: int8_t[n] out; scales: float[ceil(n/block)] out; block: a multiple
+ * of 64 in [64, 4096], else ZPP_EINVAL.  Order on `stream`: wait
+ * `wait_before` (e.g. the last gather that read the codes), copy and
+ * quantize, record `done_after`, which the gather of these codes must wait
+ * on (the paper's fix).  No two of the four ranges may overlap
+ * (ZPP_EOVERLAP).  Alignment: secondary and src 2 bytes, scales 4
+ * (ZPP_EALIGN); src and secondary 16 and codes 8 bytes select the vector
+ * kernel. */
+ZPP_API zpp_status zpp_refresh_quantize_i8(uint16_t *secondary_bf16, const uint16_t *src_bf16,
+                                           size_t n, uint32_t block, int8_t *codes, float *scales,
+                                           hipStream_t stream, hipEvent_t wait_before,
+                                           hipEvent_t done_after);
+
 /* Fused partition step: zpp_adam_partition_step, then the secondary refresh
  * and the qwZ quantization of the new bf16 weights, in one pass over HBM
  * (optimizer.step() of Algorithm 1, the secondary copy of the forward loop

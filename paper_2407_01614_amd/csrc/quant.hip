@@ -11,6 +11,11 @@
 // block's scale and inverse itself (two correctly rounded divisions per 8
 // elements) and writes its 8 codes as one 8-byte store.  Blocks that are
 // not powers of two (any multiple of 64 up to 4096) take one wave per block.
+//
+// The same kernels can also store the bf16 they read to a second array:
+// the secondary refresh and its quantization in one pass (2 B read, 2 B +
+// 1 B + 4/B B written per element, against 4 + 3 + 4/B B for the two
+// calls).
 #include "zpp_device.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
@@ -30,10 +35,12 @@ namespace {
 
 constexpr int kQuantThreads = ZPP_QUANT_THREADS;
 
+// `copy` (may be null): the loaded bf16 are also stored there, bit for bit
+// (the secondary refresh taken into the quantization's pass).
 template <int B, int U>
 __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
     const uint16_t *__restrict__ src, size_t n, int8_t *__restrict__ codes,
-    float *__restrict__ scales) {
+    float *__restrict__ scales, uint16_t *__restrict__ copy) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;  // lanes per quant block
     constexpr int V = (B / 8 > kWave) ? B / (8 * kWave) : 1;
     constexpr int kGroupsPerWave = kWave / L;
@@ -92,10 +99,15 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
                 c.y = quant_word(x[u][v].z, x[u][v].w, q);
                 if (valid && i + 8 <= n) {
                     st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
+                    if (copy)
+                        st_nt(reinterpret_cast<u32x4 *>(copy + i), x[u][v]);
                 } else if (valid) {
-                    for (int e = 0; e < 8 && i + e < n; ++e)
+                    for (int e = 0; e < 8 && i + e < n; ++e) {
                         codes[i + e] =
                             (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
+                        if (copy)
+                            copy[i + e] = src[i + e];
+                    }
                 }
             }
             if (valid && li == 0)
@@ -110,7 +122,7 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
 // over the whole wave.
 __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
     const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
-    float *__restrict__ scales) {
+    float *__restrict__ scales, uint16_t *__restrict__ copy) {
     constexpr int kMaxV = 4096 / (8 * kWave);  // vectors per lane of the largest block
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
@@ -153,10 +165,15 @@ __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
             c.y = quant_word(x[v].z, x[v].w, q);
             if (off < block && i + 8 <= n) {
                 st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
+                if (copy)
+                    st_nt(reinterpret_cast<u32x4 *>(copy + i), x[v]);
             } else if (off < block) {
-                for (int e = 0; e < 8 && i + e < n; ++e)
+                for (int e = 0; e < 8 && i + e < n; ++e) {
                     codes[i + e] =
                         (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
+                    if (copy)
+                        copy[i + e] = src[i + e];
+                }
             }
         }
         if (lane == 0)
@@ -168,7 +185,7 @@ __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
 // element by element.
 __global__ __launch_bounds__(kThreads) void quant_scalar_kernel(
     const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
-    float *__restrict__ scales) {
+    float *__restrict__ scales, uint16_t *__restrict__ copy) {
     const size_t nblocks = (n + block - 1) / block;
     const int lane = threadIdx.x & (kWave - 1);
     const size_t wave0 = (size_t)blockIdx.x * (kThreads / kWave) + threadIdx.x / kWave;
@@ -182,15 +199,19 @@ __global__ __launch_bounds__(kThreads) void quant_scalar_kernel(
         for (int off = kWave / 2; off >= 1; off >>= 1)
             mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
         const BlockQuant q = block_params(mx);
-        for (size_t i = lo + lane; i < hi; i += kWave)
-            codes[i] = (int8_t)quant_one(bf16_lo((uint32_t)src[i]), q);
+        for (size_t i = lo + lane; i < hi; i += kWave) {
+            const uint16_t h = src[i];
+            codes[i] = (int8_t)quant_one(bf16_lo((uint32_t)h), q);
+            if (copy)
+                copy[i] = h;
+        }
         if (lane == 0)
             scales[k] = q.scale;
     }
 }
 
 template <int B>
-void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales,
+void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales, uint16_t *copy,
                 hipStream_t stream) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;
     constexpr size_t kGroupsPerBlock = (kWave / L) * (kQuantThreads / kWave) * ZPP_QUANT_UNROLL;
@@ -198,22 +219,23 @@ void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales,
     const size_t need = (nblocks + kGroupsPerBlock - 1) / kGroupsPerBlock;
     const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
     hipLaunchKernelGGL((quant_vec_kernel<B, ZPP_QUANT_UNROLL>), dim3(grid), dim3(kQuantThreads), 0,
-                       stream, src, n, codes, scales);
+                       stream, src, n, codes, scales, copy);
 }
 
 }  // namespace
 
-hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
-                           float *scales, bool vector_path, hipStream_t stream) {
+hipError_t launch_quantize_copy(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
+                                float *scales, uint16_t *copy, bool vector_path,
+                                hipStream_t stream) {
     if (vector_path) {
         switch (block) {
-        case 64: launch_vec<64>(src, n, codes, scales, stream); break;
-        case 128: launch_vec<128>(src, n, codes, scales, stream); break;
-        case 256: launch_vec<256>(src, n, codes, scales, stream); break;
-        case 512: launch_vec<512>(src, n, codes, scales, stream); break;
-        case 1024: launch_vec<1024>(src, n, codes, scales, stream); break;
-        case 2048: launch_vec<2048>(src, n, codes, scales, stream); break;
-        case 4096: launch_vec<4096>(src, n, codes, scales, stream); break;
+        case 64: launch_vec<64>(src, n, codes, scales, copy, stream); break;
+        case 128: launch_vec<128>(src, n, codes, scales, copy, stream); break;
+        case 256: launch_vec<256>(src, n, codes, scales, copy, stream); break;
+        case 512: launch_vec<512>(src, n, codes, scales, copy, stream); break;
+        case 1024: launch_vec<1024>(src, n, codes, scales, copy, stream); break;
+        case 2048: launch_vec<2048>(src, n, codes, scales, copy, stream); break;
+        case 4096: launch_vec<4096>(src, n, codes, scales, copy, stream); break;
         default: {
             const size_t nblocks = (n + block - 1) / block;
             constexpr size_t kWaves = kQuantThreads / kWave;
@@ -221,7 +243,7 @@ hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t
             const unsigned grid =
                 (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
             hipLaunchKernelGGL(quant_any_kernel, dim3(grid), dim3(kQuantThreads), 0, stream, src,
-                               n, block, codes, scales);
+                               n, block, codes, scales, copy);
         }
         }
     } else {
@@ -229,9 +251,14 @@ hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t
         const size_t need = (nblocks + (kThreads / kWave) - 1) / (kThreads / kWave);
         const unsigned grid = (unsigned)(need < (1u << 20) ? need : (1u << 20));
         hipLaunchKernelGGL(quant_scalar_kernel, dim3(grid), dim3(kThreads), 0, stream, src, n,
-                           block, codes, scales);
+                           block, codes, scales, copy);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
+                           float *scales, bool vector_path, hipStream_t stream) {
+    return launch_quantize_copy(src, n, block, codes, scales, nullptr, vector_path, stream);
 }
 
 }  // namespace zpp

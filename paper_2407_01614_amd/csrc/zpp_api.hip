@@ -218,6 +218,37 @@ ZPP_API zpp_status zpp_quantize_blockwise_i8(const uint16_t *src_bf16, size_t n,
     return record(stream, done_after);
 }
 
+ZPP_API zpp_status zpp_refresh_quantize_i8(uint16_t *secondary_bf16, const uint16_t *src_bf16,
+                                           size_t n, uint32_t block, int8_t *codes, float *scales,
+                                           hipStream_t stream, hipEvent_t wait_before,
+                                           hipEvent_t done_after) {
+    if (!valid_block(block) || n > kMaxElems)
+        return ZPP_EINVAL;
+    const size_t nblocks = (n + block - 1) / block;
+    if (n) {
+        if (!secondary_bf16 || !src_bf16 || !codes || !scales)
+            return ZPP_EINVAL;
+        if (!aligned(secondary_bf16, 2) || !aligned(src_bf16, 2) || !aligned(scales, 4))
+            return ZPP_EALIGN;
+        const void *ptrs[4] = {secondary_bf16, src_bf16, codes, scales};
+        const size_t bytes[4] = {2 * n, 2 * n, n, 4 * nblocks};
+        if (any_overlap(ptrs, bytes, 4))
+            return ZPP_EOVERLAP;
+    }
+    zpp_status st = wait_on(stream, wait_before);
+    if (st != ZPP_OK)
+        return st;
+    if (n) {
+        const bool vec = aligned(src_bf16, 16) && aligned(secondary_bf16, 16) && aligned(codes, 8);
+        const hipError_t e =
+            zpp::launch_quantize_copy(src_bf16, n, block, codes, scales, secondary_bf16, vec,
+                                      stream);
+        if (e != hipSuccess)
+            return hip_fail(e);
+    }
+    return record(stream, done_after);
+}
+
 ZPP_API zpp_status zpp_dequant_gather_layer(const int8_t *const *shard_codes,
                                             const float *const *shard_scales, uint32_t num_shards,
                                             size_t shard_elems, uint32_t block, size_t layer_elems,

@@ -56,6 +56,12 @@ hipError_t launch_refresh(uint16_t *dst, const uint16_t *src, size_t count, bool
 hipError_t launch_quantize(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
                            float *scales, bool vector_path, hipStream_t stream);
 
+// The quantization that also stores the bf16 it reads to `copy`: the
+// secondary refresh and its quantization in one pass.
+hipError_t launch_quantize_copy(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
+                                float *scales, uint16_t *copy, bool vector_path,
+                                hipStream_t stream);
+
 // Adam step + bf16 primary + optional bf16 secondary + int8 codes/scales of
 // the primary, in one pass (vector_path) or as the three scalar kernels.
 hipError_t launch_fused(float *p, float *m, float *v, const float *g, uint16_t *primary,

@@ -38,7 +38,7 @@ from . import synth
 from . import zpp
 from .workloads import (BYTES_ADAM, BYTES_REFRESH, bytes_fused, bytes_fused_receive,
                         bytes_gather, bytes_quant, bytes_quant_i4, bytes_receive_adam,
-                        bytes_reduce_i4)
+                        bytes_reduce_i4, bytes_refresh_quant)
 
 
 SYNC_MODES = ("event", "host", "none")
@@ -64,10 +64,13 @@ class PartitionPipeline:
     gradient of its partition, from the backward pass) opens every step with
     its int4 quantization into source slot 0 of the exchange, the copy this
     rank contributes to its own partition; the other slots stand for the
-    copies the exchange delivers from the other ranks."""
+    copies the exchange delivers from the other ranks.  `fuse_copy` runs the
+    refresh and the quantization of the separate-kernel path as one pass
+    (`zpp_refresh_quantize_i8`)."""
 
     def __init__(self, wl, device="cuda", fused=False, sync="event", overlap=True,
-                 qgz_sources=0, streams=3, fuse_receive=False, qgz_interleaved=False):
+                 qgz_sources=0, streams=3, fuse_receive=False, qgz_interleaved=False,
+                 fuse_copy=False):
         if sync not in SYNC_MODES:
             raise ValueError("sync must be one of %s" % (SYNC_MODES,))
         if streams not in (1, 3):
@@ -79,6 +82,7 @@ class PartitionPipeline:
         self.overlap = overlap
         self.streams = streams
         self.fuse_receive = fuse_receive
+        self.fuse_copy = fuse_copy
         # with qgz_sources > 0 every step starts with the qgZ receive: the mean
         # of that many int4 copies of this partition's gradient becomes `grad`
         self.exchange = (GradientExchange(wl.n, qgz_sources, wl.block, device,
@@ -244,7 +248,9 @@ class PartitionPipeline:
                 # the fused kernel writes the codes, which the last gather reads
                 zpp.stream_wait(self.compute, self.ev_gather)
             else:
-                zpp.stream_wait(self.compute, self.ev_refresh)
+                # the last refresh has read the primary
+                zpp.stream_wait(self.compute,
+                                self.ev_quant if self.fuse_copy else self.ev_refresh)
         self._send(self.compute)
         if self._receive_apart():
             self._timed("reduce_i4", self.compute,
@@ -259,17 +265,10 @@ class PartitionPipeline:
                 # timed run waits first, so that the start of the timing pair
                 # follows the wait
                 zpp.stream_wait(self.copy, self.ev_primary)
-            self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
-                self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary,
-                done_after=self.ev_refresh))
-            if t > 1 and not serial:
-                # the quantization rewrites the codes the last gather read;
-                # in serial order the step already waited for that gather
-                # before the partition step, which the copy stream follows
-                zpp.stream_wait(self.copy, self.ev_gather)
-            self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
-                self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
-                done_after=self.ev_quant))
+            if self.fuse_copy:
+                self._copy_and_quantize(t, serial)
+            else:
+                self._copy_then_quantize(t, serial)
         waits = []
         if self.sync == "event":
             # the gather waits on the quantization itself (the fix, through
@@ -280,6 +279,33 @@ class PartitionPipeline:
         elif self.sync == "host":
             self.ev_quant.synchronize()
         self._gathers(self.comm, waits, self.ev_gather)
+
+    def _copy_and_quantize(self, t, serial):
+        """Three streams: the refresh and the quantization as one pass on the
+        copy stream, after the primary and (across iterations) after the last
+        gather read the codes."""
+        n, B = self.wl.n, self.wl.block
+        if t > 1 and not serial:
+            zpp.stream_wait(self.copy, self.ev_gather)
+        self._timed("refresh_quant", self.copy, lambda: zpp.refresh_quantize_i8(
+            self.secondary, self.primary, self.codes, self.scales, block=B, n=n,
+            stream=self.copy, wait_before=self.ev_primary, done_after=self.ev_quant))
+
+    def _copy_then_quantize(self, t, serial):
+        """Three streams: the refresh, then the quantization, on the copy
+        stream."""
+        n, B = self.wl.n, self.wl.block
+        self._timed("refresh", self.copy, lambda: zpp.refresh_secondary(
+            self.secondary, self.primary, n, stream=self.copy, wait_before=self.ev_primary,
+            done_after=self.ev_refresh))
+        if t > 1 and not serial:
+            # the quantization rewrites the codes the last gather read; in
+            # serial order the step already waited for that gather before the
+            # partition step, which the copy stream follows
+            zpp.stream_wait(self.copy, self.ev_gather)
+        self._timed("quant", self.copy, lambda: zpp.quantize_blockwise_i8(
+            self.secondary, self.codes, self.scales, block=B, n=n, stream=self.copy,
+            done_after=self.ev_quant))
 
     def _step_one_stream(self, t):
         """The iteration in path order on the compute stream: each kernel
@@ -305,10 +331,15 @@ class PartitionPipeline:
             self._fused_pass(t, cs, None)
         else:
             self._partition_step(t, cs)
-            self._timed("refresh", cs, lambda: zpp.refresh_secondary(
-                self.secondary, self.primary, n, stream=cs))
-            self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
-                self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
+            if self.fuse_copy:
+                self._timed("refresh_quant", cs, lambda: zpp.refresh_quantize_i8(
+                    self.secondary, self.primary, self.codes, self.scales, block=B, n=n,
+                    stream=cs))
+            else:
+                self._timed("refresh", cs, lambda: zpp.refresh_secondary(
+                    self.secondary, self.primary, n, stream=cs))
+                self._timed("quant", cs, lambda: zpp.quantize_blockwise_i8(
+                    self.secondary, self.codes, self.scales, block=B, n=n, stream=cs))
         self._gathers(cs)
 
     def _sends(self):
@@ -407,11 +438,12 @@ class PartitionPipeline:
             out["receive_adam"] = float(bytes_receive_adam(wl.n, self.exchange.num_src, wl.block))
         else:
             out["adam"] = BYTES_ADAM * wl.n
-        out.update({
-            "refresh": BYTES_REFRESH * wl.n,
-            "quant": float(bytes_quant(wl.n, wl.block)),
-            "gather": gather,
-        })
+        if self.fuse_copy:
+            out["refresh_quant"] = float(bytes_refresh_quant(wl.n, wl.block))
+        else:
+            out.update({"refresh": BYTES_REFRESH * wl.n,
+                        "quant": float(bytes_quant(wl.n, wl.block))})
+        out["gather"] = gather
         return out
 
     def kernel_times_ms(self):

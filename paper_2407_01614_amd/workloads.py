@@ -105,6 +105,12 @@ def bytes_quant(n, block=BLOCK):
     return 2 * n + n + 4 * ((n + block - 1) // block)
 
 
+def bytes_refresh_quant(n, block=BLOCK):
+    # the refresh and its quantization in one pass: read 2 B once, write the
+    # secondary (2 B), the codes (1 B) and one fp32 scale per block
+    return 2 * n + 2 * n + n + 4 * ((n + block - 1) // block)
+
+
 def bytes_gather(shard_elems, num_shards, layer_elems, block=BLOCK):
     # reads whole shards only as far as the layer reaches
     read_codes = layer_elems

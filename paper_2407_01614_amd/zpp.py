@@ -45,6 +45,8 @@ _lib.zpp_refresh_secondary.restype = ctypes.c_int
 _lib.zpp_refresh_secondary.argtypes = [_P, _P, _sz, _P, _P, _P]
 _lib.zpp_quantize_blockwise_i8.restype = ctypes.c_int
 _lib.zpp_quantize_blockwise_i8.argtypes = [_P, _sz, _u32, _P, _P, _P, _P, _P]
+_lib.zpp_refresh_quantize_i8.restype = ctypes.c_int
+_lib.zpp_refresh_quantize_i8.argtypes = [_P, _P, _sz, _u32, _P, _P, _P, _P, _P]
 _lib.zpp_dequant_gather_layer.restype = ctypes.c_int
 _lib.zpp_dequant_gather_layer.argtypes = [_P, _P, _u32, _sz, _u32, _sz, _P, _P, _P, _u32, _P]
 _lib.zpp_quantize_blockwise_i4.restype = ctypes.c_int
@@ -79,7 +81,8 @@ _lib.zpp_last_hip_error.restype = ctypes.c_int
 _lib.zpp_last_hip_error.argtypes = []
 
 EXPORTS = ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize", "zpp_refresh_secondary",
-           "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer", "zpp_quantize_blockwise_i4",
+           "zpp_quantize_blockwise_i8", "zpp_refresh_quantize_i8", "zpp_dequant_gather_layer",
+           "zpp_quantize_blockwise_i4",
            "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
            "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
            "zpp_dequant_reduce_i4_interleaved", "zpp_qgz_receive_adam_step_interleaved",
@@ -317,6 +320,25 @@ def quantize_blockwise_i8(src_bf16, codes, scales, *, block=256, n=None, stream=
                                         scales.data_ptr(), stream_handle(stream),
                                         _event_handle(wait_before), _event_handle(done_after))
     _check(st, "zpp_quantize_blockwise_i8")
+
+
+def refresh_quantize_i8(secondary_bf16, src_bf16, codes, scales, *, block=256, n=None,
+                        stream=None, wait_before=None, done_after=None):
+    """zpp_refresh_quantize_i8 over the first ``n`` elements of src: the
+    secondary refresh and its quantization in one pass."""
+    _dev(secondary_bf16, _BF16, "secondary_bf16")
+    _dev(src_bf16, _BF16, "src_bf16")
+    _dev(codes, _I8, "codes")
+    _dev(scales, _F32, "scales")
+    if n is None:
+        n = src_bf16.numel()
+    if (src_bf16.numel() < n or secondary_bf16.numel() < n or codes.numel() < n
+            or scales.numel() < num_blocks(n, block)):
+        raise ValueError("a buffer is too small for n = %d" % n)
+    st = _lib.zpp_refresh_quantize_i8(secondary_bf16.data_ptr(), src_bf16.data_ptr(), n, block,
+                                      codes.data_ptr(), scales.data_ptr(), stream_handle(stream),
+                                      _event_handle(wait_before), _event_handle(done_after))
+    _check(st, "zpp_refresh_quantize_i8")
 
 
 def dequant_gather_layer(shard_codes, shard_scales, shard_elems, layer_elems, out_bf16, *,

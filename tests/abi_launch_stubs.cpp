@@ -28,6 +28,10 @@ hipError_t launch_quantize(const uint16_t *, size_t, uint32_t, int8_t *, float *
                            hipStream_t) {
     return reached();
 }
+hipError_t launch_quantize_copy(const uint16_t *, size_t, uint32_t, int8_t *, float *, uint16_t *,
+                                bool, hipStream_t) {
+    return reached();
+}
 hipError_t launch_fused(float *, float *, float *, const float *, uint16_t *, uint16_t *, int8_t *,
                         float *, size_t, uint32_t, const AdamConsts &, bool, hipStream_t) {
     return reached();

@@ -131,6 +131,15 @@ static void check_refresh_and_quantize(void)
                                             NULL, NULL),
                   ZPP_EOVERLAP);
 
+    uint16_t *sec = dev(6);
+    EXPECT_STATUS(zpp_refresh_quantize_i8(sec, a, 0, 256, c, s, NULL, NULL, NULL), ZPP_OK);
+    EXPECT_STATUS(zpp_refresh_quantize_i8(sec, a, 1000, 4160, c, s, NULL, NULL, NULL), ZPP_EINVAL);
+    EXPECT_STATUS(zpp_refresh_quantize_i8(NULL, a, 1000, 256, c, s, NULL, NULL, NULL), ZPP_EINVAL);
+    EXPECT_STATUS(zpp_refresh_quantize_i8(sec, a, 1000, 256, c, dev_off(3, 2), NULL, NULL, NULL),
+                  ZPP_EALIGN);
+    EXPECT_STATUS(zpp_refresh_quantize_i8(dev_off(0, 1000), a, 1000, 256, c, s, NULL, NULL, NULL),
+                  ZPP_EOVERLAP);
+
     float *x = dev(4);
     uint8_t *c4 = dev(5);
     EXPECT_STATUS(zpp_quantize_blockwise_i4(x, 0, 256, c4, s, NULL, NULL, NULL), ZPP_OK);

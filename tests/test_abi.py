@@ -34,7 +34,8 @@ def declared_functions():
 def test_header_declares_every_entry_point():
     names = declared_functions()
     for fn in ("zpp_adam_partition_step", "zpp_adam_step_refresh_quantize",
-               "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_dequant_gather_layer",
+               "zpp_refresh_secondary", "zpp_quantize_blockwise_i8", "zpp_refresh_quantize_i8",
+               "zpp_dequant_gather_layer",
                "zpp_quantize_blockwise_i4", "zpp_dequant_reduce_i4", "zpp_qgz_receive_adam_step",
                "zpp_qgz_receive_step_refresh_quantize", "zpp_quantize_blockwise_i4_interleaved",
                "zpp_dequant_reduce_i4_interleaved", "zpp_qgz_receive_adam_step_interleaved",
@@ -174,6 +175,22 @@ def test_refresh_validation(zpp):
     assert r(A, A + 30, 16, None, None, None) == zpp.ZPP_EOVERLAP
     assert r(A, A, 16, None, None, None) == zpp.ZPP_EOVERLAP
     assert r(A, B, (1 << 63), None, None, None) == zpp.ZPP_EINVAL
+
+
+def test_refresh_quantize_validation(zpp):
+    rq = zpp.raw.zpp_refresh_quantize_i8
+    assert rq(None, None, 0, 256, None, None, None, None, None) == zpp.ZPP_OK
+    for blk in (0, 32, 100, 4160):
+        assert rq(D, A, 1024, blk, B, C, None, None, None) == zpp.ZPP_EINVAL, blk
+    assert rq(None, A, 1024, 256, B, C, None, None, None) == zpp.ZPP_EINVAL
+    assert rq(D, A, 1024, 256, None, C, None, None, None) == zpp.ZPP_EINVAL
+    assert rq(D + 1, A, 1024, 256, B, C, None, None, None) == zpp.ZPP_EALIGN
+    assert rq(D, A + 1, 1024, 256, B, C, None, None, None) == zpp.ZPP_EALIGN
+    assert rq(D, A, 1024, 256, B, C + 2, None, None, None) == zpp.ZPP_EALIGN
+    assert rq(A + 2046, A, 1024, 256, B, C, None, None, None) == zpp.ZPP_EOVERLAP
+    assert rq(D, A, 1024, 256, D + 2047, C, None, None, None) == zpp.ZPP_EOVERLAP
+    assert rq(D, A, 1024, 256, B, B + 1020, None, None, None) == zpp.ZPP_EOVERLAP
+    assert rq(D, A, 1024, 256, B, A + 2044, None, None, None) == zpp.ZPP_EOVERLAP
 
 
 def test_quant_validation(zpp):

@@ -37,7 +37,7 @@ def hip():
     return h
 
 
-@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+@pytest.mark.parametrize("fused", [False, True, "copy"], ids=["separate", "fused", "fused-copy"])
 def test_iteration_in_a_hip_graph(zpp, fused):
     n, B, P2 = (1 << 20) + 256, 256, 2
     hp = dict(lr=float(np.float32(1e-4)), beta1=float(np.float32(0.9)),
@@ -60,7 +60,14 @@ def test_iteration_in_a_hip_graph(zpp, fused):
     ev_prim, ev_quant, ev_gather = zpp.Event(), zpp.Event(), zpp.Event()
 
     def iteration(st):
-        if fused:
+        if fused == "copy":
+            # the refresh and the quantization as one pass
+            zpp.adam_partition_step(st["p"], st["m"], st["v"], g, st["prim"], step=1,
+                                    stream=compute, **hp)
+            ev_prim.record(compute)
+            zpp.refresh_quantize_i8(st["sec"], st["prim"], st["codes"], st["scales"], block=B,
+                                    stream=copy, wait_before=ev_prim, done_after=ev_quant)
+        elif fused:
             ev_prim.record(compute)  # the fork: the second stream joins the capture here
             zpp.adam_step_refresh_quantize(st["p"], st["m"], st["v"], g, st["prim"], st["sec"],
                                            st["codes"], st["scales"], step=1, block=B,

@@ -281,6 +281,51 @@ def test_quant_arbitrary_bit_patterns(zpp):
     assert_quant_equal(run_quant_gpu(zpp, x, 256), oracle.quantize_blockwise_i8(x, 256), "bits")
 
 
+def run_refresh_quant_gpu(zpp, x, block, pad_src=0, pad_dst=0, pad_codes=0):
+    tx = to_dev(x, pad=pad_src)
+    sec = empty_dev(x.size, np.uint16, pad=pad_dst, fill=0x7FC0)
+    codes = empty_dev(x.size, np.int8, pad=pad_codes, fill=99)
+    nb = (x.size + block - 1) // block
+    scales = empty_dev(nb, np.float32, fill=-1.0)
+    zpp.refresh_quantize_i8(sec, tx, codes, scales, block=block)
+    torch.cuda.synchronize()
+    return to_host(sec, np.uint16), to_host(codes, np.int8), to_host(scales, np.float32)
+
+
+@pytest.mark.parametrize("block", [64, 192, 256, 320, 1024, 4096])
+@pytest.mark.parametrize("n", [1, 7, 255, 256, 257, 256 * 5 + 80, 100000, 1 << 17])
+def test_refresh_quantize_vs_oracle(zpp, block, n):
+    """The refresh and its quantization in one pass: the secondary is the
+    source bit for bit, codes and scales are the oracle's quantization."""
+    x = synth.bf16_weights(n, 56, n + block)
+    sec, codes, scales = run_refresh_quant_gpu(zpp, x, block)
+    assert_bits_equal(sec, oracle.refresh(x), "secondary n=%d block=%d" % (n, block))
+    assert_quant_equal((codes, scales), oracle.quantize_blockwise_i8(x, block),
+                       "n=%d block=%d" % (n, block))
+
+
+@pytest.mark.parametrize("pads", [(1, 0, 0), (0, 1, 0), (0, 0, 3), (8, 0, 0)],
+                         ids=["src", "secondary", "codes", "src-16"])
+def test_refresh_quantize_misaligned(zpp, pads):
+    """Misaligned views take the scalar kernel (or, for a 16-byte-aligned
+    offset, the vector one): the same bits."""
+    n = 256 * 37 + 80
+    x = synth.bf16_weights(n, 57)
+    sec, codes, scales = run_refresh_quant_gpu(zpp, x, 256, *pads)
+    assert_bits_equal(sec, x, "secondary pads=%s" % (pads,))
+    assert_quant_equal((codes, scales), oracle.quantize_blockwise_i8(x, 256), "pads=%s" % (pads,))
+
+
+@pytest.mark.parametrize("block", [256, 4032])
+def test_refresh_quantize_special_blocks_and_bits(zpp, block):
+    """Zero, Inf, NaN, tiny and huge blocks and arbitrary bit patterns (NaN
+    payloads copied as they are)."""
+    x = np.concatenate([special_blocks(block), synth.random_bits16(block * 64 + 33, 58)])
+    sec, codes, scales = run_refresh_quant_gpu(zpp, x, block)
+    assert_bits_equal(sec, x, "secondary")
+    assert_quant_equal((codes, scales), oracle.quantize_blockwise_i8(x, block), "special")
+
+
 # ===========================================================================
 # Dequant-gather
 # ===========================================================================

@@ -313,11 +313,11 @@ def test_iterations_with_buffer_reuse(zpp):
 
 
 def test_pipeline_modes_agree(zpp):
-    """Separate kernels or the fused one, on three streams ordered by a device
-    event or by a host wait, or on one stream in path order, or switching
-    between three streams and one from one iteration to the next: from the
-    same inputs, three iterations end in bit-identical state, codes and
-    gathered layer."""
+    """Separate kernels or the fused one, the refresh and quantization as two
+    kernels or one pass, on three streams ordered by a device event or by a
+    host wait, or on one stream in path order, or switching between three
+    streams and one from one iteration to the next: from the same inputs,
+    three iterations end in bit-identical state, codes and gathered layer."""
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import Workload
     wl = Workload(name="small", cfg_id=9, n=1 << 20, layer_elems=8 * (1 << 17) - 1000,
@@ -327,21 +327,26 @@ def test_pipeline_modes_agree(zpp):
     peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
                                           wl.block) for j in range(wl.secondary_world - 1)]
     results = {}
-    modes = [(fused, sync, (3, 3, 3)) for fused in (False, True) for sync in ("event", "host")]
-    modes += [(False, "event", (1, 1, 1)), (True, "event", (1, 1, 1)),
-              (False, "event", (3, 1, 3)), (True, "event", (1, 3, 1))]
-    for fused, sync, per_step in modes:
-        pipe = PartitionPipeline(wl, fused=fused, sync=sync, streams=per_step[0])
+    modes = [(fused, sync, (3, 3, 3), False) for fused in (False, True)
+             for sync in ("event", "host")]
+    modes += [(False, "event", (1, 1, 1), False), (True, "event", (1, 1, 1), False),
+              (False, "event", (3, 1, 3), False), (True, "event", (1, 3, 1), False)]
+    # the refresh and the quantization as one pass
+    modes += [(False, "event", (3, 3, 3), True), (False, "host", (3, 3, 3), True),
+              (False, "event", (1, 1, 1), True), (False, "event", (1, 3, 1), True)]
+    for fused, sync, per_step, fuse_copy in modes:
+        pipe = PartitionPipeline(wl, fused=fused, sync=sync, streams=per_step[0],
+                                 fuse_copy=fuse_copy)
         pipe.load(p0, g0, [q[0] for q in peers], [q[1] for q in peers])
         for k in per_step:
             pipe.streams = k
             pipe.step()
         pipe.wait()
-        results[(fused, sync, per_step)] = [t.cpu().numpy().copy() for t in
-                                            (pipe.master, pipe.exp_avg, pipe.exp_avg_sq,
+        results[(fused, sync, per_step, fuse_copy)] = [
+            t.cpu().numpy().copy() for t in (pipe.master, pipe.exp_avg, pipe.exp_avg_sq,
                                              pipe.primary, pipe.secondary, pipe.codes,
                                              pipe.scales, pipe.out)]
-    ref = results[(False, "event", (3, 3, 3))]
+    ref = results[(False, "event", (3, 3, 3), False)]
     for key, res in results.items():
         for i, (a, b) in enumerate(zip(res, ref)):
             assert_bits_equal(a.view(np.uint8), b.view(np.uint8), "%s output %d" % (key, i))
