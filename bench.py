@@ -67,6 +67,32 @@ def parse():
     return ap.parse_args()
 
 
+# The sources each kernel is built from: a counter figure in the traffic file
+# is reported only while their digest still matches.
+_COMMON = ["zpp_device.h", "zpp_launch.h"]
+TRAFFIC_SOURCES = {
+    "adam": ["adam.hip", "zpp_adam.h"] + _COMMON,
+    "refresh": ["refresh.hip"] + _COMMON,
+    "quant": ["quant.hip", "zpp_quant.h"] + _COMMON,
+    "refresh_quant": ["quant.hip", "zpp_quant.h"] + _COMMON,
+    "gather": ["gather.hip"] + _COMMON,
+    "fused": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
+    "quant_i4": ["qgz.hip", "zpp_quant.h"] + _COMMON,
+    "reduce_i4": ["qgz.hip", "zpp_i4grad.h", "zpp_quant.h"] + _COMMON,
+    "receive_adam": ["receive_adam.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
+    "fused_receive": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
+}
+
+
+def source_digest(sources):
+    """The first 16 hex digits of the SHA-256 of the named csrc files."""
+    h = hashlib.sha256()
+    for fn in sources:
+        with open(os.path.join(ROOT, "paper_2407_01614_amd", "csrc", fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def measured_traffic(path, workload, kernel, sources):
     """HBM bytes per launch of `kernel` measured with rocprofv3 FETCH_SIZE /
     WRITE_SIZE (scaled by a plain copy of known size), or None when absent or
@@ -78,11 +104,7 @@ def measured_traffic(path, workload, kernel, sources):
     entry = tr.get("kernels", {}).get(kernel)
     if tr.get("workload") != workload or entry is None:
         return None
-    h = hashlib.sha256()
-    for fn in sources:
-        with open(os.path.join(ROOT, "paper_2407_01614_amd", "csrc", fn), "rb") as f:
-            h.update(f.read())
-    if h.hexdigest()[:16] != entry.get("source_digest"):
+    if source_digest(sources) != entry.get("source_digest"):
         return None
     return round(entry["bytes_per_launch"])
 
@@ -523,8 +545,7 @@ def main():
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
     sr_gbps = (kb["adam"] + kb["refresh"]) / (sr_us * 1e-6) / 1e9
 
-    traffic = measured_traffic(args.traffic, wl.name, "adam",
-                               ["adam.hip", "zpp_adam.h", "zpp_device.h"])
+    traffic = measured_traffic(args.traffic, wl.name, "adam", TRAFFIC_SOURCES["adam"])
 
     # the dominant kernel's mean launch duration over the K timed steps
     adam_live = live_times["adam"]

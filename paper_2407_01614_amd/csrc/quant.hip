@@ -35,9 +35,9 @@ namespace {
 
 constexpr int kQuantThreads = ZPP_QUANT_THREADS;
 
-// `copy` (may be null): the loaded bf16 are also stored there, bit for bit
-// (the secondary refresh taken into the quantization's pass).
-template <int B, int U>
+// With COPY the loaded bf16 are also stored to `copy`, bit for bit (the
+// secondary refresh taken into the quantization's pass).
+template <int B, int U, bool COPY>
 __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
     const uint16_t *__restrict__ src, size_t n, int8_t *__restrict__ codes,
     float *__restrict__ scales, uint16_t *__restrict__ copy) {
@@ -99,13 +99,13 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
                 c.y = quant_word(x[u][v].z, x[u][v].w, q);
                 if (valid && i + 8 <= n) {
                     st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
-                    if (copy)
+                    if (COPY)
                         st_nt(reinterpret_cast<u32x4 *>(copy + i), x[u][v]);
                 } else if (valid) {
                     for (int e = 0; e < 8 && i + e < n; ++e) {
                         codes[i + e] =
                             (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
-                        if (copy)
+                        if (COPY)
                             copy[i + e] = src[i + e];
                     }
                 }
@@ -120,6 +120,7 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
 // block; lane l holds the 8 elements [k B + 8 (64 v + l), +8) for v < B / 512
 // (lanes past the block's end hold nothing), so the absmax is a reduction
 // over the whole wave.
+template <bool COPY>
 __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
     const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
     float *__restrict__ scales, uint16_t *__restrict__ copy) {
@@ -165,13 +166,13 @@ __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
             c.y = quant_word(x[v].z, x[v].w, q);
             if (off < block && i + 8 <= n) {
                 st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
-                if (copy)
+                if (COPY)
                     st_nt(reinterpret_cast<u32x4 *>(copy + i), x[v]);
             } else if (off < block) {
                 for (int e = 0; e < 8 && i + e < n; ++e) {
                     codes[i + e] =
                         (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
-                    if (copy)
+                    if (COPY)
                         copy[i + e] = src[i + e];
                 }
             }
@@ -210,7 +211,7 @@ __global__ __launch_bounds__(kThreads) void quant_scalar_kernel(
     }
 }
 
-template <int B>
+template <int B, bool COPY>
 void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales, uint16_t *copy,
                 hipStream_t stream) {
     constexpr int L = (B / 8 < kWave) ? B / 8 : kWave;
@@ -218,8 +219,30 @@ void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales, uin
     const size_t nblocks = (n + B - 1) / B;
     const size_t need = (nblocks + kGroupsPerBlock - 1) / kGroupsPerBlock;
     const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
-    hipLaunchKernelGGL((quant_vec_kernel<B, ZPP_QUANT_UNROLL>), dim3(grid), dim3(kQuantThreads), 0,
-                       stream, src, n, codes, scales, copy);
+    hipLaunchKernelGGL((quant_vec_kernel<B, ZPP_QUANT_UNROLL, COPY>), dim3(grid),
+                       dim3(kQuantThreads), 0, stream, src, n, codes, scales, copy);
+}
+
+template <bool COPY>
+void launch_vector(const uint16_t *src, size_t n, uint32_t block, int8_t *codes, float *scales,
+                   uint16_t *copy, hipStream_t stream) {
+    switch (block) {
+    case 64: launch_vec<64, COPY>(src, n, codes, scales, copy, stream); break;
+    case 128: launch_vec<128, COPY>(src, n, codes, scales, copy, stream); break;
+    case 256: launch_vec<256, COPY>(src, n, codes, scales, copy, stream); break;
+    case 512: launch_vec<512, COPY>(src, n, codes, scales, copy, stream); break;
+    case 1024: launch_vec<1024, COPY>(src, n, codes, scales, copy, stream); break;
+    case 2048: launch_vec<2048, COPY>(src, n, codes, scales, copy, stream); break;
+    case 4096: launch_vec<4096, COPY>(src, n, codes, scales, copy, stream); break;
+    default: {
+        const size_t nblocks = (n + block - 1) / block;
+        constexpr size_t kWaves = kQuantThreads / kWave;
+        const size_t need = (nblocks + kWaves - 1) / kWaves;
+        const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
+        hipLaunchKernelGGL((quant_any_kernel<COPY>), dim3(grid), dim3(kQuantThreads), 0, stream,
+                           src, n, block, codes, scales, copy);
+    }
+    }
 }
 
 }  // namespace
@@ -228,24 +251,10 @@ hipError_t launch_quantize_copy(const uint16_t *src, size_t n, uint32_t block, i
                                 float *scales, uint16_t *copy, bool vector_path,
                                 hipStream_t stream) {
     if (vector_path) {
-        switch (block) {
-        case 64: launch_vec<64>(src, n, codes, scales, copy, stream); break;
-        case 128: launch_vec<128>(src, n, codes, scales, copy, stream); break;
-        case 256: launch_vec<256>(src, n, codes, scales, copy, stream); break;
-        case 512: launch_vec<512>(src, n, codes, scales, copy, stream); break;
-        case 1024: launch_vec<1024>(src, n, codes, scales, copy, stream); break;
-        case 2048: launch_vec<2048>(src, n, codes, scales, copy, stream); break;
-        case 4096: launch_vec<4096>(src, n, codes, scales, copy, stream); break;
-        default: {
-            const size_t nblocks = (n + block - 1) / block;
-            constexpr size_t kWaves = kQuantThreads / kWave;
-            const size_t need = (nblocks + kWaves - 1) / kWaves;
-            const unsigned grid =
-                (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
-            hipLaunchKernelGGL(quant_any_kernel, dim3(grid), dim3(kQuantThreads), 0, stream, src,
-                               n, block, codes, scales, copy);
-        }
-        }
+        if (copy)
+            launch_vector<true>(src, n, block, codes, scales, copy, stream);
+        else
+            launch_vector<false>(src, n, block, codes, scales, nullptr, stream);
     } else {
         const size_t nblocks = (n + block - 1) / block;
         const size_t need = (nblocks + (kThreads / kWave) - 1) / (kThreads / kWave);
