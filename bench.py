@@ -508,20 +508,20 @@ def main():
     copy_gbps = ceil["copy"]["GB/s"]
     torch_ctx = torch_adamw_context(wl, args.steps)
     # the whole iteration seen by the rank with qgZ: the int4 quantization of
-    # its own gradient (the send), the receive of 8 int4 copies of its
-    # partition's gradient delivered into one interleaved receive buffer
-    # (their mean) feeding the step, as its own kernel, fused into the
-    # partition step, and inside the single pass of step, refresh and
-    # quantization
+    # its gradient into its send buffer (the send), the receive of 8 int4
+    # copies of its partition's gradient delivered into one interleaved
+    # receive buffer (their mean) feeding the step, as its own kernel, fused
+    # into the partition step, and inside the single pass of step, refresh
+    # and quantization
     from paper_2407_01614_amd import synth as _synth
     from paper_2407_01614_amd.pipeline import GradientExchange
     pipe.exchange = GradientExchange(wl.n, 8, wl.block, interleaved=True)
-    for q in range(1, 8):
+    for q in range(8):
         g = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id, _synth.KIND_GRAD, rank=q)
         pipe.exchange.quantize(q, g)
         del g
     pipe.send_grad = _synth.device_normal_f32(wl.n, _synth.GRAD_STD, wl.cfg_id,
-                                              _synth.KIND_GRAD, rank=0)
+                                              _synth.KIND_GRAD, rank=8)
     torch.cuda.synchronize()
     pipe.fuse_receive = False
     ilr_ms, ilr_times, ilr_kb, ilr_step_bytes = run(False, "event", True)

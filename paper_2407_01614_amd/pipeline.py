@@ -60,11 +60,11 @@ class PartitionPipeline:
     and quantization (`zpp_qgz_receive_step_refresh_quantize`).
     `qgz_interleaved` keeps the int4 copies in one interleaved receive buffer
     (`GradientExchange`), read by the `..._interleaved` entry points.  With
-    an exchange, setting `send_grad` (an fp32 tensor of n: this rank's own
-    gradient of its partition, from the backward pass) opens every step with
-    its int4 quantization into source slot 0 of the exchange, the copy this
-    rank contributes to its own partition; the other slots stand for the
-    copies the exchange delivers from the other ranks.  `fuse_copy` runs the
+    an exchange, setting `send_grad` (an fp32 tensor of n: one partition's
+    worth of this rank's gradient, from the backward pass) opens every step
+    with its int4 quantization into the exchange's send buffer (plain
+    layout), the sender's share of the exchange; the receive slots stand for
+    the copies the exchange delivers from the ranks.  `fuse_copy` runs the
     refresh and the quantization of the separate-kernel path as one pass
     (`zpp_refresh_quantize_i8`)."""
 
@@ -346,11 +346,11 @@ class PartitionPipeline:
         return self.exchange is not None and self.send_grad is not None
 
     def _send(self, stream):
-        """The qgZ send of this rank's own gradient: its int4 quantization
-        into source slot 0, ahead of the receive on the same stream."""
+        """The qgZ send: the int4 quantization of this rank's gradient into
+        the exchange's send buffer, ahead of the receive on the same stream."""
         if self._sends():
-            self._timed("quant_i4", stream, lambda: self.exchange.quantize(
-                0, self.send_grad, stream=stream))
+            self._timed("quant_i4", stream, lambda: self.exchange.send(
+                self.send_grad, stream=stream))
 
     def _receive_fused(self):
         return self.exchange is not None and self.fuse_receive
@@ -457,7 +457,9 @@ class GradientExchange:
     int4 (sources other than this rank are simulated in this GPU's memory),
     and the rank reduces the copies into the fp32 mean gradient that the
     partition step reads.  With `interleaved` the copies arrive in one
-    receive buffer, block by block (the layout of include/zpp.h)."""
+    receive buffer, block by block (the layout of include/zpp.h).  `send`
+    quantizes this rank's own gradient into a send buffer of the plain
+    layout (`send_codes`, `send_scales`), what a sender hands the exchange."""
 
     def __init__(self, n, num_src, block=256, device="cuda", interleaved=False):
         self.n, self.num_src, self.block = n, num_src, block
@@ -472,6 +474,15 @@ class GradientExchange:
                           for _ in range(num_src)]
             self.scales = [torch.empty(nb, dtype=torch.float32, device=device)
                            for _ in range(num_src)]
+
+    def send(self, grad, stream=None, done_after=None):
+        if getattr(self, "send_codes", None) is None:
+            dev = grad.device
+            self.send_codes = torch.empty((self.n + 1) // 2, dtype=torch.uint8, device=dev)
+            self.send_scales = torch.empty((self.n + self.block - 1) // self.block,
+                                           dtype=torch.float32, device=dev)
+        zpp.quantize_blockwise_i4(grad, self.send_codes, self.send_scales, block=self.block,
+                                  n=self.n, stream=stream, done_after=done_after)
 
     def quantize(self, q, grad, stream=None, done_after=None):
         if self.interleaved:

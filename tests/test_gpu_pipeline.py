@@ -461,12 +461,12 @@ def test_pipeline_with_qgz_receive(zpp):
 @pytest.mark.parametrize("streams", [1, 3])
 @pytest.mark.parametrize("fuse", [False, True], ids=["reduce", "fused-receive"])
 def test_pipeline_with_qgz_send(zpp, streams, fuse):
-    """Each step opens with the int4 quantization of this rank's own gradient
-    into source slot 0 of an interleaved receive buffer whose other 7 slots
-    hold the oracle's quantizations of the other ranks' gradients; the slot
-    equals the oracle's quantization, and two steps follow the oracle's Adam
-    on the oracle's mean of the 8 copies (the separate reduce's gradient
-    bit for bit)."""
+    """Each step opens with the int4 quantization of this rank's gradient
+    into the exchange's send buffer (the oracle's quantization of it, bit for
+    bit, after every step), then receives the 8 copies of an interleaved
+    receive buffer (the oracle's quantizations of 8 ranks' gradients,
+    written at set-up): two steps follow the oracle's Adam on the oracle's
+    mean of the 8 copies (the separate reduce's gradient bit for bit)."""
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import Workload
     wl = Workload(name="small-qgz-send", cfg_id=15, n=(1 << 19) + 40, layer_elems=4 * (1 << 17),
@@ -474,24 +474,26 @@ def test_pipeline_with_qgz_send(zpp, streams, fuse):
     P, B = 8, wl.block
     srcs = [synth.gradients(wl.n, wl.cfg_id, q) for q in range(P)]
     quants = [oracle.quantize_blockwise_i4(x, B) for x in srcs]
+    own = synth.gradients(wl.n, wl.cfg_id, 99)
     pipe = PartitionPipeline(wl, qgz_sources=P, qgz_interleaved=True, streams=streams,
                              fuse_receive=fuse)
     peers = [oracle.quantize_blockwise_i8(synth.bf16_weights(wl.shard_elems, wl.cfg_id, j + 1),
                                           B) for j in range(wl.secondary_world - 1)]
     p0 = synth.master_weights(wl.n, wl.cfg_id)
     pipe.load(p0, np.zeros(wl.n, np.float32), [q[0] for q in peers], [q[1] for q in peers])
-    for q in range(1, P):
+    for q in range(P):
         pipe.exchange.quantize(q, to_dev(srcs[q]))
-    nb = -(-wl.n // B)
-    # slot 0 (poisoned here) is written by the send of every step
-    pipe.exchange.codes.view(nb, P, B // 2)[:, 0, :].fill_(0x77)
-    pipe.exchange.scales.view(nb, P)[:, 0].fill_(float("nan"))
-    pipe.send_grad = to_dev(srcs[0])
+    pipe.send_grad = to_dev(own)
     torch.cuda.synchronize()
     assert "quant_i4" in pipe.kernel_bytes()
-    pipe.step()
-    pipe.step()
-    pipe.wait()
+    rc, rs = oracle.quantize_blockwise_i4(own, B)
+    for t in range(2):
+        pipe.step()
+        pipe.wait()
+        assert_bits_equal(pipe.exchange.send_codes.cpu().numpy(), rc, "sent codes, step %d" % t)
+        assert_bits_equal(to_host(pipe.exchange.send_scales, np.float32), rs,
+                          "sent scales, step %d" % t)
+        pipe.exchange.send_codes.fill_(0x77)  # the next step must write them again
     got = deinterleave(pipe.exchange.codes.cpu().numpy(), to_host(pipe.exchange.scales,
                                                                   np.float32), wl.n, B, P)
     for q in range(P):
