@@ -447,6 +447,33 @@ int main(int argc, char **argv)
     EXPECT(same * 100 >= nb * 99, "only %zu of %zu blocks agree", same, nb);
     EXPECT(memcmp(gout + s, rout + s, (N - s) * 2) == 0, "gather of the peer shards");
 
+    /* the refresh and the quantization as one pass over the same primary:
+     * the same secondary, codes and scales as the two calls, bit for bit */
+    {
+        uint16_t *dsec2 = dev_alloc(n * 2);
+        int8_t *dcodes2 = dev_alloc(n);
+        float *dscales2 = dev_alloc(nb * 4);
+        uint16_t *gsec2 = malloc(n * 2);
+        int8_t *gcodes2 = malloc(n);
+        float *gscales2 = malloc(nb * 4);
+        EXPECT(zpp_refresh_quantize_i8(dsec2, dprim, n, B, dcodes2, dscales2, copy, ev_gather,
+                                       ev_quant) == ZPP_OK,
+               "refresh + quantize");
+        HIP_OK(hipEventSynchronize(ev_quant));
+        HIP_OK(hipMemcpy(gsec2, dsec2, n * 2, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(gcodes2, dcodes2, n, hipMemcpyDeviceToHost));
+        HIP_OK(hipMemcpy(gscales2, dscales2, nb * 4, hipMemcpyDeviceToHost));
+        EXPECT(memcmp(gsec2, gsec, n * 2) == 0, "one-pass secondary");
+        EXPECT(memcmp(gcodes2, gcodes, n) == 0, "one-pass codes");
+        EXPECT(memcmp(gscales2, gscales, nb * 4) == 0, "one-pass scales");
+        free(gsec2);
+        free(gcodes2);
+        free(gscales2);
+        HIP_OK(hipFree(dsec2));
+        HIP_OK(hipFree(dcodes2));
+        HIP_OK(hipFree(dscales2));
+    }
+
     check_receive(n, p, &hp);
     check_validation();
 
