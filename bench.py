@@ -32,7 +32,7 @@ and, for context, PyTorch's fused AdamW on a partition of the same size.
 The CPU baseline times the plain CPU oracle on a bounded sample of the same
 workload on this host.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload llama-2-13b]
+    python bench.py [--gpus 1] [--steps 200] [--warmup 10] [--workload llama-2-13b]
 """
 import argparse
 import ctypes
@@ -52,8 +52,8 @@ METRIC = "achieved HBM GB/s (and % of peak) for partition step+refresh and dequa
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama-2-13b")
     ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of the workload the CPU oracle is timed on (0 = skip)")
