@@ -64,6 +64,10 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy 5 times, the known-size reference "
                          "that scales rocprofv3's FETCH_SIZE / WRITE_SIZE counters")
+    ap.add_argument("--no-clock-query", action="store_true",
+                    help="do not start the amd-smi child that reports the clock policy (under "
+                         "rocprofv3 --pmc the profiler's preloaded library initialises the GPU in "
+                         "every child process, before amd-smi's interpreter is started)")
     return ap.parse_args()
 
 
@@ -439,7 +443,7 @@ def main():
               % args.gpus, file=sys.stderr)
         sys.exit(2)
 
-    clocks = gpu_clock_state()
+    clocks = None if args.no_clock_query else gpu_clock_state()
     import torch
     from paper_2407_01614_amd.pipeline import PartitionPipeline
     from paper_2407_01614_amd.workloads import WORKLOADS
