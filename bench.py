@@ -59,6 +59,8 @@ def parse():
                     help="fraction of the workload the CPU oracle is timed on (0 = skip)")
     ap.add_argument("--cpu-steps", type=int, default=2,
                     help="consecutive steps the CPU oracle is timed over")
+    ap.add_argument("--cpu-other", type=int, default=1,
+                    help="also time the CPU oracle at the other workloads (1) or not (0)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters, if present")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -398,6 +400,37 @@ def cpu_baseline(wl, frac, threads=1, steps=1):
             "seconds": {k: round(v, 3) for k, v in secs_by.items()}}
 
 
+# The oracle at the workloads other than the benchmarked one: (fraction, steps)
+# for one thread, then for all host threads, chosen so that each leg takes
+# about 0.1-8 s of CPU time (Falcon-40B's all-threads leg runs its 10 steps).
+CPU_OTHER_SAMPLES = {
+    "tiny": ((1.0, 2), (1.0, 2)),
+    "falcon-7b-layer": ((0.5, 2), (1.0, 2)),
+    "llama-2-7b": ((0.1, 2), (1.0, 2)),
+    "llama-2-13b": ((0.1, 2), (1.0, 2)),
+    "falcon-40b": ((0.05, 2), (1.0, 10)),
+}
+
+
+def cpu_baseline_others(skip):
+    """The CPU oracle's rate at every other workload: one thread on a bounded
+    sample, and all host threads (at most 16) on the whole partition."""
+    from paper_2407_01614_amd.workloads import WORKLOADS
+    out = {}
+    for name, ((f1, k1), (fa, ka)) in CPU_OTHER_SAMPLES.items():
+        if name == skip:
+            continue
+        wl = WORKLOADS[name]
+        legs = {}
+        for leg, frac, steps, threads in (("one_thread", f1, k1, 1),
+                                          ("all_cores", fa, ka, host_threads())):
+            r = cpu_baseline(wl, frac, threads, steps=steps)
+            legs[leg] = {"value": r["value"], "unit": r["unit"], "cores": r["cores"],
+                         "sample": r["sample"]}
+        out[name] = legs
+    return out
+
+
 def gpu_clock_state():
     """Clock policy of GPU 0 as amd-smi reports it (graphics clock range and
     whether it is locked, HBM clock) and its market name, or None.  Called before this process
@@ -630,6 +663,8 @@ def main():
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample, steps=args.cpu_steps)
         line["cpu_baseline_all_cores"] = cpu_baseline(wl, args.cpu_sample, host_threads(),
                                                       steps=args.cpu_steps)
+        if args.cpu_other:
+            line["cpu_baseline_other_workloads"] = cpu_baseline_others(wl.name)
     else:
         line["cpu_baseline"] = None
         line["cpu_baseline_all_cores"] = None

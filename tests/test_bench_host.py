@@ -82,3 +82,15 @@ def test_cpu_baseline_record(bench):
         assert rec["value"] > 0
         assert set(rec["seconds"]) == {"adam", "refresh", "quant", "gather"}
         assert "2 step(s)" in rec["sample"]
+
+
+def test_cpu_baseline_other_workloads(bench, monkeypatch):
+    monkeypatch.setattr(bench, "CPU_OTHER_SAMPLES",
+                        {"tiny": ((0.05, 1), (0.05, 2)), "llama-2-13b": ((0.001, 1), (0.001, 1))})
+    monkeypatch.setattr(bench, "host_threads", lambda: 2)
+    out = bench.cpu_baseline_others("llama-2-13b")
+    assert set(out) == {"tiny"}
+    legs = out["tiny"]
+    assert legs["one_thread"]["cores"] == 1 and legs["all_cores"]["cores"] == 2
+    assert "2 step(s)" in legs["all_cores"]["sample"]
+    assert all(leg["value"] > 0 and leg["unit"] == "GB/s" for leg in legs.values())
