@@ -3,13 +3,26 @@
 // dequantization fused in.  1 B + 4/B B read, 2 B written per element.
 //
 // The shard pointers travel by value in the kernel arguments; blockIdx.y picks
-// the shard, so the pointer is a uniform (scalar) load.  Vector kernel: a lane
-// turns 8 codes (one 8-byte load) and one scale (shared by the 32 lanes of a
-// 256-block, served from cache) into 8 bf16 (one 16-byte store), about three
-// VALU operations per element.  Shape, swept at the Llama-2-13B layer:
-// two-wave workgroups with two rows per wave, at most 12 workgroups per CU,
-// 149-150 us; four-wave workgroups with four rows (uncapped) 155-156 us, one
-// row 178-181 us.
+// the shard, so the pointer is a uniform (scalar) load.
+//
+// Row kernel (blocks that are powers of two): a one-wave workgroup takes one
+// row of 512 consecutive elements of a shard; lane l turns the 8 codes
+// [8 l, 8 l + 8) of the row (one 8-byte load) into 8 bf16 (one 16-byte
+// store), about three VALU operations per element.  The row's max(1, 512/B)
+// scales are the same for the whole wave, so they are read by scalar loads
+// (through the scalar cache, beside the vector loads of the codes rather than
+// among them), and whether every one of them takes the fast dequantization is
+// one scalar branch.  Measured at the Llama-2-13B layer: 143.7-144.8 us
+// against 148.4-149.7 us for two-wave workgroups of two rows per wave reading
+// the scales by vector loads (the vector kernel below); more rows per wave or
+// more waves per workgroup were slower (148.8-152.4 us), and an access
+// pattern of the same loads and stores with no scales and no arithmetic
+// takes 139 us.
+//
+// Vector kernel (any other multiple of 64 as the block): a lane's scale is
+// a vector load at its own block index (shared by the lanes of a block,
+// served from cache); two-wave workgroups with two rows per wave, at most 12
+// workgroups per CU.
 #include "zpp_device.h"
 #include "zpp_launch.h"
 
@@ -24,6 +37,11 @@
 #endif
 #ifndef ZPP_GATHER_MAX_GRID_X
 #define ZPP_GATHER_MAX_GRID_X (1u << 20)
+#endif
+// the row kernel takes shards of up to this many rows (one workgroup each);
+// longer shards (beyond 2^40 elements) go to the grid-stride vector kernel
+#ifndef ZPP_GATHER_ROW_MAX_GRID_X
+#define ZPP_GATHER_ROW_MAX_GRID_X 0x7FFFFFFFu
 #endif
 
 namespace zpp {
@@ -131,6 +149,63 @@ __global__ __launch_bounds__(kGatherThreads) void gather_vec_kernel(GatherArgs a
     }
 }
 
+
+// One row of 512 elements per one-wave workgroup, one workgroup per row (a
+// one-shot grid: no loop, so the scale loads come before any store and the
+// compiler keeps them scalar).  B is a power of two: the row holds
+// kBlocks = max(1, 512 / B) whole blocks, or lies inside one.
+template <int B>
+__global__ __launch_bounds__(kWave) void gather_row_kernel(GatherArgs a) {
+    constexpr int kBlocks = B >= 512 ? 1 : 512 / B;
+    constexpr int kLanesPerBlock = B >= 512 ? kWave : B / 8;
+    const uint32_t j = blockIdx.y;  // every shard of the grid holds layer elements
+    const size_t lo = (size_t)j * a.shard_elems;
+    const size_t rest = a.layer_elems - lo;
+    const size_t valid = rest < a.shard_elems ? rest : a.shard_elems;
+    const int8_t *__restrict__ codes = a.shards.codes[j];
+    const float *__restrict__ scales = a.shards.scales[j];
+    uint16_t *__restrict__ out = a.out + lo;
+    const uint32_t lane = threadIdx.x;
+    const size_t r = blockIdx.x;
+    const size_t i = r * 512 + (size_t)lane * 8;
+    if ((r + 1) * 512 <= valid) {
+        const u32x2 c = ld_nt(reinterpret_cast<const u32x2 *>(codes + i));
+        // the row's scales: uniform indices, scalar loads
+        const size_t k0 = r * 512 / B;
+        float sv[kBlocks];
+        bool fast = true;
+#pragma unroll
+        for (int q = 0; q < kBlocks; ++q) {
+            sv[q] = scales[k0 + q];
+            fast = fast && fast_scale(sv[q]);
+        }
+        float s = sv[0];
+#pragma unroll
+        for (int q = 1; q < kBlocks; ++q)
+            s = (lane / kLanesPerBlock == (uint32_t)q) ? sv[q] : s;
+        u32x2 r0, r1;
+        if (fast) {
+            const float cb = -128.0f * s;
+            r0 = dequant_word_fast(c.x ^ 0x80808080u, s, cb);
+            r1 = dequant_word_fast(c.y ^ 0x80808080u, s, cb);
+        } else {
+            r0 = dequant_word_any(c.x, s);
+            r1 = dequant_word_any(c.y, s);
+        }
+        st_nt(reinterpret_cast<u32x4 *>(out + i), u32x4{r0.x, r0.y, r1.x, r1.y});
+    } else {
+        for (size_t e = i; e < i + 8 && e < valid; ++e) {
+            const float x = (float)codes[e] * scales[e / B];
+            out[e] = (uint16_t)bf16_rne_bits(x);
+        }
+    }
+}
+
+template <int B>
+void launch_rows(const GatherArgs &a, unsigned rows, unsigned shards, hipStream_t stream) {
+    hipLaunchKernelGGL((gather_row_kernel<B>), dim3(rows, shards), dim3(kWave), 0, stream, a);
+}
+
 // Any shard length and alignment: one output element per thread.
 __global__ __launch_bounds__(kThreads) void gather_scalar_kernel(GatherArgs a) {
     const uint32_t j = blockIdx.y;
@@ -160,7 +235,21 @@ hipError_t launch_gather(const GatherShards &shards, uint32_t num_shards, size_t
     a.layer_elems = layer_elems;
     a.block = make_block_div(block);
     const size_t per_shard = shard_elems < layer_elems ? shard_elems : layer_elems;
-    if (vector_path) {
+    const size_t nrows = (per_shard + 511) / 512;
+    if (vector_path && (block & (block - 1)) == 0 && nrows <= ZPP_GATHER_ROW_MAX_GRID_X) {
+        // only the shards that hold layer elements
+        const unsigned gy = (unsigned)((layer_elems + shard_elems - 1) / shard_elems);
+        const unsigned gx = (unsigned)nrows;
+        switch (block) {
+        case 64: launch_rows<64>(a, gx, gy, stream); break;
+        case 128: launch_rows<128>(a, gx, gy, stream); break;
+        case 256: launch_rows<256>(a, gx, gy, stream); break;
+        case 512: launch_rows<512>(a, gx, gy, stream); break;
+        case 1024: launch_rows<1024>(a, gx, gy, stream); break;
+        case 2048: launch_rows<2048>(a, gx, gy, stream); break;
+        default: launch_rows<4096>(a, gx, gy, stream); break;
+        }
+    } else if (vector_path) {
         constexpr size_t kTile = (size_t)kGatherThreads * 8 * ZPP_GATHER_UNROLL;
         const size_t tiles = (per_shard + kTile - 1) / kTile;
         const unsigned gx =

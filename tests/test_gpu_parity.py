@@ -362,6 +362,8 @@ def test_gather_tiny_layer(zpp):
     (64, 64 * 1024 - 1, 128),    # the largest secondary group
     (5, 5 * 2048 - 2048, 512),   # last shard entirely padding
     (2, 2 * 4096, 4096),
+    (4, 4 * 6144 - 100, 2048),
+    (3, 3 * 5120 - 1000, 1024),
     (8, 8 * 8192 - 1152, 192),   # blocks that are not powers of two
     (3, 3 * 5000 - 77, 320),
     (2, 2 * 4032 - 4031, 4032),
