@@ -43,33 +43,45 @@ __device__ __forceinline__ float i4grad_at(const I4Grad &s, size_t i) {
 // The gradient of the four consecutive elements i .. i+3 (i a multiple of 4,
 // all four in range): one 2-byte code load and one scale per source, the
 // sources taken eight at a time with all eight loads in flight before their
-// fma passes, which keep the source order.
-__device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
-    constexpr int kBatch = 8;
-    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    const size_t k = block_of(s.block, i);
-    for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
-        uint32_t w[kBatch];
-        float sc[kBatch];
+// fma passes, which keep the source order.  Whole batches of eight carry no
+// per-source test, so their loads issue back to back (the receive step at
+// the Llama-2-13B partition: 945 against 974 us, the dequant-reduce 259
+// against 270 us); a last partial batch tests each source.
+constexpr int kI4Batch = 8;
+
+template <bool FULL>
+__device__ __forceinline__ void i4grad_batch(float (&acc)[4], const I4Grad &s, size_t i, size_t k,
+                                             uint32_t q0) {
+    uint32_t w[kI4Batch];
+    float sc[kI4Batch];
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const uint32_t q = q0 + j;
-            w[j] = 0u;
-            sc[j] = 0.0f;
-            if (q < s.num_src) {
-                w[j] = ld_nt(reinterpret_cast<const uint16_t *>(s.codes[q] + i / 2));
-                sc[j] = s.scales[q][k];
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            if (q0 + j < s.num_src) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    acc[e] = __builtin_fmaf(i4_code(w[j], e), sc[j], acc[e]);
-            }
+    for (int j = 0; j < kI4Batch; ++j) {
+        const uint32_t q = q0 + j;
+        w[j] = 0u;
+        sc[j] = 0.0f;
+        if (FULL || q < s.num_src) {
+            w[j] = ld_nt(reinterpret_cast<const uint16_t *>(s.codes[q] + i / 2));
+            sc[j] = s.scales[q][k];
         }
     }
+#pragma unroll
+    for (int j = 0; j < kI4Batch; ++j) {
+        if (FULL || q0 + j < s.num_src) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc[e] = __builtin_fmaf(i4_code(w[j], e), sc[j], acc[e]);
+        }
+    }
+}
+
+__device__ __forceinline__ f32x4 i4grad_load4(const I4Grad &s, size_t i) {
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const size_t k = block_of(s.block, i);
+    uint32_t q0 = 0;
+    for (; q0 + kI4Batch <= s.num_src; q0 += kI4Batch)
+        i4grad_batch<true>(acc, s, i, k, q0);
+    if (q0 < s.num_src)
+        i4grad_batch<false>(acc, s, i, k, q0);
     return f32x4{i4grad_scaled(acc[0], s.scale_out), i4grad_scaled(acc[1], s.scale_out),
                  i4grad_scaled(acc[2], s.scale_out), i4grad_scaled(acc[3], s.scale_out)};
 }
@@ -115,34 +127,42 @@ __device__ __forceinline__ float i4grad_at(const I4GradIl &s, size_t i) {
 // the fma passes, which keep the source order), addressed in the interleaved
 // buffer: a wave's loads of one source are 128 contiguous bytes, and those of
 // all sources lie within one run of the buffer.
+template <bool FULL>
+__device__ __forceinline__ void i4grad_il_batch(float (&acc)[4], const I4GradIl &s,
+                                                const uint8_t *base, size_t stride,
+                                                const float *sbase, uint32_t q0) {
+    uint32_t w[kI4Batch];
+    float sc[kI4Batch];
+#pragma unroll
+    for (int b = 0; b < kI4Batch; ++b) {
+        w[b] = 0u;
+        sc[b] = 0.0f;
+        if (FULL || q0 + b < s.num_src) {
+            w[b] = ld_nt(reinterpret_cast<const uint16_t *>(base + (q0 + b) * stride));
+            sc[b] = sbase[q0 + b];
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < kI4Batch; ++b) {
+        if (FULL || q0 + b < s.num_src) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc[e] = __builtin_fmaf(i4_code(w[b], e), sc[b], acc[e]);
+        }
+    }
+}
+
 __device__ __forceinline__ f32x4 i4grad_load4(const I4GradIl &s, size_t i) {
-    constexpr int kBatch = 8;
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     const size_t k = block_of(s.block, i);
     const uint8_t *base = s.codes + il_code_byte(s, i, k, 0);
     const size_t stride = s.block.block / 2;
     const float *sbase = s.scales + k * s.num_src;
-    for (uint32_t q0 = 0; q0 < s.num_src; q0 += kBatch) {
-        uint32_t w[kBatch];
-        float sc[kBatch];
-#pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-            w[b] = 0u;
-            sc[b] = 0.0f;
-            if (q0 + b < s.num_src) {
-                w[b] = ld_nt(reinterpret_cast<const uint16_t *>(base + (q0 + b) * stride));
-                sc[b] = sbase[q0 + b];
-            }
-        }
-#pragma unroll
-        for (int b = 0; b < kBatch; ++b) {
-            if (q0 + b < s.num_src) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    acc[e] = __builtin_fmaf(i4_code(w[b], e), sc[b], acc[e]);
-            }
-        }
-    }
+    uint32_t q0 = 0;
+    for (; q0 + kI4Batch <= s.num_src; q0 += kI4Batch)
+        i4grad_il_batch<true>(acc, s, base, stride, sbase, q0);
+    if (q0 < s.num_src)
+        i4grad_il_batch<false>(acc, s, base, stride, sbase, q0);
     return f32x4{i4grad_scaled(acc[0], s.scale_out), i4grad_scaled(acc[1], s.scale_out),
                  i4grad_scaled(acc[2], s.scale_out), i4grad_scaled(acc[3], s.scale_out)};
 }

@@ -107,7 +107,7 @@ def run_reduce_i4(zpp, quants, n, block, scale_out, pad_out=0, pad_codes=0):
     return to_host(out, np.float32)
 
 
-@pytest.mark.parametrize("P", [1, 2, 3, 8, 64])
+@pytest.mark.parametrize("P", [1, 2, 3, 8, 13, 64])
 @pytest.mark.parametrize("n", [1, 7, 8, 9, 256 * 5 + 3, 65536 + 8])
 def test_dequant_reduce_i4_vs_oracle(zpp, P, n):
     block = 256
@@ -649,7 +649,8 @@ def run_receive_pass_il(zpp, quants, n, grad_block, block, scale_out, state, sec
     (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
     (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
     (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
-    (16, 256 * 17 + 100, 128, 512, True), (8, 192 * 37 + 5, 192, 320, True)])
+    (16, 256 * 17 + 100, 128, 512, True), (8, 192 * 37 + 5, 192, 320, True),
+    (13, 256 * 9 + 81, 256, 256, True)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_pass_interleaved_equals_separate(zpp, P, n, grad_block, block, secondary,
                                                   regime):
@@ -732,7 +733,7 @@ def run_reduce_il(zpp, quants, n, block, scale_out, pad_out=0, pad_codes=0):
 @pytest.mark.parametrize("P,n,block", [
     (1, 1, 256), (2, 7, 64), (8, 9, 256), (3, 256 * 5 + 3, 128), (8, 65536 + 8, 256),
     (8, 100001, 1024), (64, 256 * 5 + 3, 256), (5, 4096 * 3 + 500, 4096), (16, 512 * 9, 64),
-    (8, 320 * 9 + 81, 320), (3, 192 * 5 + 3, 192)])
+    (8, 320 * 9 + 81, 320), (3, 192 * 5 + 3, 192), (13, 256 * 7 + 5, 256)])
 def test_dequant_reduce_interleaved_vs_oracle(zpp, P, n, block):
     """The dequant-reduce from one interleaved receive buffer against the
     oracle's reduction of the same P copies (separate arrays), bit for bit."""
