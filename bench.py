@@ -61,6 +61,9 @@ def parse():
                     help="consecutive steps the CPU oracle is timed over")
     ap.add_argument("--cpu-other", type=int, default=1,
                     help="also time the CPU oracle at the other workloads (1) or not (0)")
+    ap.add_argument("--sustain-s", type=float, default=10.0,
+                    help="seconds of back-to-back headline steps after the timed ones, reported "
+                         "as `sustained` (0 = skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters, if present")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -431,6 +434,29 @@ def cpu_baseline_others(skip):
     return out
 
 
+def sustain(pipe, step_bytes, seconds, chunk=50):
+    """The headline path (one stream, in order) run back to back for about
+    `seconds` of wall time, synchronised every `chunk` steps to read the
+    clock: the rate the GPU holds over many seconds, not only over the timed
+    steps."""
+    import torch
+    pipe.fused, pipe.sync, pipe.overlap, pipe.timing, pipe.streams = False, "event", True, None, 1
+    torch.cuda.synchronize()
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        for _ in range(chunk):
+            pipe.step()
+        steps += chunk
+        pipe.wait()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    gbps = step_bytes * steps / el / 1e9
+    return {"seconds": round(el, 2), "steps": steps, "ms_per_step": round(el * 1e3 / steps, 4),
+            "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+
+
 def gpu_clock_state():
     """Clock policy of GPU 0 as amd-smi reports it (graphics clock range and
     whether it is locked, HBM clock) and its market name, or None.  Called before this process
@@ -532,6 +558,7 @@ def main():
     # fix), the Adam launches timed inside its K timed steps; then the same
     # kernels on three streams ordered by events
     ms_per_step, times, kb, step_bytes, live_times = run(False, "event", True, live={"adam"})
+    sustained = sustain(pipe, step_bytes, args.sustain_s) if args.sustain_s > 0 else None
     three_ms = run(False, "event", False, overlap=True, streams=3)[0]
     fused_ms, fused_times, fused_kb, fused_step_bytes = run(True, "event", True)
     # the refresh and its quantization as one pass (zpp_refresh_quantize_i8)
@@ -598,6 +625,7 @@ def main():
         "ms_per_step": round(ms_per_step, 4),
         "ms_per_step_three_streams": {"overlap": round(three_ms, 4),
                                       "without_overlap": sync_ab["event"]},
+        "sustained": sustained,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

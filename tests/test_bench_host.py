@@ -94,3 +94,25 @@ def test_cpu_baseline_other_workloads(bench, monkeypatch):
     assert legs["one_thread"]["cores"] == 1 and legs["all_cores"]["cores"] == 2
     assert "2 step(s)" in legs["all_cores"]["sample"]
     assert all(leg["value"] > 0 and leg["unit"] == "GB/s" for leg in legs.values())
+
+
+def test_sustain_runs_whole_chunks_for_the_asked_time(bench, monkeypatch):
+    class FakePipe:
+        steps = 0
+
+        def step(self):
+            FakePipe.steps += 1
+
+        def wait(self):
+            pass
+
+    import torch
+    monkeypatch.setattr(torch.cuda, "synchronize", lambda: None)
+    clock = iter(range(0, 1000))
+    monkeypatch.setattr(bench.time, "perf_counter", lambda: float(next(clock)))
+    pipe = FakePipe()
+    rec = bench.sustain(pipe, 1000.0, 3.0, chunk=5)
+    # the clock advances one second per read: start, then one read per chunk
+    assert rec["steps"] == 15 and FakePipe.steps == 15 and rec["seconds"] == 3.0
+    assert rec["GB/s"] == round(1000.0 * 15 / 3.0 / 1e9, 1)
+    assert pipe.streams == 1 and pipe.fused is False and pipe.sync == "event"
