@@ -119,16 +119,19 @@ def measured_traffic(path, workload, kernel, sources):
 
 
 def kernel_table(kb, times, copy_gbps=None):
-    """Per kernel: algorithmic bytes, launch durations, GB/s, the fraction of
-    the HBM peak and, given the copy ceiling measured in the same run, the
-    fraction of that."""
+    """Per kernel: algorithmic bytes, launch durations (mean, median, min),
+    GB/s at the median duration (one launch delayed by the host, e.g. a
+    descheduled thread while the stream had run dry, moves the mean but not
+    the median), the fraction of the HBM peak and, given the copy ceiling
+    measured in the same run, the fraction of that."""
     out = {}
     for k in kb:
         ts = sorted(times[k])
         mean = sum(ts) / len(ts)
-        gbps = kb[k] / (mean * 1e-3) / 1e9
+        med = ts[len(ts) // 2]
+        gbps = kb[k] / (med * 1e-3) / 1e9
         out[k] = {"bytes": kb[k], "mean_us": round(mean * 1e3, 2),
-                  "median_us": round(ts[len(ts) // 2] * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
+                  "median_us": round(med * 1e3, 2), "min_us": round(ts[0] * 1e3, 2),
                   "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
         if copy_gbps:
             out[k]["frac_of_copy_ceiling"] = round(gbps / copy_gbps, 4)
@@ -269,8 +272,9 @@ def ceilings(reps=20):
     shapes that stream fastest): read-only, write-only and copy; beside
     them the runtime's device-to-device memcpy and this library's refresh
     kernel (a bf16 copy) on the same 1 GiB.  GB/s counts bytes read plus
-    bytes written.  The kernels of the path all read and write, so the copy
-    is the ceiling they are compared with (frac_of_copy_ceiling)."""
+    bytes written, at the median of `reps` launches.  The kernels of the
+    path all read and write, so the copy is the ceiling they are compared
+    with (frac_of_copy_ceiling)."""
     import torch
     from paper_2407_01614_amd import zpp
     if not os.path.exists(CEILING_LIB):
@@ -310,13 +314,84 @@ def ceilings(reps=20):
             b.record(stream)
             evs.append((a, b))
         torch.cuda.synchronize()
-        mean = sum(a.elapsed_ms(b) for a, b in evs) / reps
-        gbps = moved / (mean * 1e-3) / 1e9
+        med = sorted(a.elapsed_ms(b) for a, b in evs)[reps // 2]
+        gbps = moved / (med * 1e-3) / 1e9
         res[name] = {"GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
     assert int(sink.item()) == 0
     del src, dst, sink
     res["bytes"] = "1 GiB read and/or 1 GiB written; GB/s = bytes read + bytes written"
     return res
+
+
+def patterns(wl, reps=20):
+    """The access patterns of the Adam step, the dequant-gather and the int8
+    quantizer at this workload's sizes (include/zpp_ceiling.h: the same
+    loads and stores in the same lane layout, launch shape and residency,
+    the arithmetic replaced by an xor), each on buffers of its own, timed
+    with events like the ceilings (median of `reps` launches).  A kernel's
+    `frac_of_pattern` is its GB/s over its pattern's: 1 or more means its
+    arithmetic costs nothing beyond its memory traffic."""
+    import torch
+    from paper_2407_01614_amd import zpp
+    from paper_2407_01614_amd.workloads import BYTES_ADAM, bytes_gather, bytes_quant
+    lib = ctypes.CDLL(CEILING_LIB)
+    for fn in ("zppc_adam_pattern", "zppc_gather_pattern", "zppc_quant_pattern"):
+        getattr(lib, fn).restype = ctypes.c_int
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(zpp.stream_handle(stream))
+    vp = lambda t: ctypes.c_void_p(t.data_ptr())
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError("access-pattern launch failed: hipError %d" % rc)
+
+    def timed(fn):
+        fn()
+        evs = []
+        for _ in range(reps):
+            a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return sorted(a.elapsed_ms(b) for a, b in evs)[reps // 2]
+
+    res = {}
+    B = wl.block
+    # Adam: n rounded down to whole 256-element tiles
+    n = wl.n // 256 * 256
+    p, m, v, g = (torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(4))
+    out = torch.empty(n, dtype=torch.int16, device="cuda")
+    ms = timed(lambda: check(lib.zppc_adam_pattern(vp(p), vp(m), vp(v), vp(g), vp(out),
+                                                   ctypes.c_size_t(n), sh)))
+    res["adam"] = (n, BYTES_ADAM * n, ms)
+    del p, m, v, g, out
+    # the gather: the layer's N codes (whole 512-element rows) as one array
+    N = wl.layer_elems // 512 * 512
+    codes = torch.empty(N, dtype=torch.int8, device="cuda")
+    scales = torch.ones(N // B, dtype=torch.float32, device="cuda")
+    out = torch.empty(N, dtype=torch.int16, device="cuda")
+    ms = timed(lambda: check(lib.zppc_gather_pattern(vp(codes), vp(scales), vp(out),
+                                                     ctypes.c_size_t(N), sh)))
+    res["gather"] = (N, bytes_gather(N, 1, N, B), ms)
+    del codes, scales, out
+    # the quantizer: n rounded down to whole workgroups of 16 blocks
+    nq = wl.n // 4096 * 4096
+    src = torch.empty(nq, dtype=torch.int16, device="cuda")
+    codes = torch.empty(nq, dtype=torch.int8, device="cuda")
+    scales = torch.empty(nq // B, dtype=torch.float32, device="cuda")
+    ms = timed(lambda: check(lib.zppc_quant_pattern(vp(src), vp(codes), vp(scales),
+                                                    ctypes.c_size_t(nq), sh)))
+    res["quant"] = (nq, bytes_quant(nq, B), ms)
+    del src, codes, scales
+    torch.cuda.empty_cache()
+    out = {}
+    for k, (elems, nbytes, ms) in res.items():
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        out[k] = {"elements": elems, "bytes": nbytes, "median_us": round(ms * 1e3, 2),
+                  "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    return out
 
 
 def _chunks(n, parts, align):
@@ -570,6 +645,7 @@ def main():
         sync_ab[mode] = round(run(False, mode, False, overlap=False, streams=3)[0], 4)
     ceil = ceilings()
     copy_gbps = ceil["copy"]["GB/s"]
+    pats = patterns(wl) if wl.block == 256 else None
     torch_ctx = torch_adamw_context(wl, args.steps)
     # the whole iteration seen by the rank with qgZ: the int4 quantization of
     # its gradient into its send buffer (the send), the receive of 8 int4
@@ -604,6 +680,9 @@ def main():
            "dequant_reduce_i4_interleaved": qgz_kernels["reduce_i4"]}
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = kernel_table(kb, times, copy_gbps)
+    for k in ("adam", "gather", "quant"):
+        if pats and k in kernels:
+            kernels[k]["frac_of_pattern"] = round(kernels[k]["GB/s"] / pats[k]["GB/s"], 4)
     fused_kernels = kernel_table(fused_kb, fused_times, copy_gbps)
     fused_gbps = fused_step_bytes / (fused_ms * 1e-3) / 1e9
     sr_us = kernels["adam"]["mean_us"] + kernels["refresh"]["mean_us"]
@@ -661,6 +740,7 @@ def main():
             "kernels": kernel_table(fc_kb, fc_times, copy_gbps)},
         "sync_ab_ms_per_step": sync_ab,
         "ceilings": ceil,
+        "access_patterns": pats,
         "torch_fused_adamw_context": dict(
             torch_ctx, speedup_of_partition_step=round(
                 torch_ctx["ms_per_step"] / (kernels["adam"]["mean_us"] * 1e-3), 3)),

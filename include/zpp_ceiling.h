@@ -14,6 +14,23 @@
  *   zppc_copy_stream   one-wave workgroups, one 16-byte load and store per
  *                      lane, residency left to the hardware.
  *
+ * Beside them, the access patterns of three partition-path kernels with
+ * their arithmetic taken out: the same loads and stores in the same lane
+ * layout, workgroup shape, one-shot grid and residency cap, each loaded word
+ * folded by one xor (what is stored is not meaningful):
+ *   zppc_adam_pattern   the Adam step: per element 16 bytes read (p, m, v, g)
+ *                       and 14 written (p, m, v in place, a bf16); n a
+ *                       multiple of 256;
+ *   zppc_gather_pattern the dequant-gather row kernel for blocks of 256:
+ *                       n int8 codes and n/256 fp32 scales read, n bf16
+ *                       written; n a multiple of 512;
+ *   zppc_quant_pattern  the int8 quantizer for blocks of 256: n bf16 read,
+ *                       n int8 codes and n/256 fp32 scales written; n a
+ *                       multiple of 4096.
+ * Their pointers are device pointers aligned to their element vectors (16
+ * bytes for fp32 and bf16 arrays read or written 16 bytes per lane, 8 for
+ * codes and the bf16 output of the Adam pattern, 4 for scales).
+ *
  * Pointers are device pointers owned by the caller, 16-byte aligned; `bytes`
  * is a non-zero multiple of 4096.  The read stream folds what it reads into
  * one word per workgroup and stores it to sink[0] only when that word equals
@@ -41,6 +58,12 @@ extern "C" {
 ZPPC_API int zppc_read_stream(const void *src, size_t bytes, uint32_t *sink, hipStream_t stream);
 ZPPC_API int zppc_write_stream(void *dst, size_t bytes, uint32_t pattern, hipStream_t stream);
 ZPPC_API int zppc_copy_stream(void *dst, const void *src, size_t bytes, hipStream_t stream);
+ZPPC_API int zppc_adam_pattern(float *p, float *m, float *v, const float *g, uint16_t *out,
+                               size_t n, hipStream_t stream);
+ZPPC_API int zppc_gather_pattern(const int8_t *codes, const float *scales, uint16_t *out,
+                                 size_t n, hipStream_t stream);
+ZPPC_API int zppc_quant_pattern(const uint16_t *src, int8_t *codes, float *scales, size_t n,
+                                hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -485,7 +485,8 @@ def test_ceiling_library_exports_and_rejects():
         from paper_2407_01614_amd import build
         build.build_ceiling()
     decl = set(re.findall(r"ZPPC_API\s+int\s+(zppc_\w+)\s*\(", open(CEILING_HEADER).read()))
-    assert decl == {"zppc_read_stream", "zppc_write_stream", "zppc_copy_stream"}
+    assert decl == {"zppc_read_stream", "zppc_write_stream", "zppc_copy_stream",
+                    "zppc_adam_pattern", "zppc_gather_pattern", "zppc_quant_pattern"}
     out = subprocess.run(["nm", "-D", "--defined-only", CEILING_LIB], capture_output=True,
                          text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -504,3 +505,19 @@ def test_ceiling_library_exports_and_rejects():
                                  None) == EINVAL
     assert lib.zppc_copy_stream(ctypes.c_void_p(A), ctypes.c_void_p(A + 4096), big, None) == EINVAL
     assert lib.zppc_copy_stream(ctypes.c_void_p(A), None, big, None) == EINVAL
+    P = lambda off=0: ctypes.c_void_p(A + off)
+    n = ctypes.c_size_t(1 << 20)
+    # the access patterns: sizes that are not whole tiles, misaligned or null
+    # pointers
+    assert lib.zppc_adam_pattern(P(), P(), P(), P(), P(), ctypes.c_size_t(1000), None) == EINVAL
+    assert lib.zppc_adam_pattern(P(), P(8), P(), P(), P(), n, None) == EINVAL
+    assert lib.zppc_adam_pattern(P(), P(), P(), P(), P(4), n, None) == EINVAL
+    assert lib.zppc_adam_pattern(P(), P(), None, P(), P(), n, None) == EINVAL
+    assert lib.zppc_gather_pattern(P(), P(), P(), ctypes.c_size_t(256), None) == EINVAL
+    assert lib.zppc_gather_pattern(P(4), P(), P(), n, None) == EINVAL
+    assert lib.zppc_gather_pattern(P(), P(2), P(), n, None) == EINVAL
+    assert lib.zppc_gather_pattern(P(), P(), P(8), n, None) == EINVAL
+    assert lib.zppc_quant_pattern(P(), P(), P(), ctypes.c_size_t(2048), None) == EINVAL
+    assert lib.zppc_quant_pattern(P(8), P(), P(), n, None) == EINVAL
+    assert lib.zppc_quant_pattern(P(), P(4), P(), n, None) == EINVAL
+    assert lib.zppc_quant_pattern(P(), P(), None, n, None) == EINVAL

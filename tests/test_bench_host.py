@@ -55,10 +55,11 @@ def test_measured_traffic_only_for_current_sources(bench, tmp_path):
 
 def test_kernel_table(bench):
     kb = {"adam": 6.0e9, "gather": 1.0e9}
-    times = {"adam": [1.0, 0.9, 1.1], "gather": [0.2, 0.2]}  # ms per launch
+    times = {"adam": [1.0, 0.9, 1.1, 19.0, 1.0], "gather": [0.2, 0.2]}  # ms per launch
     t = bench.kernel_table(kb, times)
-    assert t["adam"]["mean_us"] == 1000.0 and t["adam"]["median_us"] == 1000.0
+    assert t["adam"]["mean_us"] == 4600.0 and t["adam"]["median_us"] == 1000.0
     assert t["adam"]["min_us"] == 900.0
+    # GB/s at the median: the one delayed launch does not move it
     assert t["adam"]["GB/s"] == 6000.0 and t["adam"]["frac_of_peak"] == 0.75
     assert t["gather"]["GB/s"] == 5000.0 and t["gather"]["bytes"] == 1.0e9
 
