@@ -166,8 +166,9 @@ def forward_gather_measure(wl, reps):
     slices by the same dequant-gather kernel over P shards (64 at most per
     call; a larger world takes several calls, each writing its part of the
     layer).  The exchange that brings the slices from the other nodes needs
-    more GPUs.  Timed with events over `reps` launches; the quantization of
-    one slice, what each rank does before the exchange, is timed too."""
+    more GPUs.  Timed with events over `reps` launches (GB/s at the median);
+    the quantization of one slice, what each rank does before the exchange,
+    is timed too."""
     import torch
     from paper_2407_01614_amd import zpp
     from paper_2407_01614_amd.workloads import bytes_gather, bytes_quant
@@ -213,14 +214,16 @@ def forward_gather_measure(wl, reps):
         b.record(stream)
         evs.append((a, b))
     torch.cuda.synchronize()
-    mean = sum(a.elapsed_ms(b) for a, b in evs) / len(evs)
+    ts = sorted(a.elapsed_ms(b) for a, b in evs)
+    mean, med = sum(ts) / len(ts), ts[len(ts) // 2]
     qmean = sum(a.elapsed_ms(b) for a, b in qevs) / len(qevs)
     nbytes = bytes_gather(s, P, N, B)
-    gbps = nbytes / (mean * 1e-3) / 1e9
+    gbps = nbytes / (med * 1e-3) / 1e9
     del w, codes, scales, out
     return {"ranks": P, "slice_elems": s, "layer_elems": N, "launches_per_gather": -(-P // G),
             "codes": "each slice int8-quantized by the library from bf16 weights ~ N(0, 0.02)",
-            "bytes": nbytes, "mean_us": round(mean * 1e3, 2), "GB/s": round(gbps, 1),
+            "bytes": nbytes, "mean_us": round(mean * 1e3, 2), "median_us": round(med * 1e3, 2),
+            "GB/s": round(gbps, 1),
             "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4),
             "quantize_one_slice": {"bytes": bytes_quant(s, B), "mean_us": round(qmean * 1e3, 2)}}
 
