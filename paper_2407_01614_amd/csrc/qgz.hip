@@ -18,12 +18,14 @@
 // buffer (layout in zpp_i4grad.h): the gradient source of the receive
 // kernels forms each float4, so the bits are those of the separate arrays.
 //
-// Blocks may be any multiple of 64 up to 4096; the quantizer takes one wave
-// per block for those that are not powers of two.
+// Blocks may be any multiple of 64 up to 4096; for those that are not powers
+// of two the quantizer takes several whole blocks per wave at a time, the
+// block absmax folded in LDS.
 //
 // Both kernels keep every wave's loads and stores contiguous: on this GPU,
 // non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
 // lane at a 32- or 64-byte stride) run two to three times slower.
+#include "zpp_chunk.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"
 #include "zpp_launch.h"
@@ -179,58 +181,114 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
     }
 }
 
-// Vector path for a block B = 64 b that is not a power of two: one wave per
-// block; lane l holds the groups of 4 values [k B + 256 g + 4 l, +4) for
-// g < B / 256 (lanes past the block's end hold nothing), so the absmax is a
-// reduction over the whole wave; each group's 4 codes are one 16-bit store.
-__global__ __launch_bounds__(kQgzThreads) void quant_i4_any_kernel(
-    const float *__restrict__ src, size_t n, uint32_t block, uint8_t *__restrict__ codes,
-    float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
-    constexpr int kMaxG = 4096 / 256;  // groups per lane of the largest block
-    const size_t nblocks = (n + block - 1) / block;
-    const int lane = threadIdx.x & (kWave - 1);
-    const size_t wave0 = (size_t)blockIdx.x * (kQgzThreads / kWave) + threadIdx.x / kWave;
-    const size_t nwaves = (size_t)gridDim.x * (kQgzThreads / kWave);
-    for (size_t k = wave0; k < nblocks; k += nwaves) {
-        const size_t lo = k * block;
-        f32x4 x[kMaxG];
-        uint32_t mx = 0;
+// Vector path for a block B = 64 b that is not a power of two: a one-wave
+// workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
+// groups of 4 values v 64 + l of the chunk for v < V (each wave load 1 KiB
+// contiguous).  Each lane folds each group's absmax into its block's word in
+// LDS (an LDS max); lane k < K then derives block k's parameters once,
+// stores its scale and leaves the parameters in LDS, from which every lane
+// quantizes its groups, each group's 4 codes one 16-bit store.  MAXV slots
+// per lane at most: 8 for blocks of up to 2048 values, 16 (4096 / 4 = 1024
+// groups fit 64 x 16) for larger ones, whose registers then allow fewer
+// waves per SIMD.
+template <int kMaxI4Slots>
+__global__ __launch_bounds__(kWave) void quant_i4_multi_kernel(
+    const float *__restrict__ src, size_t n, BlockDiv blk, uint32_t K, uint32_t V,
+    uint8_t *__restrict__ codes, float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
+    __shared__ uint32_t bmax[64];
+    __shared__ I4Quant bq[64];
+    const uint32_t lane = threadIdx.x;
+    const uint32_t B = blk.block;
+    const size_t nblocks = (n + B - 1) / B;
+    for (size_t k0 = (size_t)blockIdx.x * K; k0 < nblocks; k0 += (size_t)gridDim.x * K) {
+        const uint32_t kc = (uint32_t)(nblocks - k0 < K ? nblocks - k0 : K);
+        const size_t base = k0 * B;
+        const size_t end = (base + (size_t)kc * B < n) ? base + (size_t)kc * B : n;
+        if (lane < kc)
+            bmax[lane] = 0u;
+        __syncthreads();
+        // every load of the chunk first, then the LDS maxima (a max in the
+        // same pass would wait for each load in turn)
+        f32x4 x[kMaxI4Slots];
+        uint32_t kl[kMaxI4Slots];
+        if (end == base + (size_t)K * B) {
+            // a whole chunk: every group complete, one predicated load each
+            const uint32_t ngrp = K * (B / 4);
 #pragma unroll
-        for (int g = 0; g < kMaxG; ++g) {
-            const uint32_t off = (uint32_t)g * 256 + (uint32_t)lane * 4;
-            const size_t i = lo + off;
-            x[g] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if (off < block && i + 4 <= n) {
-                x[g] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
-            } else if (off < block) {
-                float h[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    h[e] = (i + e < n) ? src[i + e] : 0.0f;
-                x[g] = f32x4{h[0], h[1], h[2], h[3]};
+            for (int v = 0; v < kMaxI4Slots; ++v) {
+                x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                const uint32_t j = (uint32_t)v * kWave + lane;
+                if ((uint32_t)v < V && j < ngrp)
+                    x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + base + (size_t)j * 4));
             }
-            mx = max(mx, abs_bits_max4(x[g]));
+        } else {
+#pragma unroll
+        for (int v = 0; v < kMaxI4Slots; ++v) {
+            x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if ((uint32_t)v < V) {
+                const size_t i = base + ((size_t)v * kWave + lane) * 4;
+                if (i + 4 <= end) {
+                    x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
+                } else if (i < end) {
+                    float h[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        h[e] = (i + e < end) ? src[i + e] : 0.0f;
+                    x[v] = f32x4{h[0], h[1], h[2], h[3]};
+                }
+            }
+        }
         }
 #pragma unroll
-        for (int off = kWave / 2; off >= 1; off >>= 1)
-            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-        const I4Quant q = i4_params(mx);
+        for (int v = 0; v < kMaxI4Slots; ++v)
+            kl[v] = 0u;
+        if (K == 1) {
+            // one block per chunk: its absmax is a reduction over the wave
+            uint32_t mx = 0;
 #pragma unroll
-        for (int g = 0; g < kMaxG; ++g) {
-            const uint32_t off = (uint32_t)g * 256 + (uint32_t)lane * 4;
-            const size_t i = lo + off;
-            if (off < block && i < n) {
-                const uint32_t h = i4_half(x[g], q);
-                const size_t byte0 = i4_out_byte_any(i, k, block, q_src, num_src);
-                // the second byte holds elements i + 2 and i + 3
-                if (i + 2 < n)
-                    st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
-                else
-                    codes[byte0] = (uint8_t)h;
+            for (int v = 0; v < kMaxI4Slots; ++v)
+                mx = max(mx, abs_bits_max4(x[v]));
+#pragma unroll
+            for (int off = kWave / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+            if (lane == 0) {
+                const I4Quant q = i4_params(mx);
+                bq[0] = q;
+                scales[k0 * num_src + q_src] = q.scale;
+            }
+        } else {
+#pragma unroll
+            for (int v = 0; v < kMaxI4Slots; ++v) {
+                const size_t i = base + ((size_t)v * kWave + lane) * 4;
+                if ((uint32_t)v < V && i < end) {
+                    kl[v] = (uint32_t)(block_of(blk, i) - k0);
+                    atomicMax(&bmax[kl[v]], abs_bits_max4(x[v]));
+                }
+            }
+            __syncthreads();
+            if (lane < kc) {
+                const I4Quant q = i4_params(bmax[lane]);
+                bq[lane] = q;
+                scales[(k0 + lane) * num_src + q_src] = q.scale;
             }
         }
-        if (lane == 0)
-            scales[k * num_src + q_src] = q.scale;
+        __syncthreads();
+#pragma unroll
+        for (int v = 0; v < kMaxI4Slots; ++v) {
+            if ((uint32_t)v >= V)
+                continue;
+            const size_t i = base + ((size_t)v * kWave + lane) * 4;
+            if (i >= end)
+                continue;
+            const uint32_t h = i4_half(x[v], bq[kl[v]]);
+            const size_t byte0 = i4_out_byte_any(i, k0 + kl[v], B, q_src, num_src);
+            // the second byte holds elements i + 2 and i + 3
+            if (i + 2 < n)
+                st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
+            else
+                codes[byte0] = (uint8_t)h;
+        }
+        __syncthreads();  // bmax and bq are rewritten for the next chunk
     }
 }
 
@@ -436,12 +494,19 @@ hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uin
         case 2048: launch_quant_i4_b<2048>(src, n, codes, scales, source, num_src, stream); break;
         case 4096: launch_quant_i4_b<4096>(src, n, codes, scales, source, num_src, stream); break;
         default: {
+            const bool small = block / 4 <= 64 * 8;
+            const ChunkShape sh = chunk_shape(block / 4, small ? 8 : 16);
             const size_t nblocks = (n + block - 1) / block;
-            const size_t waves = kQgzThreads / kWave;
-            const size_t need = (nblocks + waves - 1) / waves;
+            const size_t need = (nblocks + sh.K - 1) / sh.K;
             const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
-            hipLaunchKernelGGL(quant_i4_any_kernel, dim3(grid), dim3(kQgzThreads), 0, stream, src,
-                               n, block, codes, scales, source, num_src);
+            if (small)
+                hipLaunchKernelGGL(quant_i4_multi_kernel<8>, dim3(grid), dim3(kWave), 0, stream,
+                                   src, n, make_block_div(block), sh.K, sh.V, codes, scales,
+                                   source, num_src);
+            else
+                hipLaunchKernelGGL(quant_i4_multi_kernel<16>, dim3(grid), dim3(kWave), 0, stream,
+                                   src, n, make_block_div(block), sh.K, sh.V, codes, scales,
+                                   source, num_src);
         }
         }
     } else {

@@ -10,12 +10,15 @@
 // traffic and no float compares are needed.  Every lane then derives the
 // block's scale and inverse itself (two correctly rounded divisions per 8
 // elements) and writes its 8 codes as one 8-byte store.  Blocks that are
-// not powers of two (any multiple of 64 up to 4096) take one wave per block.
+// not powers of two (any multiple of 64 up to 4096) take a one-wave kernel
+// that works on several whole blocks at a time, the block absmax folded in
+// LDS.
 //
 // The same kernels can also store the bf16 they read to a second array:
 // the secondary refresh and its quantization in one pass (2 B read, 2 B +
 // 1 B + 4/B B written per element, against 4 + 3 + 4/B B for the two
 // calls).
+#include "zpp_chunk.h"
 #include "zpp_device.h"
 #include "zpp_launch.h"
 #include "zpp_quant.h"
@@ -122,60 +125,121 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
     }
 }
 
-// Vector path for a block B = 64 b that is not a power of two: one wave per
-// block; lane l holds the 8 elements [k B + 8 (64 v + l), +8) for v < B / 512
-// (lanes past the block's end hold nothing), so the absmax is a reduction
-// over the whole wave.
+// Vector path for a block B = 64 b that is not a power of two: a one-wave
+// workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
+// 8-element vectors v 64 + l of the chunk for v < V (each wave load 1 KiB
+// contiguous, as in the power-of-two kernel).  Each lane folds each of its
+// vectors' absmax into its block's word in LDS (an LDS max); lane k < K then
+// derives block k's parameters once, stores its scale and leaves the
+// parameters in LDS, from which every lane quantizes its vectors.
+constexpr int kMaxQuantSlots = 8;  // 4096 / 8 = 512 vectors of a block fit 64 x 8
+
 template <bool COPY>
-__global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
-    const uint16_t *__restrict__ src, size_t n, uint32_t block, int8_t *__restrict__ codes,
-    float *__restrict__ scales, uint16_t *__restrict__ copy) {
-    constexpr int kMaxV = 4096 / (8 * kWave);  // vectors per lane of the largest block
-    const size_t nblocks = (n + block - 1) / block;
-    const int lane = threadIdx.x & (kWave - 1);
-    const size_t wave0 = (size_t)blockIdx.x * (kQuantThreads / kWave) + threadIdx.x / kWave;
-    const size_t nwaves = (size_t)gridDim.x * (kQuantThreads / kWave);
-    for (size_t k = wave0; k < nblocks; k += nwaves) {
-        const size_t lo = k * block;
-        u32x4 x[kMaxV];
-        u16x2 m2 = {0, 0};
+__global__ __launch_bounds__(kWave) void quant_multi_kernel(
+    const uint16_t *__restrict__ src, size_t n, BlockDiv blk, uint32_t K, uint32_t V,
+    int8_t *__restrict__ codes, float *__restrict__ scales, uint16_t *__restrict__ copy) {
+    __shared__ uint32_t bmax[64];
+    __shared__ BlockQuant bq[64];
+    const uint32_t lane = threadIdx.x;
+    const size_t B = blk.block;
+    const size_t nblocks = (n + B - 1) / B;
+    for (size_t k0 = (size_t)blockIdx.x * K; k0 < nblocks; k0 += (size_t)gridDim.x * K) {
+        const uint32_t kc = (uint32_t)(nblocks - k0 < K ? nblocks - k0 : K);
+        const size_t base = k0 * B;
+        const size_t end = (base + kc * B < n) ? base + kc * B : n;
+        if (lane < kc)
+            bmax[lane] = 0u;
+        __syncthreads();
+        // every load of the chunk first, then the LDS maxima (a max in the
+        // same pass would wait for each load in turn)
+        u32x4 x[kMaxQuantSlots];
+        uint32_t kl[kMaxQuantSlots];
+        if (end == base + (size_t)K * B) {
+            // a whole chunk: every vector complete, one predicated load each
+            const uint32_t nvec = K * (uint32_t)(B / 8);
 #pragma unroll
-        for (int v = 0; v < kMaxV; ++v) {
-            const uint32_t off = (uint32_t)(v * kWave + lane) * 8;
-            const size_t i = lo + off;
-            x[v] = u32x4{0u, 0u, 0u, 0u};
-            if (off < block && i + 8 <= n) {
-                x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
-            } else if (off < block) {
-                uint32_t h[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    h[e] = (i + e < n) ? (uint32_t)src[i + e] : 0u;
-                x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                             h[6] | (h[7] << 16)};
+            for (int v = 0; v < kMaxQuantSlots; ++v) {
+                x[v] = u32x4{0u, 0u, 0u, 0u};
+                const uint32_t j = (uint32_t)v * kWave + lane;
+                if ((uint32_t)v < V && j < nvec)
+                    x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + base + (size_t)j * 8));
             }
-            m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
-                     __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
-                     __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
+        } else {
+#pragma unroll
+        for (int v = 0; v < kMaxQuantSlots; ++v) {
+            x[v] = u32x4{0u, 0u, 0u, 0u};
+            if ((uint32_t)v < V) {
+                const size_t i = base + ((size_t)v * kWave + lane) * 8;
+                if (i + 8 <= end) {
+                    x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
+                } else if (i < end) {
+                    uint32_t h[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        h[e] = (i + e < end) ? (uint32_t)src[i + e] : 0u;
+                    x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16),
+                                 h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+                }
+            }
         }
-        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+        }
 #pragma unroll
-        for (int off = kWave / 2; off >= 1; off >>= 1)
-            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-        const BlockQuant q = block_params(mx);
+        for (int v = 0; v < kMaxQuantSlots; ++v)
+            kl[v] = 0u;
+        if (K == 1) {
+            // one block per chunk: its absmax is a reduction over the wave
+            u16x2 m2 = {0, 0};
 #pragma unroll
-        for (int v = 0; v < kMaxV; ++v) {
-            const uint32_t off = (uint32_t)(v * kWave + lane) * 8;
-            const size_t i = lo + off;
+            for (int v = 0; v < kMaxQuantSlots; ++v)
+                m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
+                         __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
+                         __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
+            uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+            for (int off = kWave / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+            if (lane == 0) {
+                const BlockQuant q = block_params(mx);
+                bq[0] = q;
+                scales[k0] = q.scale;
+            }
+        } else {
+#pragma unroll
+            for (int v = 0; v < kMaxQuantSlots; ++v) {
+                const size_t i = base + ((size_t)v * kWave + lane) * 8;
+                if ((uint32_t)v < V && i < end) {
+                    kl[v] = (uint32_t)(block_of(blk, i) - k0);
+                    const u16x2 m2 = __builtin_elementwise_max(
+                        __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
+                        __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w)));
+                    atomicMax(&bmax[kl[v]], max((uint32_t)m2.x, (uint32_t)m2.y));
+                }
+            }
+            __syncthreads();
+            if (lane < kc) {
+                const BlockQuant q = block_params(bmax[lane]);
+                bq[lane] = q;
+                scales[k0 + lane] = q.scale;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int v = 0; v < kMaxQuantSlots; ++v) {
+            if ((uint32_t)v >= V)
+                continue;
+            const size_t i = base + ((size_t)v * kWave + lane) * 8;
+            if (i >= end)
+                continue;
+            const BlockQuant q = bq[kl[v]];
             u32x2 c;
             c.x = quant_word(x[v].x, x[v].y, q);
             c.y = quant_word(x[v].z, x[v].w, q);
-            if (off < block && i + 8 <= n) {
+            if (i + 8 <= end) {
                 st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
                 if (COPY)
                     st_nt(reinterpret_cast<u32x4 *>(copy + i), x[v]);
-            } else if (off < block) {
-                for (int e = 0; e < 8 && i + e < n; ++e) {
+            } else {
+                for (int e = 0; e < 8 && i + e < end; ++e) {
                     codes[i + e] =
                         (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
                     if (COPY)
@@ -183,8 +247,7 @@ __global__ __launch_bounds__(kQuantThreads) void quant_any_kernel(
                 }
             }
         }
-        if (lane == 0)
-            scales[k] = q.scale;
+        __syncthreads();  // bmax and bq are rewritten for the next chunk
     }
 }
 
@@ -242,12 +305,12 @@ void launch_vector(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
     case 2048: launch_vec<2048, COPY>(src, n, codes, scales, copy, stream); break;
     case 4096: launch_vec<4096, COPY>(src, n, codes, scales, copy, stream); break;
     default: {
+        const ChunkShape sh = chunk_shape(block / 8, kMaxQuantSlots);
         const size_t nblocks = (n + block - 1) / block;
-        constexpr size_t kWaves = kQuantThreads / kWave;
-        const size_t need = (nblocks + kWaves - 1) / kWaves;
+        const size_t need = (nblocks + sh.K - 1) / sh.K;
         const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
-        hipLaunchKernelGGL((quant_any_kernel<COPY>), dim3(grid), dim3(kQuantThreads), 0, stream,
-                           src, n, block, codes, scales, copy);
+        hipLaunchKernelGGL((quant_multi_kernel<COPY>), dim3(grid), dim3(kWave), 0, stream, src,
+                           n, make_block_div(block), sh.K, sh.V, codes, scales, copy);
     }
     }
 }

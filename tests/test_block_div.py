@@ -24,3 +24,16 @@ def test_block_index_is_exact(tmp_path):
     assert r.returncode == 0, " ".join(cmd) + "\n" + r.stderr
     r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0 and "block index ok" in r.stdout, r.stdout + r.stderr
+
+
+@pytest.mark.skipif(not os.path.exists(CLANGXX), reason="ROCm clang++ not found")
+def test_chunk_shapes_cover_every_element(tmp_path):
+    """The non-power-of-two quantizers' chunk shapes (csrc/zpp_chunk.h),
+    checked on the host by tests/chunk_shape_check.cpp."""
+    exe = str(tmp_path / "chunk_shape_check")
+    cmd = [CLANGXX, "-std=c++17", "-O2", "-I", os.path.join(ROOT, "paper_2407_01614_amd", "csrc"),
+           os.path.join(HERE, "chunk_shape_check.cpp"), "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, " ".join(cmd) + "\n" + r.stderr
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "chunk shapes ok" in r.stdout, r.stdout + r.stderr

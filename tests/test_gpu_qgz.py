@@ -46,7 +46,8 @@ def grads(n, cfg, rank=0, scale=1.0):
     return synth.gradients(n, cfg, rank) * np.float32(scale)
 
 
-@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 2048, 4032, 4096])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 960, 2048, 2112, 4032,
+                                   4096])
 @pytest.mark.parametrize("n", [1, 2, 7, 8, 9, 255, 256, 257, 256 * 9 + 81, 100001, 1 << 18])
 def test_quant_i4_vs_oracle(zpp, block, n):
     x = grads(n, 80, n + block)
