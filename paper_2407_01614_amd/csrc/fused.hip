@@ -16,7 +16,8 @@
 // updated weights stays in registers (two per 4 elements) until the block's
 // absmax is known; a 256-block is exactly one wave, so its absmax is a
 // six-step cross-lane reduction.  A block that is not a power of two (any
-// multiple of 64 up to 4096) takes one wave per block (fused_any_kernel).
+// multiple of 64 up to 4096) takes fused_multi_kernel: several whole blocks
+// per wave at a time, the block absmax folded in LDS.
 // Residency is capped at ZPP_FUSED_RESIDENCY
 // workgroups per CU, as for the optimizer step: 1031-1046 us with 12 resident
 // at the Llama-2-13B partition (9-20 within 1%), 1127-1145 us uncapped.  With
@@ -26,6 +27,7 @@
 // (ZPP_FUSED_RECV_IL_RESIDENCY): 1054 us with 14, 1062 with 16, 1075 with 12,
 // 1097 uncapped, against 1096 us from separate arrays in the same run.
 #include "zpp_adam.h"
+#include "zpp_chunk.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"
 #include "zpp_launch.h"
@@ -39,6 +41,16 @@
 #endif
 #ifndef ZPP_FUSED_RECV_IL_RESIDENCY
 #define ZPP_FUSED_RECV_IL_RESIDENCY 14
+#endif
+// The chunked kernel of blocks that are not powers of two keeps up to four
+// groups per lane in flight, so fewer of its workgroups share a CU: at the
+// Llama-2-13B partition, blocks of 192 / 320 / 960 / 2112 / 4032, 8 per CU
+// took 1162 / 1189 / 1178 / 1189 / 1286 us, 6 per CU 1200 / 1195 / 1185 /
+// 1180 / 1259, 12 per CU 1193 / 1228 / 1228 / 1220 / 1291, 4 per CU
+// 1313-1606; one wave per block (the kernel it replaced) 1424 / 1215 / 1231
+// / 1232 / 1284.
+#ifndef ZPP_FUSED_MULTI_RESIDENCY
+#define ZPP_FUSED_MULTI_RESIDENCY 8
 #endif
 #ifndef ZPP_FUSED_MAX_GRID
 #define ZPP_FUSED_MAX_GRID (1u << 30)
@@ -141,87 +153,183 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a, GS gs) {
     }
 }
 
-// A block B = 64 b that is not a power of two: one wave per block; lane l
-// holds the 4 elements [k B + 256 w + 4 l, +4) for w < B / 256 (lanes past
-// the block's end hold nothing), so the absmax is a reduction over the whole
-// wave.  Otherwise as fused_kernel, with the same results as the three
-// separate kernels.
-template <bool ADAMW, class GS>
-__global__ __launch_bounds__(kWave) void fused_any_kernel(FusedArgs a, GS gs, uint32_t block) {
-    constexpr int kMaxW = 4096 / 256;  // float4 groups per lane of the largest block
-    const int lane = threadIdx.x;
-    const size_t nblocks = (a.n + block - 1) / block;
-    for (size_t k = blockIdx.x; k < nblocks; k += gridDim.x) {
-        const size_t base = k * block;
-        u32x2 pk[kMaxW];
-        u16x2 m2 = {0, 0};
+// A block B = 64 b that is not a power of two: a wave takes K whole blocks at
+// a time (zpp_chunk.h), lane l holding the float4 groups v 64 + l of the
+// chunk for v < V, so every wave access of p, m, v and the gradient is
+// 1 KiB contiguous as in fused_kernel.  The loads of up to four groups per
+// lane are issued together; each group is updated and stored as in
+// fused_kernel and its bf16 kept in registers; the groups' absmax is folded per block in LDS (or
+// across the wave when one block fills the chunk), lane k < K derives block
+// k's parameters and scale once, and every lane then stores its codes.  The
+// results are those of the three separate kernels.
+constexpr int kFusedBatch = 4;  // float4 groups per lane whose loads are in flight at once
+
+template <bool ADAMW, class GS, int MAXV>
+__global__ __launch_bounds__(kWave) void fused_multi_kernel(FusedArgs a, GS gs, BlockDiv blk,
+                                                            uint32_t K, uint32_t V) {
+    __shared__ uint32_t bmax[64];
+    __shared__ BlockQuant bq[64];
+    const uint32_t lane = threadIdx.x;
+    const size_t B = blk.block;
+    const size_t nblocks = (a.n + B - 1) / B;
+    for (size_t k0 = (size_t)blockIdx.x * K; k0 < nblocks; k0 += (size_t)gridDim.x * K) {
+        const uint32_t kc = (uint32_t)(nblocks - k0 < K ? nblocks - k0 : K);
+        const size_t base = k0 * B;
+        const size_t end = (base + kc * B < a.n) ? base + kc * B : a.n;
+        if (lane < kc)
+            bmax[lane] = 0u;
+        __syncthreads();
+        u32x2 pk[MAXV];
+        if (end == base + (size_t)K * B) {
+            // a whole chunk: every group complete; the loads of up to
+            // kFusedBatch groups per lane in flight at once
+            const uint32_t ngrp = K * (uint32_t)(B / 4);
 #pragma unroll
-        for (int w = 0; w < kMaxW; ++w) {
-            const uint32_t off = (uint32_t)w * 256 + (uint32_t)lane * 4;
-            const size_t i = base + off;
-            pk[w] = u32x2{0u, 0u};
-            if (off < block && i + 4 <= a.n) {
-                f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
-                f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
-                f32x4 V = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
-                const f32x4 G = grad_load4(gs, i);
+            for (int v = 0; v < MAXV; ++v)
+                pk[v] = u32x2{0u, 0u};
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float p = P[e], m = M[e], v = V[e];
-                    adam_update<ADAMW>(p, m, v, G[e], a.c);
-                    P[e] = p;
-                    M[e] = m;
-                    V[e] = v;
-                }
-                st_nt(reinterpret_cast<f32x4 *>(a.p + i), P);
-                st_nt(reinterpret_cast<f32x4 *>(a.m + i), M);
-                st_nt(reinterpret_cast<f32x4 *>(a.v + i), V);
-                pk[w] = u32x2{pack_bf16x2(P.x, P.y), pack_bf16x2(P.z, P.w)};
-                st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk[w]);
-                if (a.secondary)
-                    st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk[w]);
-            } else if (off < block) {
-                // the partition's last elements: one by one
-                uint32_t h[4];
+            for (int b0 = 0; b0 < MAXV; b0 += kFusedBatch) {
+                if ((uint32_t)b0 >= V)
+                    break;
+                f32x4 P[kFusedBatch], M[kFusedBatch], Q[kFusedBatch], G[kFusedBatch];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    h[e] = 0u;
-                    if (i + e < a.n) {
-                        float p = a.p[i + e], m = a.m[i + e], v = a.v[i + e];
-                        adam_update<ADAMW>(p, m, v, grad_at(gs, i + e), a.c);
-                        a.p[i + e] = p;
-                        a.m[i + e] = m;
-                        a.v[i + e] = v;
-                        h[e] = bf16_rne_bits(p);
-                        a.primary[i + e] = (uint16_t)h[e];
-                        if (a.secondary)
-                            a.secondary[i + e] = (uint16_t)h[e];
+                for (int u = 0; u < kFusedBatch; ++u) {
+                    const uint32_t v = (uint32_t)(b0 + u), j = v * kWave + lane;
+                    if (v < V && j < ngrp) {
+                        const size_t i = base + (size_t)j * 4;
+                        P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
+                        M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
+                        Q[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
+                        G[u] = grad_load4(gs, i);
                     }
                 }
-                pk[w] = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+#pragma unroll
+                for (int u = 0; u < kFusedBatch; ++u) {
+                    const uint32_t v = (uint32_t)(b0 + u), j = v * kWave + lane;
+                    if (v < V && j < ngrp) {
+                        const size_t i = base + (size_t)j * 4;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            float p = P[u][e], m = M[u][e], q = Q[u][e];
+                            adam_update<ADAMW>(p, m, q, G[u][e], a.c);
+                            P[u][e] = p;
+                            M[u][e] = m;
+                            Q[u][e] = q;
+                        }
+                        st_nt(reinterpret_cast<f32x4 *>(a.p + i), P[u]);
+                        st_nt(reinterpret_cast<f32x4 *>(a.m + i), M[u]);
+                        st_nt(reinterpret_cast<f32x4 *>(a.v + i), Q[u]);
+                        pk[b0 + u] = u32x2{pack_bf16x2(P[u].x, P[u].y),
+                                           pack_bf16x2(P[u].z, P[u].w)};
+                        st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk[b0 + u]);
+                        if (a.secondary)
+                            st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk[b0 + u]);
+                    }
+                }
             }
-            m2 = __builtin_elementwise_max(
-                m2, __builtin_elementwise_max(absbits2(pk[w].x), absbits2(pk[w].y)));
+        } else {
+            // the partition's last chunk: complete groups as above, the last
+            // elements one by one
+#pragma unroll
+            for (int v = 0; v < MAXV; ++v) {
+                pk[v] = u32x2{0u, 0u};
+                const size_t i = base + ((size_t)v * kWave + lane) * 4;
+                if ((uint32_t)v >= V || i >= end)
+                    continue;
+                if (i + 4 <= end) {
+                    f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
+                    f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
+                    f32x4 Q = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
+                    const f32x4 G = grad_load4(gs, i);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float p = P[e], m = M[e], q = Q[e];
+                        adam_update<ADAMW>(p, m, q, G[e], a.c);
+                        P[e] = p;
+                        M[e] = m;
+                        Q[e] = q;
+                    }
+                    st_nt(reinterpret_cast<f32x4 *>(a.p + i), P);
+                    st_nt(reinterpret_cast<f32x4 *>(a.m + i), M);
+                    st_nt(reinterpret_cast<f32x4 *>(a.v + i), Q);
+                    pk[v] = u32x2{pack_bf16x2(P.x, P.y), pack_bf16x2(P.z, P.w)};
+                    st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk[v]);
+                    if (a.secondary)
+                        st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk[v]);
+                } else {
+                    uint32_t h[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        h[e] = 0u;
+                        if (i + e < end) {
+                            float p = a.p[i + e], m = a.m[i + e], q = a.v[i + e];
+                            adam_update<ADAMW>(p, m, q, grad_at(gs, i + e), a.c);
+                            a.p[i + e] = p;
+                            a.m[i + e] = m;
+                            a.v[i + e] = q;
+                            h[e] = bf16_rne_bits(p);
+                            a.primary[i + e] = (uint16_t)h[e];
+                            if (a.secondary)
+                                a.secondary[i + e] = (uint16_t)h[e];
+                        }
+                    }
+                    pk[v] = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+                }
+            }
         }
-        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+        uint32_t kl[MAXV];
 #pragma unroll
-        for (int off = kWave / 2; off >= 1; off >>= 1)
-            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-        const BlockQuant q = block_params(mx);
+        for (int v = 0; v < MAXV; ++v)
+            kl[v] = 0u;
+        if (K == 1) {
+            // one block per chunk: its absmax is a reduction over the wave
+            u16x2 m2 = {0, 0};
 #pragma unroll
-        for (int w = 0; w < kMaxW; ++w) {
-            const uint32_t off = (uint32_t)w * 256 + (uint32_t)lane * 4;
-            const size_t i = base + off;
-            const uint32_t c4 = quant_word(pk[w].x, pk[w].y, q);
-            if (off < block && i + 4 <= a.n) {
+            for (int v = 0; v < MAXV; ++v)
+                m2 = __builtin_elementwise_max(
+                    m2, __builtin_elementwise_max(absbits2(pk[v].x), absbits2(pk[v].y)));
+            uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+#pragma unroll
+            for (int off = kWave / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+            if (lane == 0) {
+                const BlockQuant q = block_params(mx);
+                bq[0] = q;
+                a.scales[k0] = q.scale;
+            }
+        } else {
+#pragma unroll
+            for (int v = 0; v < MAXV; ++v) {
+                const size_t i = base + ((size_t)v * kWave + lane) * 4;
+                if ((uint32_t)v < V && i < end) {
+                    kl[v] = (uint32_t)(block_of(blk, i) - k0);
+                    const u16x2 m2 =
+                        __builtin_elementwise_max(absbits2(pk[v].x), absbits2(pk[v].y));
+                    atomicMax(&bmax[kl[v]], max((uint32_t)m2.x, (uint32_t)m2.y));
+                }
+            }
+            __syncthreads();
+            if (lane < kc) {
+                const BlockQuant q = block_params(bmax[lane]);
+                bq[lane] = q;
+                a.scales[k0 + lane] = q.scale;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int v = 0; v < MAXV; ++v) {
+            const size_t i = base + ((size_t)v * kWave + lane) * 4;
+            if ((uint32_t)v >= V || i >= end)
+                continue;
+            const uint32_t c4 = quant_word(pk[v].x, pk[v].y, bq[kl[v]]);
+            if (i + 4 <= end) {
                 st_nt(reinterpret_cast<uint32_t *>(a.codes + i), c4);
-            } else if (off < block) {
-                for (int e = 0; e < 4 && i + e < a.n; ++e)
+            } else {
+                for (int e = 0; e < 4 && i + e < end; ++e)
                     a.codes[i + e] = (int8_t)((c4 >> (8 * e)) & 0xFFu);
             }
         }
-        if (lane == 0)
-            a.scales[k] = q.scale;
+        __syncthreads();  // bmax and bq are rewritten for the next chunk
     }
 }
 
@@ -257,16 +365,30 @@ hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
     case 2048: launch_fused_b<2048>(a, gs, stream); break;
     case 4096: launch_fused_b<4096>(a, gs, stream); break;
     default: {
+        // blocks of up to 1024 values: at most 4 float4 groups per lane;
+        // larger ones 16 (4096 / 4 = 1024 groups fit 64 x 16)
+        const bool small = block / 4 <= 64 * 4;
+        const ChunkShape sh = chunk_shape(block / 4, small ? 4 : 16);
         const size_t nblocks = (a.n + block - 1) / block;
-        const unsigned grid =
-            (unsigned)(nblocks < ZPP_FUSED_MAX_GRID ? nblocks : ZPP_FUSED_MAX_GRID);
-        constexpr size_t lds = residency_lds(fused_residency<GS>());
-        if (a.c.adamw)
-            hipLaunchKernelGGL((fused_any_kernel<true, GS>), dim3(grid), dim3(kWave), lds, stream,
-                               a, gs, block);
-        else
-            hipLaunchKernelGGL((fused_any_kernel<false, GS>), dim3(grid), dim3(kWave), lds,
-                               stream, a, gs, block);
+        const size_t need = (nblocks + sh.K - 1) / sh.K;
+        const unsigned grid = (unsigned)(need < ZPP_FUSED_MAX_GRID ? need : ZPP_FUSED_MAX_GRID);
+        constexpr size_t lds = residency_lds(ZPP_FUSED_MULTI_RESIDENCY);
+        const BlockDiv d = make_block_div(block);
+        if (small) {
+            if (a.c.adamw)
+                hipLaunchKernelGGL((fused_multi_kernel<true, GS, 4>), dim3(grid), dim3(kWave),
+                                   lds, stream, a, gs, d, sh.K, sh.V);
+            else
+                hipLaunchKernelGGL((fused_multi_kernel<false, GS, 4>), dim3(grid), dim3(kWave),
+                                   lds, stream, a, gs, d, sh.K, sh.V);
+        } else {
+            if (a.c.adamw)
+                hipLaunchKernelGGL((fused_multi_kernel<true, GS, 16>), dim3(grid), dim3(kWave),
+                                   lds, stream, a, gs, d, sh.K, sh.V);
+            else
+                hipLaunchKernelGGL((fused_multi_kernel<false, GS, 16>), dim3(grid), dim3(kWave),
+                                   lds, stream, a, gs, d, sh.K, sh.V);
+        }
     }
     }
     return hipGetLastError();

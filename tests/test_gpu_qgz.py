@@ -416,7 +416,8 @@ def run_receive_pass(zpp, quants, n, grad_block, block, scale_out, state, second
     (8, 256 * 40, 256, 256, True), (8, 256 * 9 + 81, 256, 256, True),
     (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
     (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
-    (8, 192 * 37 + 5, 192, 320, True), (3, 320 * 11 + 7, 320, 192, False)])
+    (8, 192 * 37 + 5, 192, 320, True), (3, 320 * 11 + 7, 320, 192, False),
+    (8, 2112 * 5 + 17, 256, 2112, True)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_pass_equals_three_calls(zpp, P, n, grad_block, block, secondary, regime):
     """Bit for bit the receive step, then the refresh and the quantization of
@@ -651,7 +652,7 @@ def run_receive_pass_il(zpp, quants, n, grad_block, block, scale_out, state, sec
     (3, 65536 + 8, 64, 1024, False), (5, 100001, 512, 128, True), (1, 7, 256, 64, True),
     (64, 256 * 5 + 3, 256, 4096, True), (8, 1 << 18, 4096, 256, False),
     (16, 256 * 17 + 100, 128, 512, True), (8, 192 * 37 + 5, 192, 320, True),
-    (13, 256 * 9 + 81, 256, 256, True)])
+    (13, 256 * 9 + 81, 256, 256, True), (8, 2112 * 5 + 17, 256, 2112, True)])
 @pytest.mark.parametrize("regime", sorted(REGIMES))
 def test_receive_pass_interleaved_equals_separate(zpp, P, n, grad_block, block, secondary,
                                                   regime):
