@@ -184,10 +184,12 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
 // Vector path for a block B = 64 b that is not a power of two: a one-wave
 // workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
 // groups of 4 values v 64 + l of the chunk for v < V (each wave load 1 KiB
-// contiguous).  Each lane folds each group's absmax into its block's word in
-// LDS (an LDS max); lane k < K then derives block k's parameters once,
-// stores its scale and leaves the parameters in LDS, from which every lane
-// quantizes its groups, each group's 4 codes one 16-bit store.  MAXV slots
+// contiguous).  All loads of a chunk are issued first.  Each lane folds
+// each group's absmax into its block's word in LDS (an LDS max), or, when
+// one block fills the chunk (K = 1), the wave reduces it with cross-lane
+// shuffles; one lane per block then derives its parameters once, stores its
+// scale and leaves the parameters in LDS, from which every lane quantizes
+// its groups, each group's 4 codes one 16-bit store.  MAXV slots
 // per lane at most: 8 for blocks of up to 2048 values, 16 (4096 / 4 = 1024
 // groups fit 64 x 16) for larger ones, whose registers then allow fewer
 // waves per SIMD.
@@ -223,21 +225,21 @@ __global__ __launch_bounds__(kWave) void quant_i4_multi_kernel(
             }
         } else {
 #pragma unroll
-        for (int v = 0; v < kMaxI4Slots; ++v) {
-            x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            if ((uint32_t)v < V) {
-                const size_t i = base + ((size_t)v * kWave + lane) * 4;
-                if (i + 4 <= end) {
-                    x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
-                } else if (i < end) {
-                    float h[4];
+            for (int v = 0; v < kMaxI4Slots; ++v) {
+                x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                if ((uint32_t)v < V) {
+                    const size_t i = base + ((size_t)v * kWave + lane) * 4;
+                    if (i + 4 <= end) {
+                        x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
+                    } else if (i < end) {
+                        float h[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        h[e] = (i + e < end) ? src[i + e] : 0.0f;
-                    x[v] = f32x4{h[0], h[1], h[2], h[3]};
+                        for (int e = 0; e < 4; ++e)
+                            h[e] = (i + e < end) ? src[i + e] : 0.0f;
+                        x[v] = f32x4{h[0], h[1], h[2], h[3]};
+                    }
                 }
             }
-        }
         }
 #pragma unroll
         for (int v = 0; v < kMaxI4Slots; ++v)

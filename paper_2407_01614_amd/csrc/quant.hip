@@ -128,9 +128,11 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
 // Vector path for a block B = 64 b that is not a power of two: a one-wave
 // workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
 // 8-element vectors v 64 + l of the chunk for v < V (each wave load 1 KiB
-// contiguous, as in the power-of-two kernel).  Each lane folds each of its
-// vectors' absmax into its block's word in LDS (an LDS max); lane k < K then
-// derives block k's parameters once, stores its scale and leaves the
+// contiguous, as in the power-of-two kernel).  All loads of a chunk are
+// issued first.  Each lane folds each of its vectors' absmax into its
+// block's word in LDS (an LDS max), or, when one block fills the chunk
+// (K = 1), the wave reduces it with cross-lane shuffles; one lane per block
+// then derives its parameters once, stores its scale and leaves the
 // parameters in LDS, from which every lane quantizes its vectors.
 constexpr int kMaxQuantSlots = 8;  // 4096 / 8 = 512 vectors of a block fit 64 x 8
 
@@ -166,22 +168,22 @@ __global__ __launch_bounds__(kWave) void quant_multi_kernel(
             }
         } else {
 #pragma unroll
-        for (int v = 0; v < kMaxQuantSlots; ++v) {
-            x[v] = u32x4{0u, 0u, 0u, 0u};
-            if ((uint32_t)v < V) {
-                const size_t i = base + ((size_t)v * kWave + lane) * 8;
-                if (i + 8 <= end) {
-                    x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
-                } else if (i < end) {
-                    uint32_t h[8];
+            for (int v = 0; v < kMaxQuantSlots; ++v) {
+                x[v] = u32x4{0u, 0u, 0u, 0u};
+                if ((uint32_t)v < V) {
+                    const size_t i = base + ((size_t)v * kWave + lane) * 8;
+                    if (i + 8 <= end) {
+                        x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
+                    } else if (i < end) {
+                        uint32_t h[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        h[e] = (i + e < end) ? (uint32_t)src[i + e] : 0u;
-                    x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16),
-                                 h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+                        for (int e = 0; e < 8; ++e)
+                            h[e] = (i + e < end) ? (uint32_t)src[i + e] : 0u;
+                        x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16),
+                                     h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+                    }
                 }
             }
-        }
         }
 #pragma unroll
         for (int v = 0; v < kMaxQuantSlots; ++v)
