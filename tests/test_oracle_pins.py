@@ -540,7 +540,8 @@ def check_round_trip(orc):
     qs = [orc.quantize_blockwise_i8(padded[j * s:(j + 1) * s], block) for j in range(P2)]
     out = orc.dequant_gather_layer([q[0] for q in qs], [q[1] for q in qs], s, block, N)
     wf = (w.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
-    of = (out.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    with np.errstate(invalid="ignore"):  # a planted mistake may return non-integers
+        of = (out.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
     sc = np.concatenate([np.repeat(q[1], block)[:s] for q in qs])[:N].astype(np.float64)
     bound = sc * (0.5 + 2.0 ** -15) + np.abs(of) * 2.0 ** -8
     assert np.all(np.abs(wf - of) <= bound)
