@@ -19,8 +19,8 @@
 // kernels forms each float4, so the bits are those of the separate arrays.
 //
 // Blocks may be any multiple of 64 up to 4096; for those that are not powers
-// of two the quantizer takes several whole blocks per wave at a time, the
-// block absmax folded in LDS.
+// of two the quantizer gives each block an aligned group of 16 to 64 lanes
+// of a wave, each lane holding several of its groups of 4 values.
 //
 // Both kernels keep every wave's loads and stores contiguous: on this GPU,
 // non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
@@ -42,6 +42,16 @@
 #endif
 #ifndef ZPP_QGZ_REDUCE_IL_GROUPS
 #define ZPP_QGZ_REDUCE_IL_GROUPS 2
+#endif
+// Shape of the quantizer for blocks that are not powers of two
+// (zpp_chunk.h): at least three slots per lane, and the widest lane group
+// whose slots the block fills to this percentage.  Swept at the Llama-2-13B
+// partition over blocks of 192 to 4032 (median of 20 launches each): 149-157
+// us with this rule, against up to 173 us with two slots and 220 with
+// groups of 8 lanes (16-byte runs of codes per store instruction), and
+// 191-228 us for the earlier layout that folded each block's absmax in LDS.
+#ifndef ZPP_QGZ_GROUP_MIN_FILL
+#define ZPP_QGZ_GROUP_MIN_FILL 75
 #endif
 #ifndef ZPP_QGZ_MAX_GRID
 #define ZPP_QGZ_MAX_GRID (1u << 30)
@@ -181,116 +191,83 @@ __global__ __launch_bounds__(kQgzThreads) void quant_i4_kernel(
     }
 }
 
-// Vector path for a block B = 64 b that is not a power of two: a one-wave
-// workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
-// groups of 4 values v 64 + l of the chunk for v < V (each wave load 1 KiB
-// contiguous).  All loads of a chunk are issued first.  Each lane folds
-// each group's absmax into its block's word in LDS (an LDS max), or, when
-// one block fills the chunk (K = 1), the wave reduces it with cross-lane
-// shuffles; one lane per block then derives its parameters once, stores its
-// scale and leaves the parameters in LDS, from which every lane quantizes
-// its groups, each group's 4 codes one 16-bit store.  MAXV slots
-// per lane at most: 8 for blocks of up to 2048 values, 16 (4096 / 4 = 1024
-// groups fit 64 x 16) for larger ones, whose registers then allow fewer
-// waves per SIMD.
-template <int kMaxI4Slots>
-__global__ __launch_bounds__(kWave) void quant_i4_multi_kernel(
-    const float *__restrict__ src, size_t n, BlockDiv blk, uint32_t K, uint32_t V,
-    uint8_t *__restrict__ codes, float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
-    __shared__ uint32_t bmax[64];
-    __shared__ I4Quant bq[64];
-    const uint32_t lane = threadIdx.x;
-    const uint32_t B = blk.block;
+// Vector path for a block B = 64 b that is not a power of two, lane-group
+// layout (zpp_chunk.h): each block owns an aligned group of G lanes, lane r
+// of the group holding the block's groups of 4 values v G + r for v < S
+// (groups past the block's end stay empty).  The block absmax is a
+// reduction over the group's G lanes with cross-lane xor shuffles and every
+// lane derives the block's parameters itself, as in the power-of-two
+// kernel: no LDS, no atomics and no barrier.  Workgroups whose blocks all
+// lie inside the array load each group with one predicated load; only the
+// last one checks every element.
+template <int G, int S>
+__global__ __launch_bounds__(kQgzThreads) void quant_i4_grp_kernel(
+    const float *__restrict__ src, size_t n, uint32_t B, uint8_t *__restrict__ codes,
+    float *__restrict__ scales, uint32_t q_src, uint32_t num_src) {
+    constexpr int kBlocksPerWave = kWave / G;
+    constexpr int kBlocksPerGroup = kBlocksPerWave * (kQgzThreads / kWave);
+    const uint32_t gpb = B / 4;
     const size_t nblocks = (n + B - 1) / B;
-    for (size_t k0 = (size_t)blockIdx.x * K; k0 < nblocks; k0 += (size_t)gridDim.x * K) {
-        const uint32_t kc = (uint32_t)(nblocks - k0 < K ? nblocks - k0 : K);
-        const size_t base = k0 * B;
-        const size_t end = (base + (size_t)kc * B < n) ? base + (size_t)kc * B : n;
-        if (lane < kc)
-            bmax[lane] = 0u;
-        __syncthreads();
-        // every load of the chunk first, then the LDS maxima (a max in the
-        // same pass would wait for each load in turn)
-        f32x4 x[kMaxI4Slots];
-        uint32_t kl[kMaxI4Slots];
-        if (end == base + (size_t)K * B) {
-            // a whole chunk: every group complete, one predicated load each
-            const uint32_t ngrp = K * (B / 4);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int li = lane % G;
+    const size_t kw = (size_t)(threadIdx.x / kWave) * kBlocksPerWave + lane / G;
+    for (size_t g0 = (size_t)blockIdx.x * kBlocksPerGroup; g0 < nblocks;
+         g0 += (size_t)gridDim.x * kBlocksPerGroup) {
+        const size_t k = g0 + kw;
+        const bool valid = k < nblocks;
+        const bool whole = (g0 + kBlocksPerGroup) * B <= n;  // uniform
+        f32x4 x[S];
+        if (whole) {
 #pragma unroll
-            for (int v = 0; v < kMaxI4Slots; ++v) {
+            for (int v = 0; v < S; ++v) {
                 x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                const uint32_t j = (uint32_t)v * kWave + lane;
-                if ((uint32_t)v < V && j < ngrp)
-                    x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + base + (size_t)j * 4));
+                const uint32_t j = (uint32_t)(v * G + li);
+                if (j < gpb)
+                    x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + k * B + (size_t)j * 4));
             }
         } else {
 #pragma unroll
-            for (int v = 0; v < kMaxI4Slots; ++v) {
+            for (int v = 0; v < S; ++v) {
                 x[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                if ((uint32_t)v < V) {
-                    const size_t i = base + ((size_t)v * kWave + lane) * 4;
-                    if (i + 4 <= end) {
+                const uint32_t j = (uint32_t)(v * G + li);
+                const size_t i = k * B + (size_t)j * 4;
+                if (valid && j < gpb) {
+                    if (i + 4 <= n) {
                         x[v] = ld_nt(reinterpret_cast<const f32x4 *>(src + i));
-                    } else if (i < end) {
+                    } else if (i < n) {
                         float h[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            h[e] = (i + e < end) ? src[i + e] : 0.0f;
+                            h[e] = (i + e < n) ? src[i + e] : 0.0f;
                         x[v] = f32x4{h[0], h[1], h[2], h[3]};
                     }
                 }
             }
         }
+        uint32_t mx = 0;
 #pragma unroll
-        for (int v = 0; v < kMaxI4Slots; ++v)
-            kl[v] = 0u;
-        if (K == 1) {
-            // one block per chunk: its absmax is a reduction over the wave
-            uint32_t mx = 0;
+        for (int v = 0; v < S; ++v)
+            mx = max(mx, abs_bits_max4(x[v]));
 #pragma unroll
-            for (int v = 0; v < kMaxI4Slots; ++v)
-                mx = max(mx, abs_bits_max4(x[v]));
+        for (int off = G / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const I4Quant q = i4_params(mx);
 #pragma unroll
-            for (int off = kWave / 2; off >= 1; off >>= 1)
-                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-            if (lane == 0) {
-                const I4Quant q = i4_params(mx);
-                bq[0] = q;
-                scales[k0 * num_src + q_src] = q.scale;
-            }
-        } else {
-#pragma unroll
-            for (int v = 0; v < kMaxI4Slots; ++v) {
-                const size_t i = base + ((size_t)v * kWave + lane) * 4;
-                if ((uint32_t)v < V && i < end) {
-                    kl[v] = (uint32_t)(block_of(blk, i) - k0);
-                    atomicMax(&bmax[kl[v]], abs_bits_max4(x[v]));
-                }
-            }
-            __syncthreads();
-            if (lane < kc) {
-                const I4Quant q = i4_params(bmax[lane]);
-                bq[lane] = q;
-                scales[(k0 + lane) * num_src + q_src] = q.scale;
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int v = 0; v < kMaxI4Slots; ++v) {
-            if ((uint32_t)v >= V)
+        for (int v = 0; v < S; ++v) {
+            const uint32_t j = (uint32_t)(v * G + li);
+            const size_t i = k * B + (size_t)j * 4;
+            if (!valid || j >= gpb || i >= n)
                 continue;
-            const size_t i = base + ((size_t)v * kWave + lane) * 4;
-            if (i >= end)
-                continue;
-            const uint32_t h = i4_half(x[v], bq[kl[v]]);
-            const size_t byte0 = i4_out_byte_any(i, k0 + kl[v], B, q_src, num_src);
+            const uint32_t h = i4_half(x[v], q);
+            const size_t byte0 = i4_out_byte_any(i, k, B, q_src, num_src);
             // the second byte holds elements i + 2 and i + 3
             if (i + 2 < n)
                 st_nt(reinterpret_cast<uint16_t *>(codes + byte0), (uint16_t)h);
             else
                 codes[byte0] = (uint8_t)h;
         }
-        __syncthreads();  // bmax and bq are rewritten for the next chunk
+        if (valid && li == 0)
+            scales[k * num_src + q_src] = q.scale;
     }
 }
 
@@ -481,6 +458,28 @@ void launch_quant_i4_b(const float *src, size_t n, uint8_t *codes, float *scales
                        0, stream, src, n, codes, scales, q_src, num_src);
 }
 
+template <int G, int S>
+void launch_quant_i4_grp(const float *src, size_t n, uint32_t block, uint8_t *codes,
+                         float *scales, uint32_t q_src, uint32_t num_src, hipStream_t stream) {
+    constexpr size_t kBlocksPerGroup = (kWave / G) * (kQgzThreads / kWave);
+    const size_t nblocks = (n + block - 1) / block;
+    const size_t need = (nblocks + kBlocksPerGroup - 1) / kBlocksPerGroup;
+    const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
+    hipLaunchKernelGGL((quant_i4_grp_kernel<G, S>), dim3(grid), dim3(kQgzThreads), 0, stream,
+                       src, n, block, codes, scales, q_src, num_src);
+}
+
+template <int S>
+void launch_quant_i4_grp_g(uint32_t G, const float *src, size_t n, uint32_t block,
+                           uint8_t *codes, float *scales, uint32_t q_src, uint32_t num_src,
+                           hipStream_t stream) {
+    switch (G) {
+    case 16: launch_quant_i4_grp<16, S>(src, n, block, codes, scales, q_src, num_src, stream); break;
+    case 32: launch_quant_i4_grp<32, S>(src, n, block, codes, scales, q_src, num_src, stream); break;
+    default: launch_quant_i4_grp<64, S>(src, n, block, codes, scales, q_src, num_src, stream); break;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uint32_t source,
@@ -496,19 +495,16 @@ hipError_t launch_quantize_i4_il(const float *src, size_t n, uint32_t block, uin
         case 2048: launch_quant_i4_b<2048>(src, n, codes, scales, source, num_src, stream); break;
         case 4096: launch_quant_i4_b<4096>(src, n, codes, scales, source, num_src, stream); break;
         default: {
-            const bool small = block / 4 <= 64 * 8;
-            const ChunkShape sh = chunk_shape(block / 4, small ? 8 : 16);
-            const size_t nblocks = (n + block - 1) / block;
-            const size_t need = (nblocks + sh.K - 1) / sh.K;
-            const unsigned grid = (unsigned)(need < ZPP_QGZ_MAX_GRID ? need : ZPP_QGZ_MAX_GRID);
-            if (small)
-                hipLaunchKernelGGL(quant_i4_multi_kernel<8>, dim3(grid), dim3(kWave), 0, stream,
-                                   src, n, make_block_div(block), sh.K, sh.V, codes, scales,
-                                   source, num_src);
+            const GroupShape sh = group_shape(block / 4, 16, ZPP_QGZ_GROUP_MIN_FILL, 3);
+            if (sh.S <= 4)
+                launch_quant_i4_grp_g<4>(sh.G, src, n, block, codes, scales, source, num_src,
+                                         stream);
+            else if (sh.S <= 8)
+                launch_quant_i4_grp_g<8>(sh.G, src, n, block, codes, scales, source, num_src,
+                                         stream);
             else
-                hipLaunchKernelGGL(quant_i4_multi_kernel<16>, dim3(grid), dim3(kWave), 0, stream,
-                                   src, n, make_block_div(block), sh.K, sh.V, codes, scales,
-                                   source, num_src);
+                launch_quant_i4_grp_g<16>(sh.G, src, n, block, codes, scales, source, num_src,
+                                          stream);
         }
         }
     } else {

@@ -10,9 +10,9 @@
 // traffic and no float compares are needed.  Every lane then derives the
 // block's scale and inverse itself (two correctly rounded divisions per 8
 // elements) and writes its 8 codes as one 8-byte store.  Blocks that are
-// not powers of two (any multiple of 64 up to 4096) take a one-wave kernel
-// that works on several whole blocks at a time, the block absmax folded in
-// LDS.
+// not powers of two (any multiple of 64 up to 4096) take the same approach
+// with the block's width a run-time value: a block owns an aligned group of
+// 16 to 64 lanes, each holding up to 16 of its vectors.
 //
 // The same kernels can also store the bf16 they read to a second array:
 // the secondary refresh and its quantization in one pass (2 B read, 2 B +
@@ -28,6 +28,20 @@
 #endif
 #ifndef ZPP_QUANT_THREADS
 #define ZPP_QUANT_THREADS 256
+#endif
+// Shape of the kernel for blocks that are not powers of two (zpp_chunk.h):
+// at least two vector slots per lane, and the widest lane group whose slots
+// the block fills to this percentage.  Swept at the Llama-2-13B partition
+// over blocks of 192 to 2112 (median of 20 launches each): the plain
+// quantizer streams best with a fill of 75% (93-102 us against 97-120 for
+// 55-85% or three slots), the pass with the copy with 55% (167-175 us
+// against 168-185); one slot per lane was slower for both (137 against
+// 97 us at 448).
+#ifndef ZPP_QUANT_GROUP_MIN_FILL
+#define ZPP_QUANT_GROUP_MIN_FILL 75
+#endif
+#ifndef ZPP_QUANT_COPY_GROUP_MIN_FILL
+#define ZPP_QUANT_COPY_GROUP_MIN_FILL 55
 #endif
 #ifndef ZPP_QUANT_MAX_GRID
 #define ZPP_QUANT_MAX_GRID (1u << 20)
@@ -125,123 +139,86 @@ __global__ __launch_bounds__(kQuantThreads) void quant_vec_kernel(
     }
 }
 
-// Vector path for a block B = 64 b that is not a power of two: a one-wave
-// workgroup takes K whole blocks at a time (zpp_chunk.h), lane l holding the
-// 8-element vectors v 64 + l of the chunk for v < V (each wave load 1 KiB
-// contiguous, as in the power-of-two kernel).  All loads of a chunk are
-// issued first.  Each lane folds each of its vectors' absmax into its
-// block's word in LDS (an LDS max), or, when one block fills the chunk
-// (K = 1), the wave reduces it with cross-lane shuffles; one lane per block
-// then derives its parameters once, stores its scale and leaves the
-// parameters in LDS, from which every lane quantizes its vectors.
-constexpr int kMaxQuantSlots = 8;  // 4096 / 8 = 512 vectors of a block fit 64 x 8
-
-template <bool COPY>
-__global__ __launch_bounds__(kWave) void quant_multi_kernel(
-    const uint16_t *__restrict__ src, size_t n, BlockDiv blk, uint32_t K, uint32_t V,
-    int8_t *__restrict__ codes, float *__restrict__ scales, uint16_t *__restrict__ copy) {
-    __shared__ uint32_t bmax[64];
-    __shared__ BlockQuant bq[64];
-    const uint32_t lane = threadIdx.x;
-    const size_t B = blk.block;
+// Vector path for a block B = 64 b that is not a power of two, lane-group
+// layout (zpp_chunk.h): each block owns an aligned group of G lanes, lane r
+// of the group holding the block's vectors v G + r for v < S (vectors past
+// the block's end stay empty), so a wave load covers 64 / G runs of G
+// consecutive vectors.  The block absmax is a reduction over the group's G
+// lanes with cross-lane xor shuffles and every lane derives the block's
+// parameters itself, as in the power-of-two kernel: no LDS, no atomics and
+// no barrier.  Workgroups whose blocks all lie inside the array load each
+// vector with one predicated load; only the last one checks every element.
+template <int G, int S, bool COPY>
+__global__ __launch_bounds__(kQuantThreads) void quant_grp_kernel(
+    const uint16_t *__restrict__ src, size_t n, uint32_t B, int8_t *__restrict__ codes,
+    float *__restrict__ scales, uint16_t *__restrict__ copy) {
+    constexpr int kGroupsPerWave = kWave / G;
+    constexpr int kGroupsPerBlock = kGroupsPerWave * (kQuantThreads / kWave);
+    const uint32_t vpb = B / 8;
     const size_t nblocks = (n + B - 1) / B;
-    for (size_t k0 = (size_t)blockIdx.x * K; k0 < nblocks; k0 += (size_t)gridDim.x * K) {
-        const uint32_t kc = (uint32_t)(nblocks - k0 < K ? nblocks - k0 : K);
-        const size_t base = k0 * B;
-        const size_t end = (base + kc * B < n) ? base + kc * B : n;
-        if (lane < kc)
-            bmax[lane] = 0u;
-        __syncthreads();
-        // every load of the chunk first, then the LDS maxima (a max in the
-        // same pass would wait for each load in turn)
-        u32x4 x[kMaxQuantSlots];
-        uint32_t kl[kMaxQuantSlots];
-        if (end == base + (size_t)K * B) {
-            // a whole chunk: every vector complete, one predicated load each
-            const uint32_t nvec = K * (uint32_t)(B / 8);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int li = lane % G;
+    const size_t kw = (size_t)(threadIdx.x / kWave) * kGroupsPerWave + lane / G;
+    for (size_t g0 = (size_t)blockIdx.x * kGroupsPerBlock; g0 < nblocks;
+         g0 += (size_t)gridDim.x * kGroupsPerBlock) {
+        const size_t k = g0 + kw;
+        const bool valid = k < nblocks;
+        const bool whole = (g0 + kGroupsPerBlock) * B <= n;  // uniform
+        u32x4 x[S];
+        if (whole) {
 #pragma unroll
-            for (int v = 0; v < kMaxQuantSlots; ++v) {
+            for (int v = 0; v < S; ++v) {
                 x[v] = u32x4{0u, 0u, 0u, 0u};
-                const uint32_t j = (uint32_t)v * kWave + lane;
-                if ((uint32_t)v < V && j < nvec)
-                    x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + base + (size_t)j * 8));
+                const uint32_t j = (uint32_t)(v * G + li);
+                if (j < vpb)
+                    x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + k * B + (size_t)j * 8));
             }
         } else {
 #pragma unroll
-            for (int v = 0; v < kMaxQuantSlots; ++v) {
+            for (int v = 0; v < S; ++v) {
                 x[v] = u32x4{0u, 0u, 0u, 0u};
-                if ((uint32_t)v < V) {
-                    const size_t i = base + ((size_t)v * kWave + lane) * 8;
-                    if (i + 8 <= end) {
+                const uint32_t j = (uint32_t)(v * G + li);
+                const size_t i = k * B + (size_t)j * 8;
+                if (valid && j < vpb) {
+                    if (i + 8 <= n) {
                         x[v] = ld_nt(reinterpret_cast<const u32x4 *>(src + i));
-                    } else if (i < end) {
+                    } else if (i < n) {
                         uint32_t h[8];
 #pragma unroll
                         for (int e = 0; e < 8; ++e)
-                            h[e] = (i + e < end) ? (uint32_t)src[i + e] : 0u;
+                            h[e] = (i + e < n) ? (uint32_t)src[i + e] : 0u;
                         x[v] = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16),
                                      h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
                     }
                 }
             }
         }
+        u16x2 m2 = {0, 0};
 #pragma unroll
-        for (int v = 0; v < kMaxQuantSlots; ++v)
-            kl[v] = 0u;
-        if (K == 1) {
-            // one block per chunk: its absmax is a reduction over the wave
-            u16x2 m2 = {0, 0};
+        for (int v = 0; v < S; ++v)
+            m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
+                     __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
+                     __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
+        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
 #pragma unroll
-            for (int v = 0; v < kMaxQuantSlots; ++v)
-                m2 = __builtin_elementwise_max(m2, __builtin_elementwise_max(
-                         __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
-                         __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w))));
-            uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+        for (int off = G / 2; off >= 1; off >>= 1)
+            mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+        const BlockQuant q = block_params(mx);
 #pragma unroll
-            for (int off = kWave / 2; off >= 1; off >>= 1)
-                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-            if (lane == 0) {
-                const BlockQuant q = block_params(mx);
-                bq[0] = q;
-                scales[k0] = q.scale;
-            }
-        } else {
-#pragma unroll
-            for (int v = 0; v < kMaxQuantSlots; ++v) {
-                const size_t i = base + ((size_t)v * kWave + lane) * 8;
-                if ((uint32_t)v < V && i < end) {
-                    kl[v] = (uint32_t)(block_of(blk, i) - k0);
-                    const u16x2 m2 = __builtin_elementwise_max(
-                        __builtin_elementwise_max(absbits2(x[v].x), absbits2(x[v].y)),
-                        __builtin_elementwise_max(absbits2(x[v].z), absbits2(x[v].w)));
-                    atomicMax(&bmax[kl[v]], max((uint32_t)m2.x, (uint32_t)m2.y));
-                }
-            }
-            __syncthreads();
-            if (lane < kc) {
-                const BlockQuant q = block_params(bmax[lane]);
-                bq[lane] = q;
-                scales[k0 + lane] = q.scale;
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int v = 0; v < kMaxQuantSlots; ++v) {
-            if ((uint32_t)v >= V)
+        for (int v = 0; v < S; ++v) {
+            const uint32_t j = (uint32_t)(v * G + li);
+            const size_t i = k * B + (size_t)j * 8;
+            if (!valid || j >= vpb || i >= n)
                 continue;
-            const size_t i = base + ((size_t)v * kWave + lane) * 8;
-            if (i >= end)
-                continue;
-            const BlockQuant q = bq[kl[v]];
             u32x2 c;
             c.x = quant_word(x[v].x, x[v].y, q);
             c.y = quant_word(x[v].z, x[v].w, q);
-            if (i + 8 <= end) {
+            if (i + 8 <= n) {
                 st_nt(reinterpret_cast<u32x2 *>(codes + i), c);
                 if (COPY)
                     st_nt(reinterpret_cast<u32x4 *>(copy + i), x[v]);
             } else {
-                for (int e = 0; e < 8 && i + e < end; ++e) {
+                for (int e = 0; e < 8 && i + e < n; ++e) {
                     codes[i + e] =
                         (int8_t)((e < 4 ? c.x >> (8 * e) : c.y >> (8 * (e - 4))) & 0xFFu);
                     if (COPY)
@@ -249,7 +226,8 @@ __global__ __launch_bounds__(kWave) void quant_multi_kernel(
                 }
             }
         }
-        __syncthreads();  // bmax and bq are rewritten for the next chunk
+        if (valid && li == 0)
+            scales[k] = q.scale;
     }
 }
 
@@ -295,6 +273,27 @@ void launch_vec(const uint16_t *src, size_t n, int8_t *codes, float *scales, uin
                        stream, src, n, codes, scales, copy);
 }
 
+template <int G, int S, bool COPY>
+void launch_grp(const uint16_t *src, size_t n, uint32_t block, int8_t *codes, float *scales,
+                uint16_t *copy, hipStream_t stream) {
+    constexpr size_t kGroupsPerBlock = (kWave / G) * (kQuantThreads / kWave);
+    const size_t nblocks = (n + block - 1) / block;
+    const size_t need = (nblocks + kGroupsPerBlock - 1) / kGroupsPerBlock;
+    const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
+    hipLaunchKernelGGL((quant_grp_kernel<G, S, COPY>), dim3(grid), dim3(kQuantThreads), 0,
+                       stream, src, n, block, codes, scales, copy);
+}
+
+template <int S, bool COPY>
+void launch_grp_g(uint32_t G, const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
+                  float *scales, uint16_t *copy, hipStream_t stream) {
+    switch (G) {
+    case 16: launch_grp<16, S, COPY>(src, n, block, codes, scales, copy, stream); break;
+    case 32: launch_grp<32, S, COPY>(src, n, block, codes, scales, copy, stream); break;
+    default: launch_grp<64, S, COPY>(src, n, block, codes, scales, copy, stream); break;
+    }
+}
+
 template <bool COPY>
 void launch_vector(const uint16_t *src, size_t n, uint32_t block, int8_t *codes, float *scales,
                    uint16_t *copy, hipStream_t stream) {
@@ -307,12 +306,17 @@ void launch_vector(const uint16_t *src, size_t n, uint32_t block, int8_t *codes,
     case 2048: launch_vec<2048, COPY>(src, n, codes, scales, copy, stream); break;
     case 4096: launch_vec<4096, COPY>(src, n, codes, scales, copy, stream); break;
     default: {
-        const ChunkShape sh = chunk_shape(block / 8, kMaxQuantSlots);
-        const size_t nblocks = (n + block - 1) / block;
-        const size_t need = (nblocks + sh.K - 1) / sh.K;
-        const unsigned grid = (unsigned)(need < ZPP_QUANT_MAX_GRID ? need : ZPP_QUANT_MAX_GRID);
-        hipLaunchKernelGGL((quant_multi_kernel<COPY>), dim3(grid), dim3(kWave), 0, stream, src,
-                           n, make_block_div(block), sh.K, sh.V, codes, scales, copy);
+        const GroupShape sh =
+            COPY ? group_shape(block / 8, 16, ZPP_QUANT_COPY_GROUP_MIN_FILL, 2)
+                 : group_shape(block / 8, 16, ZPP_QUANT_GROUP_MIN_FILL, 2);
+        if (sh.S <= 2)
+            launch_grp_g<2, COPY>(sh.G, src, n, block, codes, scales, copy, stream);
+        else if (sh.S <= 4)
+            launch_grp_g<4, COPY>(sh.G, src, n, block, codes, scales, copy, stream);
+        else if (sh.S <= 8)
+            launch_grp_g<8, COPY>(sh.G, src, n, block, codes, scales, copy, stream);
+        else
+            launch_grp_g<16, COPY>(sh.G, src, n, block, codes, scales, copy, stream);
     }
     }
 }

@@ -1,12 +1,24 @@
-// Host check of the quantizers' work shape for blocks that are not powers of
-// two (zpp_chunk.h): for every such block size and both vector widths (8
-// bf16 of the int8 quantizer, 4 fp32 of the int4 one), the shape exists,
-// its K blocks fit the 64 V vector slots of a wave and the LDS word of each
-// block (K <= 64), and the lane/slot walk of one chunk -- vector j = 64 v +
-// l of the chunk for v < V -- covers every element of every block of the
-// chunk exactly once, including a last chunk of fewer blocks and a last
-// block cut short by the end of the array.  Prints the worst fill of the
-// slots and "chunk shapes ok".
+// Host check of the work shapes for blocks that are not powers of two
+// (zpp_chunk.h).
+//
+// Chunk shapes (the fused step, 4 fp32 per float4 group, 4 slots for blocks
+// of up to 1024 values and 16 above): for every such block size the shape
+// exists, its K blocks fit the 64 V slots of a wave and the LDS word of each
+// block (K <= 64), and the lane/slot walk of one chunk -- group j = 64 v + l
+// of the chunk for v < V -- covers every element of every block of the chunk
+// exactly once, including a last chunk of fewer blocks and a last block cut
+// short by the end of the array.
+//
+// Lane-group shapes (the int8 quantizer, 8 bf16 per vector, with and without
+// the copy; the int4 quantizer, 4 fp32 per group), with the kernels' own
+// parameters: the shape exists, G is 16, 32 or 64, S is at most 16 and at
+// least the kernel's minimum where the fill allows it, the G S slots hold
+// the block, and the walk -- block k in lanes [G (k % (64 /
+// G)), +G) of a wave, lane r holding the block's vectors v G + r for v below
+// the kernel's slot count (the power of two at or above S) -- covers every
+// element exactly once, the last block cut short included.
+//
+// Prints the worst fills and "chunk shapes ok".
 #include <stdint.h>
 #include <stdio.h>
 
@@ -14,60 +26,133 @@
 
 #include "zpp_chunk.h"
 
-int main() {
+static long check_chunks(double &worst) {
     long bad = 0;
-    double worst = 1.0;
-    // int8: 8 bf16 per vector, 8 slots; int4: 4 fp32 per group, 8 slots for
-    // blocks of up to 2048 values and 16 above (the kernels' two instances)
-    const struct { uint32_t w; } kinds[2] = {{8}, {4}};
-    for (const auto &kd : kinds) {
-        for (uint32_t b = 1; b <= 64; ++b) {
-            if ((b & (b - 1)) == 0)
-                continue;  // powers of two take the other kernels
-            const uint32_t B = 64 * b, vpb = B / kd.w;
-            const uint32_t max_v = (kd.w == 8 || vpb <= 64 * 8) ? 8 : 16;
-            const zpp::ChunkShape sh = zpp::chunk_shape(vpb, max_v);
-            if (sh.K == 0 || sh.K > 64 || sh.V == 0 || sh.V > max_v ||
-                (uint64_t)sh.K * vpb > 64ull * sh.V) {
-                printf("bad shape: w %u B %u -> K %u V %u\n", kd.w, B, sh.K, sh.V);
-                ++bad;
-                continue;
-            }
-            const double fill = (double)sh.K * vpb / (64.0 * sh.V);
-            if (fill < worst)
-                worst = fill;
-            // one array of 2.5 chunks whose last block is short
-            const uint64_t n = (uint64_t)B * (sh.K * 2 + sh.K / 2 + 1) - 3 * kd.w - 1;
-            std::vector<int> seen(n, 0);
-            const uint64_t nblocks = (n + B - 1) / B;
-            for (uint64_t k0 = 0; k0 < nblocks; k0 += sh.K) {
-                const uint64_t kc = nblocks - k0 < sh.K ? nblocks - k0 : sh.K;
-                const uint64_t base = k0 * B, end = base + kc * B < n ? base + kc * B : n;
-                for (uint32_t v = 0; v < sh.V; ++v)
-                    for (uint32_t l = 0; l < 64; ++l) {
-                        const uint64_t i = base + ((uint64_t)v * 64 + l) * kd.w;
-                        if (i >= end)
-                            continue;
-                        const uint64_t kl = i / B - k0;
-                        if (kl >= kc || (i + kd.w <= end && (i + kd.w - 1) / B != i / B)) {
-                            printf("vector outside its block: w %u B %u i %llu\n", kd.w, B,
-                                   (unsigned long long)i);
-                            ++bad;
-                        }
-                        for (uint32_t e = 0; e < kd.w && i + e < end; ++e)
-                            ++seen[i + e];
+    const uint32_t w = 4;
+    for (uint32_t b = 1; b <= 64; ++b) {
+        if ((b & (b - 1)) == 0)
+            continue;  // powers of two take the other kernels
+        const uint32_t B = 64 * b, vpb = B / w;
+        const uint32_t max_v = vpb <= 64 * 4 ? 4 : 16;
+        const zpp::ChunkShape sh = zpp::chunk_shape(vpb, max_v);
+        if (sh.K == 0 || sh.K > 64 || sh.V == 0 || sh.V > max_v ||
+            (uint64_t)sh.K * vpb > 64ull * sh.V) {
+            printf("bad chunk shape: B %u -> K %u V %u\n", B, sh.K, sh.V);
+            ++bad;
+            continue;
+        }
+        const double fill = (double)sh.K * vpb / (64.0 * sh.V);
+        if (fill < worst)
+            worst = fill;
+        // one array of 2.5 chunks whose last block is short
+        const uint64_t n = (uint64_t)B * (sh.K * 2 + sh.K / 2 + 1) - 3 * w - 1;
+        std::vector<int> seen(n, 0);
+        const uint64_t nblocks = (n + B - 1) / B;
+        for (uint64_t k0 = 0; k0 < nblocks; k0 += sh.K) {
+            const uint64_t kc = nblocks - k0 < sh.K ? nblocks - k0 : sh.K;
+            const uint64_t base = k0 * B, end = base + kc * B < n ? base + kc * B : n;
+            for (uint32_t v = 0; v < sh.V; ++v)
+                for (uint32_t l = 0; l < 64; ++l) {
+                    const uint64_t i = base + ((uint64_t)v * 64 + l) * w;
+                    if (i >= end)
+                        continue;
+                    const uint64_t kl = i / B - k0;
+                    if (kl >= kc || (i + w <= end && (i + w - 1) / B != i / B)) {
+                        printf("group outside its block: B %u i %llu\n", B,
+                               (unsigned long long)i);
+                        ++bad;
                     }
-            }
-            for (uint64_t i = 0; i < n; ++i)
-                if (seen[i] != 1) {
-                    printf("element %llu seen %d times: w %u B %u\n", (unsigned long long)i,
-                           seen[i], kd.w, B);
-                    ++bad;
-                    break;
+                    for (uint32_t e = 0; e < w && i + e < end; ++e)
+                        ++seen[i + e];
                 }
         }
+        for (uint64_t i = 0; i < n; ++i)
+            if (seen[i] != 1) {
+                printf("element %llu seen %d times: chunk B %u\n", (unsigned long long)i,
+                       seen[i], B);
+                ++bad;
+                break;
+            }
     }
-    printf("worst fill %.4f\n", worst);
+    return bad;
+}
+
+static uint32_t slot_bucket(uint32_t s, uint32_t smallest) {
+    uint32_t b = smallest;
+    while (b < s)
+        b *= 2;
+    return b;
+}
+
+static long check_groups(uint32_t w, uint32_t min_fill, uint32_t min_s, uint32_t smallest_bucket,
+                         const char *what, double &worst) {
+    long bad = 0;
+    for (uint32_t b = 1; b <= 64; ++b) {
+        if ((b & (b - 1)) == 0)
+            continue;
+        const uint32_t B = 64 * b, vpb = B / w;
+        const zpp::GroupShape sh = zpp::group_shape(vpb, 16, min_fill, min_s);
+        const bool pow2 = sh.G != 0 && (sh.G & (sh.G - 1)) == 0;
+        if (!pow2 || sh.G < 16 || sh.G > 64 || sh.S == 0 || sh.S > 16 ||
+            (uint64_t)sh.G * sh.S < vpb || (uint64_t)sh.G * (sh.S - 1) >= vpb) {
+            printf("bad group shape: %s B %u -> G %u S %u\n", what, B, sh.G, sh.S);
+            ++bad;
+            continue;
+        }
+        const double fill = (double)vpb / ((double)sh.G * sh.S);
+        if (fill < worst)
+            worst = fill;
+        // the rule: a shape with at least min_s slots and the fill asked for
+        // is taken whenever one exists, the widest such group first
+        for (uint32_t g = 64; g > sh.G; g /= 2) {
+            const uint32_t s = (vpb + g - 1) / g;
+            if (s >= min_s && s <= 16 && 100ull * vpb >= (uint64_t)min_fill * g * s) {
+                printf("wider group passed over: %s B %u G %u (took %u)\n", what, B, g, sh.G);
+                ++bad;
+            }
+        }
+        const uint32_t slots = slot_bucket(sh.S, smallest_bucket);
+        const uint32_t bpw = 64 / sh.G;
+        // 2.5 waves of blocks, the last block short
+        const uint64_t n = (uint64_t)B * (bpw * 2 + bpw / 2 + 1) - 3 * w - 1;
+        std::vector<int> seen(n, 0);
+        const uint64_t nblocks = (n + B - 1) / B;
+        for (uint64_t k = 0; k < nblocks; ++k)
+            for (uint32_t r = 0; r < sh.G; ++r)
+                for (uint32_t v = 0; v < slots; ++v) {
+                    const uint64_t j = (uint64_t)v * sh.G + r;
+                    const uint64_t i = k * B + j * w;
+                    if (j >= vpb || i >= n)
+                        continue;
+                    if (v >= sh.S) {
+                        printf("slot past S holds data: %s B %u\n", what, B);
+                        ++bad;
+                    }
+                    for (uint32_t e = 0; e < w && i + e < n; ++e)
+                        ++seen[i + e];
+                }
+        for (uint64_t i = 0; i < n; ++i)
+            if (seen[i] != 1) {
+                printf("element %llu seen %d times: %s B %u\n", (unsigned long long)i, seen[i],
+                       what, B);
+                ++bad;
+                break;
+            }
+    }
+    return bad;
+}
+
+int main() {
+    double worst_chunk = 1.0, worst_i8 = 1.0, worst_i8c = 1.0, worst_i4 = 1.0;
+    long bad = check_chunks(worst_chunk);
+    // the kernels' parameters: int8 fill 75% (55% with the copy), two slots
+    // at least, slot instances 2 / 4 / 8 / 16; int4 fill 75%, three slots,
+    // instances 4 / 8 / 16
+    bad += check_groups(8, 75, 2, 2, "int8", worst_i8);
+    bad += check_groups(8, 55, 2, 2, "int8+copy", worst_i8c);
+    bad += check_groups(4, 75, 3, 4, "int4", worst_i4);
+    printf("worst fill: chunks %.4f, int8 %.4f, int8+copy %.4f, int4 %.4f\n", worst_chunk,
+           worst_i8, worst_i8c, worst_i4);
     if (bad) {
         printf("%ld failures\n", bad);
         return 1;

@@ -229,8 +229,8 @@ def test_quant_tiny_secondary_shards(zpp):
                            "shard %d" % j)
 
 
-@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 960, 1024, 2048, 2112, 4032,
-                                   4096])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 448, 512, 960, 1024, 1088, 2048, 2112,
+                                   4032, 4096])
 @pytest.mark.parametrize("n", [1, 7, 8, 63, 255, 256, 257, 256 * 5 + 80, 100000, 1 << 17])
 def test_quant_blocks_and_ragged(zpp, block, n):
     x = synth.bf16_weights(n, 52, n + block)
@@ -293,7 +293,7 @@ def run_refresh_quant_gpu(zpp, x, block, pad_src=0, pad_dst=0, pad_codes=0):
     return to_host(sec, np.uint16), to_host(codes, np.int8), to_host(scales, np.float32)
 
 
-@pytest.mark.parametrize("block", [64, 192, 256, 320, 960, 1024, 4032, 4096])
+@pytest.mark.parametrize("block", [64, 192, 256, 320, 576, 960, 1024, 4032, 4096])
 @pytest.mark.parametrize("n", [1, 7, 255, 256, 257, 256 * 5 + 80, 100000, 1 << 17])
 def test_refresh_quantize_vs_oracle(zpp, block, n):
     """The refresh and its quantization in one pass: the secondary is the
