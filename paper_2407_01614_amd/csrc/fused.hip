@@ -17,7 +17,9 @@
 // absmax is known; a 256-block is exactly one wave, so its absmax is a
 // six-step cross-lane reduction.  A block that is not a power of two (any
 // multiple of 64 up to 4096) takes fused_multi_kernel: several whole blocks
-// per wave at a time, the block absmax folded in LDS.
+// per wave at a time, the block absmax folded in LDS.  Blocks of more than
+// 1024 values take fused_wg_kernel: a workgroup of several waves, one float4
+// group per thread, the block absmax folded in LDS.
 // Residency is capped at ZPP_FUSED_RESIDENCY
 // workgroups per CU, as for the optimizer step: 1031-1046 us with 12 resident
 // at the Llama-2-13B partition (9-20 within 1%), 1127-1145 us uncapped.  With
@@ -51,6 +53,20 @@
 // / 1232 / 1284.
 #ifndef ZPP_FUSED_MULTI_RESIDENCY
 #define ZPP_FUSED_MULTI_RESIDENCY 8
+#endif
+// Blocks of more than 1024 values take fused_wg_kernel, workgroups of up to
+// 16 waves with one float4 group per thread, capped at about this many waves
+// per CU.  At the Llama-2-13B partition (median of 20 launches): 1088 /
+// 2048 / 2112 / 4032 / 4096 took 1186 / 1180 / 1150 / 1205 / 1188 us with
+// 16, against 1282 / 1240 / 1228 / 1343 / 1261 for the one-wave kernels
+// (fused_kernel, fused_multi_kernel); with 12 per CU the workgroups of 9
+// waves (1088, 2112) fit only once per CU and took 1342-1349 us.  At 1024
+// and below it was no faster than the one-wave kernels (192 / 448 / 512 /
+// 576 / 1024: 1190 / 1252 / 1106 / 1253 / 1210 against 1180 / 1214 / 1086
+// / 1224 / 1178 us): a wave waits at the workgroup's barrier for the
+// slowest of its block.
+#ifndef ZPP_FUSED_WG_WAVES
+#define ZPP_FUSED_WG_WAVES 16
 #endif
 #ifndef ZPP_FUSED_MAX_GRID
 #define ZPP_FUSED_MAX_GRID (1u << 30)
@@ -333,6 +349,102 @@ __global__ __launch_bounds__(kWave) void fused_multi_kernel(FusedArgs a, GS gs, 
     }
 }
 
+// Blocks of more than 1024 values: a workgroup of NW waves (NW = blockDim.x / 64, up to 16) takes kb whole blocks, one
+// float4 group per thread, thread t holding the group at 4 t of the
+// workgroup's span, so every thread does what a thread of fused_kernel does
+// at 256: one group loaded, updated and stored at a time.  The block absmax
+// goes through LDS: a wave that lies inside one block reduces it with
+// cross-lane shuffles and folds it in with one LDS max, a wave that crosses
+// a block boundary folds each lane's in; one barrier later every thread
+// reads its block's absmax, derives the parameters and stores its codes.
+template <bool ADAMW, class GS>
+__global__ __launch_bounds__(1024) void fused_wg_kernel(FusedArgs a, GS gs, uint32_t B,
+                                                        uint32_t kb) {
+    extern __shared__ uint32_t bmax[];  // kb words at the start of the reservation
+    const uint32_t tid = threadIdx.x;
+    const uint32_t gpb = B / 4;  // float4 groups per block
+    const uint32_t kl = tid / gpb;
+    const bool active = kl < kb;
+    const size_t nblocks = (a.n + B - 1) / B;
+    // the wave lies inside one block of the workgroup (uniform)
+    const uint32_t w0 = tid & ~(uint32_t)(kWave - 1);
+    const bool wave_in_block = w0 / gpb == (w0 + kWave - 1) / gpb && (w0 + kWave - 1) / gpb < kb;
+    for (size_t k0 = (size_t)blockIdx.x * kb; k0 < nblocks; k0 += (size_t)gridDim.x * kb) {
+        if (tid < kb)
+            bmax[tid] = 0u;
+        const size_t i = k0 * B + (size_t)tid * 4;
+        const bool live = active && i < a.n;
+        u32x2 pk = {0u, 0u};
+        if (live && i + 4 <= a.n) {
+            f32x4 P = ld_nt(reinterpret_cast<const f32x4 *>(a.p + i));
+            f32x4 M = ld_nt(reinterpret_cast<const f32x4 *>(a.m + i));
+            f32x4 Q = ld_nt(reinterpret_cast<const f32x4 *>(a.v + i));
+            const f32x4 G = grad_load4(gs, i);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float p = P[e], m = M[e], q = Q[e];
+                adam_update<ADAMW>(p, m, q, G[e], a.c);
+                P[e] = p;
+                M[e] = m;
+                Q[e] = q;
+            }
+            st_nt(reinterpret_cast<f32x4 *>(a.p + i), P);
+            st_nt(reinterpret_cast<f32x4 *>(a.m + i), M);
+            st_nt(reinterpret_cast<f32x4 *>(a.v + i), Q);
+            pk = u32x2{pack_bf16x2(P.x, P.y), pack_bf16x2(P.z, P.w)};
+            st_nt(reinterpret_cast<u32x2 *>(a.primary + i), pk);
+            if (a.secondary)
+                st_nt(reinterpret_cast<u32x2 *>(a.secondary + i), pk);
+        } else if (live) {
+            // the partition's last elements, one by one; absent ones hold
+            // bf16 zero, which no absmax can see
+            uint32_t h[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                h[e] = 0u;
+                if (i + e < a.n) {
+                    float p = a.p[i + e], m = a.m[i + e], q = a.v[i + e];
+                    adam_update<ADAMW>(p, m, q, grad_at(gs, i + e), a.c);
+                    a.p[i + e] = p;
+                    a.m[i + e] = m;
+                    a.v[i + e] = q;
+                    h[e] = bf16_rne_bits(p);
+                    a.primary[i + e] = (uint16_t)h[e];
+                    if (a.secondary)
+                        a.secondary[i + e] = (uint16_t)h[e];
+                }
+            }
+            pk = u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        }
+        const u16x2 m2 = __builtin_elementwise_max(absbits2(pk.x), absbits2(pk.y));
+        uint32_t mx = max((uint32_t)m2.x, (uint32_t)m2.y);
+        __syncthreads();  // the zeroed words are visible
+        if (wave_in_block) {
+#pragma unroll
+            for (int off = kWave / 2; off >= 1; off >>= 1)
+                mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+            if ((tid & (kWave - 1)) == 0)
+                atomicMax(&bmax[kl], mx);
+        } else if (active) {
+            atomicMax(&bmax[kl], mx);
+        }
+        __syncthreads();
+        if (live) {
+            const BlockQuant q = block_params(bmax[kl]);
+            const uint32_t c4 = quant_word(pk.x, pk.y, q);
+            if (i + 4 <= a.n) {
+                st_nt(reinterpret_cast<uint32_t *>(a.codes + i), c4);
+            } else {
+                for (int e = 0; e < 4 && i + e < a.n; ++e)
+                    a.codes[i + e] = (int8_t)((c4 >> (8 * e)) & 0xFFu);
+            }
+            if (tid == kl * gpb)
+                a.scales[k0 + kl] = q.scale;
+        }
+        __syncthreads();  // the words are zeroed again for the next blocks
+    }
+}
+
 // Workgroups per CU for each gradient source.
 template <class GS> constexpr int fused_residency();
 template <> constexpr int fused_residency<F32Grad>() { return ZPP_FUSED_RESIDENCY; }
@@ -353,6 +465,53 @@ void launch_fused_b(const FusedArgs &a, const GS &gs, hipStream_t stream) {
                            gs);
 }
 
+// Workgroup shape of fused_wg_kernel for a block of gpb float4 groups: the
+// fewest waves (1 to 16) whose threads the workgroup's whole blocks fill to
+// at least 90%, failing that the largest fill.
+struct WgShape {
+    uint32_t waves, blocks;
+};
+inline WgShape fused_wg_shape(uint32_t gpb) {
+    WgShape best = {0, 0};
+    uint64_t best_used = 0, best_threads = 1;
+    for (uint32_t nw = 1; nw <= 16; ++nw) {
+        const uint32_t kb = nw * kWave / gpb;
+        if (kb == 0)
+            continue;
+        const uint64_t used = (uint64_t)kb * gpb, threads = (uint64_t)nw * kWave;
+        if (10 * used >= 9 * threads)
+            return {nw, kb};
+        if (used * best_threads > best_used * threads) {
+            best = {nw, kb};
+            best_used = used;
+            best_threads = threads;
+        }
+    }
+    return best;
+}
+
+template <class GS>
+void launch_fused_wg(const FusedArgs &a, const GS &gs, uint32_t block, hipStream_t stream) {
+    const WgShape sh = fused_wg_shape(block / 4);
+    const size_t nblocks = (a.n + block - 1) / block;
+    const size_t need = (nblocks + sh.blocks - 1) / sh.blocks;
+    const unsigned grid = (unsigned)(need < ZPP_FUSED_MAX_GRID ? need : ZPP_FUSED_MAX_GRID);
+    // about ZPP_FUSED_WG_WAVES waves per CU, as for the one-wave kernel
+    int per_cu = (ZPP_FUSED_WG_WAVES + (int)sh.waves / 2) / (int)sh.waves;
+    if (per_cu < 1)
+        per_cu = 1;
+    size_t lds = residency_lds(per_cu);
+    if (lds < sh.blocks * sizeof(uint32_t))
+        lds = sh.blocks * sizeof(uint32_t);
+    const dim3 threads(sh.waves * kWave);
+    if (a.c.adamw)
+        hipLaunchKernelGGL((fused_wg_kernel<true, GS>), dim3(grid), threads, lds, stream, a, gs,
+                           block, sh.blocks);
+    else
+        hipLaunchKernelGGL((fused_wg_kernel<false, GS>), dim3(grid), threads, lds, stream, a, gs,
+                           block, sh.blocks);
+}
+
 template <class GS>
 hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
                            hipStream_t stream) {
@@ -362,9 +521,11 @@ hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
     case 256: launch_fused_b<256>(a, gs, stream); break;
     case 512: launch_fused_b<512>(a, gs, stream); break;
     case 1024: launch_fused_b<1024>(a, gs, stream); break;
-    case 2048: launch_fused_b<2048>(a, gs, stream); break;
-    case 4096: launch_fused_b<4096>(a, gs, stream); break;
     default: {
+        if (block > 1024) {
+            launch_fused_wg(a, gs, block, stream);
+            break;
+        }
         // blocks of up to 1024 values: at most 4 float4 groups per lane;
         // larger ones 16 (4096 / 4 = 1024 groups fit 64 x 16)
         const bool small = block / 4 <= 64 * 4;

@@ -478,8 +478,9 @@ def assert_fused_matches_oracle(got, p, m, v, g, hp, step, block, what):
     assert_bits_equal(gsc[same], rs[same], what + " scales")
 
 
-@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 960, 1088, 2112, 4032, 4096])
-@pytest.mark.parametrize("n", [1, 255, 256, 4099, 256 * 40 + 80, 65536 + 64 + 3])
+@pytest.mark.parametrize("block", [64, 128, 192, 256, 320, 512, 960, 1088, 2048, 2112, 4032,
+                                   4096])
+@pytest.mark.parametrize("n", [1, 255, 256, 4099, 1088 * 4 + 7, 256 * 40 + 80, 65536 + 64 + 3])
 def test_fused_vs_oracle(zpp, block, n):
     hp = f32hp(HP_TINY)
     p = synth.master_weights(n, 70, n)
