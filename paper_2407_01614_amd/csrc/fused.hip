@@ -85,6 +85,11 @@ struct FusedArgs {
     AdamConsts c;
 };
 
+// Runs of consecutive workgroups per XCD: grouped for the qgZ receive from
+// separate arrays (zpp_i4grad.h), plain otherwise.
+template <class GS> constexpr size_t fused_xcd_run() { return 0; }
+template <> constexpr size_t fused_xcd_run<I4Grad>() { return kSeparateXcdRun; }
+
 // The gradient comes from `gs`: the fp32 array of the partition step
 // (F32Grad), or the int4 copies of the qgZ receive (I4Grad, zpp_i4grad.h).
 template <bool ADAMW, int B, class GS>
@@ -94,7 +99,8 @@ __global__ __launch_bounds__(kWave) void fused_kernel(FusedArgs a, GS gs) {
     constexpr int L = B < 256 ? B / 4 : kWave;  // lanes per quant block
     const int lane = threadIdx.x;
     const size_t nchunks = (a.n + C - 1) / C;
-    for (size_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
+    for (size_t ch = xcd_grouped(blockIdx.x, gridDim.x, fused_xcd_run<GS>()); ch < nchunks;
+         ch += gridDim.x) {
         const size_t base = ch * C;
         const bool full = base + C <= a.n;
         u32x2 pk[W];

@@ -316,6 +316,8 @@ struct ReduceArgs {
 // contiguous wave loads (2 bytes per lane) and every store of the wave
 // writes 1 KiB contiguously.  Sources are taken eight at a time, all their
 // loads in flight before the fma passes, which keep the order q = 0, 1, ...
+// Workgroups are renumbered in runs per XCD (kSeparateXcdRun), so that the
+// tiles sharing a line of a source's scales read it through one L2.
 template <int G>
 __global__ __launch_bounds__(kQgzThreads) void reduce_i4_kernel(ReduceArgs a) {
     constexpr int kBatch = 8;
@@ -324,7 +326,8 @@ __global__ __launch_bounds__(kQgzThreads) void reduce_i4_kernel(ReduceArgs a) {
     const size_t ntiles = (a.n + C - 1) / C;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    for (size_t tile = (size_t)blockIdx.x * kWaves + wave; tile < ntiles;
+    const size_t wg = xcd_grouped(blockIdx.x, gridDim.x, kSeparateXcdRun);
+    for (size_t tile = wg * kWaves + wave; tile < ntiles;
          tile += (size_t)gridDim.x * kWaves) {
         const size_t base = tile * C + (size_t)lane * 4;
         const bool full = tile * C + C <= a.n;

@@ -68,11 +68,17 @@ __device__ __forceinline__ void scalar_step(const RecvArgs<GS> &a, size_t i) {
     a.out[i] = (uint16_t)bf16_rne_bits(p);
 }
 
+// Runs of consecutive workgroups per XCD: grouped for the separate arrays
+// (zpp_i4grad.h), plain otherwise.
+template <class GS> constexpr size_t recv_xcd_run() { return 0; }
+template <> constexpr size_t recv_xcd_run<I4Grad>() { return kSeparateXcdRun; }
+
 template <bool ADAMW, class GS>
 __global__ __launch_bounds__(kWave) void recv_adam_kernel(RecvArgs<GS> a) {
     const size_t ntiles = (a.n + 255) / 256;
     const int lane = threadIdx.x;
-    for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    for (size_t t = xcd_grouped(blockIdx.x, gridDim.x, recv_xcd_run<GS>()); t < ntiles;
+         t += gridDim.x) {
         const size_t i = t * 256 + (size_t)lane * 4;
         if (t * 256 + 256 > a.n) {
             // the last, partial tile: element by element

@@ -13,6 +13,19 @@
 
 namespace zpp {
 
+// Workgroup numbering of the kernels that read the P copies from separate
+// arrays (xcd_grouped in zpp_device.h): a 128-byte line of one source's
+// scales serves 32 blocks, so 32 or more neighbouring tiles read it, and
+// runs of this many consecutive workgroups per XCD let one L2 fetch it.  At
+// the Llama-2-13B partition with 8 sources (median of 20 launches): the
+// dequant-reduce 285 against 305 us, the receive step 990 against 1110, the
+// single receive pass 1155 against 1235 (runs of 16 / 32 / 64 in between).
+// The interleaved buffer keeps a block's scales of all sources in one
+// 32-byte run, and the fused step has no shared lines: both were as fast or
+// slower with grouping (the fused step 1079-1152 against 1046 us), so their
+// kernels keep the plain numbering.
+constexpr size_t kSeparateXcdRun = 128;
+
 struct I4Grad {
     const uint8_t *codes[kMaxShards];  // packed int4, element 2i in the low nibble
     const float *scales[kMaxShards];   // one per block
