@@ -29,6 +29,7 @@
 // contiguous run): 938 us with ZPP_RECV_IL_RESIDENCY = 12 (14: 949, 16: 955,
 // uncapped 978) against 981 us from separate arrays in the same run.
 #include "zpp_adam.h"
+#include "zpp_chunk.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"
 #include "zpp_launch.h"

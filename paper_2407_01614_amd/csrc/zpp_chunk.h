@@ -7,6 +7,7 @@
 // vector slots that K blocks fill, then the most blocks.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 namespace zpp {
@@ -70,6 +71,21 @@ inline GroupShape group_shape(uint32_t vectors_per_block, uint32_t max_s, uint32
         }
     }
     return best;
+}
+
+// The dispatcher hands workgroups to the GPU's 8 XCDs in turn (workgroup w
+// to XCD w % 8), each XCD with its own L2.  xcd_grouped(w, grid, R)
+// renumbers workgroup w so that in every run of 8 R workgroups each XCD
+// takes R consecutive positions (an incomplete last run keeps its order):
+// neighbouring workgroups that read the same cache lines -- a line of
+// per-block scales serving several tiles -- then fetch them through one L2.
+// A permutation of [0, grid) for any R; R <= 1 is the identity.  (constexpr,
+// so kernels and host checks call the same function.)
+constexpr size_t xcd_grouped(size_t w, size_t grid, size_t R) {
+    if (R <= 1)
+        return w;
+    const size_t run = w / (8 * R), r = w % (8 * R);
+    return (run + 1) * 8 * R <= grid ? run * 8 * R + (r % 8) * R + r / 8 : w;
 }
 
 }  // namespace zpp

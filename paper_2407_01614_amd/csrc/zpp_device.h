@@ -61,20 +61,6 @@ static_assert(kLdsPerCU / residency_lds(11) == 11 && kLdsPerCU / residency_lds(1
                   kLdsPerCU / residency_lds(13) == 13 && kLdsPerCU / residency_lds(14) == 14,
               "a reservation caps residency at exactly the requested count");
 
-// The dispatcher hands workgroups to the GPU's 8 XCDs in turn (workgroup w
-// to XCD w % 8), each XCD with its own L2.  xcd_grouped(w, grid, R)
-// renumbers workgroup w so that in every run of 8 R workgroups each XCD
-// takes R consecutive positions (an incomplete last run keeps its order):
-// neighbouring workgroups that read the same cache lines -- a line of
-// per-block scales serving several tiles -- then fetch them through one L2.
-// A permutation of [0, grid) for any R; R <= 1 is the identity.
-__device__ __forceinline__ size_t xcd_grouped(size_t w, size_t grid, size_t R) {
-    if (R <= 1)
-        return w;
-    const size_t run = w / (8 * R), r = w % (8 * R);
-    return (run + 1) * 8 * R <= grid ? run * 8 * R + (r % 8) * R + r / 8 : w;
-}
-
 // Streaming accesses: every byte is touched once, so loads and stores are
 // marked non-temporal.
 #ifndef ZPP_NT_LOAD

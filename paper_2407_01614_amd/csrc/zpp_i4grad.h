@@ -14,7 +14,7 @@
 namespace zpp {
 
 // Workgroup numbering of the kernels that read the P copies from separate
-// arrays (xcd_grouped in zpp_device.h): a 128-byte line of one source's
+// arrays (xcd_grouped in zpp_chunk.h): a 128-byte line of one source's
 // scales serves 32 blocks, so 32 or more neighbouring tiles read it, and
 // runs of this many consecutive workgroups per XCD let one L2 fetch it.  At
 // the Llama-2-13B partition with 8 sources (median of 20 launches): the

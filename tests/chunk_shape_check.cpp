@@ -18,6 +18,11 @@
 // the kernel's slot count (the power of two at or above S) -- covers every
 // element exactly once, the last block cut short included.
 //
+// Workgroup renumbering per XCD (xcd_grouped): a permutation of [0, grid)
+// for every grid and run length tried, and in every complete run of 8 R
+// workgroups the ones that XCD x receives (positions x, x + 8, ...) take R
+// consecutive numbers.
+//
 // Prints the worst fills and "chunk shapes ok".
 #include <stdint.h>
 #include <stdio.h>
@@ -142,6 +147,44 @@ static long check_groups(uint32_t w, uint32_t min_fill, uint32_t min_s, uint32_t
     return bad;
 }
 
+static long check_xcd_grouped() {
+    long bad = 0;
+    const size_t runs[] = {0, 1, 2, 4, 16, 128, 1000};
+    const size_t grids[] = {1, 7, 8, 9, 63, 64, 65, 1023, 1024, 1025, 8 * 128 * 3 + 5, 99305};
+    for (size_t R : runs)
+        for (size_t grid : grids) {
+            std::vector<int> seen(grid, 0);
+            for (size_t w = 0; w < grid; ++w) {
+                const size_t t = zpp::xcd_grouped(w, grid, R);
+                if (t >= grid) {
+                    printf("xcd_grouped out of range: R %zu grid %zu w %zu -> %zu\n", R, grid, w, t);
+                    ++bad;
+                    continue;
+                }
+                ++seen[t];
+            }
+            for (size_t t = 0; t < grid; ++t)
+                if (seen[t] != 1) {
+                    printf("xcd_grouped not a permutation: R %zu grid %zu\n", R, grid);
+                    ++bad;
+                    break;
+                }
+            if (R <= 1)
+                continue;
+            for (size_t run = 0; (run + 1) * 8 * R <= grid; ++run)
+                for (size_t x = 0; x < 8; ++x)
+                    for (size_t j = 0; j < R; ++j) {
+                        const size_t w = run * 8 * R + x + 8 * j;
+                        if (zpp::xcd_grouped(w, grid, R) != run * 8 * R + x * R + j) {
+                            printf("xcd_grouped: XCD %zu not consecutive: R %zu grid %zu\n", x,
+                                   R, grid);
+                            ++bad;
+                        }
+                    }
+        }
+    return bad;
+}
+
 int main() {
     double worst_chunk = 1.0, worst_i8 = 1.0, worst_i8c = 1.0, worst_i4 = 1.0;
     long bad = check_chunks(worst_chunk);
@@ -151,6 +194,7 @@ int main() {
     bad += check_groups(8, 75, 2, 2, "int8", worst_i8);
     bad += check_groups(8, 55, 2, 2, "int8+copy", worst_i8c);
     bad += check_groups(4, 75, 3, 4, "int4", worst_i4);
+    bad += check_xcd_grouped();
     printf("worst fill: chunks %.4f, int8 %.4f, int8+copy %.4f, int4 %.4f\n", worst_chunk,
            worst_i8, worst_i8c, worst_i4);
     if (bad) {
