@@ -22,9 +22,12 @@
 // of two the quantizer gives each block an aligned group of 16 to 64 lanes
 // of a wave, each lane holding several of its groups of 4 values.
 //
-// Both kernels keep every wave's loads and stores contiguous: on this GPU,
-// non-temporal stores that leave gaps inside a wave's footprint (16 bytes per
-// lane at a 32- or 64-byte stride) run two to three times slower.
+// The power-of-two kernels keep every wave's loads and stores contiguous: on
+// this GPU, non-temporal stores that leave gaps inside a wave's footprint
+// (16 bytes per lane at a 32- or 64-byte stride) run two to three times
+// slower.  The lane-group quantizer's code stores are runs of 2 G bytes per
+// block (32 to 128), which the sweep of its shapes measured: groups of 8
+// lanes (16-byte runs) were the slow ones and are not used.
 #include "zpp_chunk.h"
 #include "zpp_device.h"
 #include "zpp_i4grad.h"
