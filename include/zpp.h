@@ -154,7 +154,10 @@ ZPP_API zpp_status zpp_refresh_quantize_i8(uint16_t *secondary_bf16, const uint1
  * weights).  Results are bit for bit those of the three separate calls
  * (zpp_adam_partition_step into primary_bf16, zpp_refresh_secondary from it,
  * zpp_quantize_blockwise_i8 of it), at 33.016 instead of 37.016 bytes of HBM
- * traffic per element for block 256.
+ * traffic per element for block 256.  Blocks of 64 to 512 take one pass;
+ * any other block takes two kernels in stream order, the step with its
+ * copies and then the quantization of primary_bf16 (2 more bytes read per
+ * element, which measured faster than one pass for such blocks).
  * master, exp_avg, exp_avg_sq: float[n] in place; grad: float[n];
  * primary_bf16: uint16_t[n] out; secondary_bf16: uint16_t[n] out, or NULL to
  * keep no bf16 secondary copy; codes: int8_t[n] out; scales:
@@ -164,8 +167,10 @@ ZPP_API zpp_status zpp_refresh_quantize_i8(uint16_t *secondary_bf16, const uint1
  * a gather of the codes waits on).
  * No two ranges may overlap (ZPP_EOVERLAP).  Alignment: floats 4, bf16 2
  * bytes (ZPP_EALIGN); 16-byte fp32 arrays, 8-byte bf16 arrays and 4-byte
- * codes select the single-pass kernel, otherwise the three scalar kernels run
- * one after another. */
+ * codes select the single-pass kernel (for the two-kernel blocks, the
+ * quantization's vector kernel further needs a 16-byte primary_bf16 and
+ * 8-byte codes), otherwise the three scalar kernels run one after
+ * another. */
 ZPP_API zpp_status zpp_adam_step_refresh_quantize(float *master, float *exp_avg, float *exp_avg_sq,
                                                   const float *grad, uint16_t *primary_bf16,
                                                   uint16_t *secondary_bf16, int8_t *codes,
@@ -289,7 +294,9 @@ ZPP_API zpp_status zpp_qgz_receive_adam_step(float *master, float *exp_avg, floa
  * zpp_qgz_receive_adam_step into primary_bf16, zpp_refresh_secondary from
  * it and zpp_quantize_blockwise_i8 of it, at 29 B + num_src * (0.5 B +
  * 4/grad_block B) + 4/block B of HBM traffic per element instead of
- * 33 B + num_src * (0.5 B + 4/grad_block B) + 4/block B.
+ * 33 B + num_src * (0.5 B + 4/grad_block B) + 4/block B.  An int8 block
+ * other than 64 to 512 takes two kernels in stream order, as for
+ * zpp_adam_step_refresh_quantize.
  * master, exp_avg, exp_avg_sq: float[n] in place.  src_codes, src_scales,
  * num_src, scale_out: as for zpp_qgz_receive_adam_step, with int4 blocks of
  * grad_block (a multiple of 64 in [64, 4096]).  primary_bf16: uint16_t[n] out;

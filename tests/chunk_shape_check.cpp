@@ -1,14 +1,6 @@
 // Host check of the work shapes for blocks that are not powers of two
 // (zpp_chunk.h).
 //
-// Chunk shapes (the fused step, 4 fp32 per float4 group, 4 slots for blocks
-// of up to 1024 values and 16 above): for every such block size the shape
-// exists, its K blocks fit the 64 V slots of a wave and the LDS word of each
-// block (K <= 64), and the lane/slot walk of one chunk -- group j = 64 v + l
-// of the chunk for v < V -- covers every element of every block of the chunk
-// exactly once, including a last chunk of fewer blocks and a last block cut
-// short by the end of the array.
-//
 // Lane-group shapes (the int8 quantizer, 8 bf16 per vector, with and without
 // the copy; the int4 quantizer, 4 fp32 per group), with the kernels' own
 // parameters: the shape exists, G is 16, 32 or 64, S is at most 16 and at
@@ -30,57 +22,6 @@
 #include <vector>
 
 #include "zpp_chunk.h"
-
-static long check_chunks(double &worst) {
-    long bad = 0;
-    const uint32_t w = 4;
-    for (uint32_t b = 1; b <= 64; ++b) {
-        if ((b & (b - 1)) == 0)
-            continue;  // powers of two take the other kernels
-        const uint32_t B = 64 * b, vpb = B / w;
-        const uint32_t max_v = vpb <= 64 * 4 ? 4 : 16;
-        const zpp::ChunkShape sh = zpp::chunk_shape(vpb, max_v);
-        if (sh.K == 0 || sh.K > 64 || sh.V == 0 || sh.V > max_v ||
-            (uint64_t)sh.K * vpb > 64ull * sh.V) {
-            printf("bad chunk shape: B %u -> K %u V %u\n", B, sh.K, sh.V);
-            ++bad;
-            continue;
-        }
-        const double fill = (double)sh.K * vpb / (64.0 * sh.V);
-        if (fill < worst)
-            worst = fill;
-        // one array of 2.5 chunks whose last block is short
-        const uint64_t n = (uint64_t)B * (sh.K * 2 + sh.K / 2 + 1) - 3 * w - 1;
-        std::vector<int> seen(n, 0);
-        const uint64_t nblocks = (n + B - 1) / B;
-        for (uint64_t k0 = 0; k0 < nblocks; k0 += sh.K) {
-            const uint64_t kc = nblocks - k0 < sh.K ? nblocks - k0 : sh.K;
-            const uint64_t base = k0 * B, end = base + kc * B < n ? base + kc * B : n;
-            for (uint32_t v = 0; v < sh.V; ++v)
-                for (uint32_t l = 0; l < 64; ++l) {
-                    const uint64_t i = base + ((uint64_t)v * 64 + l) * w;
-                    if (i >= end)
-                        continue;
-                    const uint64_t kl = i / B - k0;
-                    if (kl >= kc || (i + w <= end && (i + w - 1) / B != i / B)) {
-                        printf("group outside its block: B %u i %llu\n", B,
-                               (unsigned long long)i);
-                        ++bad;
-                    }
-                    for (uint32_t e = 0; e < w && i + e < end; ++e)
-                        ++seen[i + e];
-                }
-        }
-        for (uint64_t i = 0; i < n; ++i)
-            if (seen[i] != 1) {
-                printf("element %llu seen %d times: chunk B %u\n", (unsigned long long)i,
-                       seen[i], B);
-                ++bad;
-                break;
-            }
-    }
-    return bad;
-}
 
 static uint32_t slot_bucket(uint32_t s, uint32_t smallest) {
     uint32_t b = smallest;
@@ -186,8 +127,8 @@ static long check_xcd_grouped() {
 }
 
 int main() {
-    double worst_chunk = 1.0, worst_i8 = 1.0, worst_i8c = 1.0, worst_i4 = 1.0;
-    long bad = check_chunks(worst_chunk);
+    double worst_i8 = 1.0, worst_i8c = 1.0, worst_i4 = 1.0;
+    long bad = 0;
     // the kernels' parameters: int8 fill 75% (55% with the copy), two slots
     // at least, slot instances 2 / 4 / 8 / 16; int4 fill 75%, three slots,
     // instances 4 / 8 / 16
@@ -195,8 +136,7 @@ int main() {
     bad += check_groups(8, 55, 2, 2, "int8+copy", worst_i8c);
     bad += check_groups(4, 75, 3, 4, "int4", worst_i4);
     bad += check_xcd_grouped();
-    printf("worst fill: chunks %.4f, int8 %.4f, int8+copy %.4f, int4 %.4f\n", worst_chunk,
-           worst_i8, worst_i8c, worst_i4);
+    printf("worst fill: int8 %.4f, int8+copy %.4f, int4 %.4f\n", worst_i8, worst_i8c, worst_i4);
     if (bad) {
         printf("%ld failures\n", bad);
         return 1;

@@ -28,10 +28,9 @@ def test_block_index_is_exact(tmp_path):
 
 @pytest.mark.skipif(not os.path.exists(CLANGXX), reason="ROCm clang++ not found")
 def test_chunk_shapes_cover_every_element(tmp_path):
-    """The work shapes of the kernels for blocks that are not powers of two
-    (csrc/zpp_chunk.h: the fused step's chunks, the quantizers' lane groups)
-    and the per-XCD workgroup renumbering, checked on the host by
-    tests/chunk_shape_check.cpp."""
+    """The lane groups of the quantizers for blocks that are not powers of two
+    and the per-XCD workgroup renumbering (csrc/zpp_chunk.h), checked on the
+    host by tests/chunk_shape_check.cpp."""
     exe = str(tmp_path / "chunk_shape_check")
     cmd = [CLANGXX, "-std=c++17", "-O2", "-I", os.path.join(ROOT, "paper_2407_01614_amd", "csrc"),
            os.path.join(HERE, "chunk_shape_check.cpp"), "-o", exe]

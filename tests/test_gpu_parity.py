@@ -444,12 +444,14 @@ def test_gather_empty_layer_records_event(zpp):
 # ===========================================================================
 # Fused step + refresh + quantize
 # ===========================================================================
-def run_fused_gpu(zpp, p, m, v, g, hp, step, block, secondary=True, pad=0):
+def run_fused_gpu(zpp, p, m, v, g, hp, step, block, secondary=True, pad=0, pad_bf16=None,
+                  pad_codes=None):
     tp, tm, tv, tg = (to_dev(x, pad=pad) for x in (p, m, v, g))
     n = p.size
-    prim = empty_dev(n, np.uint16, pad=pad, fill=0x5555)
-    sec = empty_dev(n, np.uint16, pad=pad, fill=0x7FC0) if secondary else None
-    codes = empty_dev(n, np.int8, pad=pad, fill=99)
+    pb = pad if pad_bf16 is None else pad_bf16
+    prim = empty_dev(n, np.uint16, pad=pb, fill=0x5555)
+    sec = empty_dev(n, np.uint16, pad=pb, fill=0x7FC0) if secondary else None
+    codes = empty_dev(n, np.int8, pad=pad if pad_codes is None else pad_codes, fill=99)
     scales = empty_dev((n + block - 1) // block, np.float32, fill=-1.0)
     zpp.adam_step_refresh_quantize(tp, tm, tv, tg, prim, sec, codes, scales, step=step,
                                    block=block, **hp)
@@ -488,6 +490,21 @@ def test_fused_vs_oracle(zpp, block, n):
     m, v = synth.moments(n, 70, n)
     got = run_fused_gpu(zpp, p, m, v, g, hp, 2, block)
     assert_fused_matches_oracle(got, p, m, v, g, hp, 2, block, "n=%d block=%d" % (n, block))
+
+
+@pytest.mark.parametrize("block", [192, 320, 1024, 4032])
+def test_fused_two_kernel_blocks_misaligned_quantization(zpp, block):
+    """Blocks other than 64-512 run the step with its copies, then the int8
+    quantizer over the primary.  An 8-byte (not 16-byte) aligned primary and
+    4-byte (not 8-byte) aligned codes keep the step's vector kernel but put
+    the quantization on its scalar kernel: the same bits."""
+    hp = f32hp(HP_TINY)
+    n = block * 37 + 100
+    p = synth.master_weights(n, 73, block)
+    g = synth.gradients(n, 73, block)
+    m, v = synth.moments(n, 73, block)
+    got = run_fused_gpu(zpp, p, m, v, g, hp, 3, block, pad_bf16=4, pad_codes=4)
+    assert_fused_matches_oracle(got, p, m, v, g, hp, 3, block, "block=%d" % block)
 
 
 @pytest.mark.parametrize("secondary", [True, False], ids=["with-secondary", "no-secondary"])
