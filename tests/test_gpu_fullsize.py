@@ -126,6 +126,50 @@ def test_fullsize_quantize(zpp):
     assert bool((full == 127).all()), "every block's absmax element maps to +-127"
 
 
+@pytest.mark.parametrize("B", [192, 2112])
+def test_fullsize_quantize_blocks_not_powers_of_two(zpp, B):
+    """The lane-group quantizers over the whole Llama-2-13B partition at
+    blocks that are not powers of two: int8 codes and scales, alone and in
+    the pass with the secondary copy, and int4 codes and scales of an fp32
+    gradient of the same length, every block against the oracle, bit for
+    bit."""
+    n = WL.n
+    nb = (n + B - 1) // B
+    x = synth.device_bf16_weights(n, WL.cfg_id, rank=1)
+    xh = x.cpu().numpy().view(np.uint16)
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    scales = torch.empty(nb, dtype=torch.float32, device="cuda")
+    sec = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    with pool() as ex:
+        rc, rs = oracle_quantize_whole(xh, B, ex)
+    zpp.quantize_blockwise_i8(x, codes, scales, block=B)
+    torch.cuda.synchronize()
+    assert_bits_equal(codes.cpu().numpy(), rc, "int8 codes B=%d" % B)
+    assert_bits_equal(scales.cpu().numpy(), rs, "int8 scales B=%d" % B)
+    codes.fill_(99)
+    scales.fill_(-1.0)
+    zpp.refresh_quantize_i8(sec, x, codes, scales, block=B)
+    torch.cuda.synchronize()
+    assert_bits_equal(sec.view(torch.int16).cpu().numpy().view(np.uint16), xh,
+                      "secondary B=%d" % B)
+    assert_bits_equal(codes.cpu().numpy(), rc, "int8 codes with the copy B=%d" % B)
+    assert_bits_equal(scales.cpu().numpy(), rs, "int8 scales with the copy B=%d" % B)
+    del sec, codes, x
+    g = synth.device_normal_f32(n, synth.GRAD_STD, WL.cfg_id, synth.KIND_GRAD, it=3)
+    c4 = torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda")
+    zpp.quantize_blockwise_i4(g, c4, scales, block=B)
+    torch.cuda.synchronize()
+    gh = g.cpu().numpy()
+    step = max(B, -(-n // 64) // B * B)
+    with pool() as ex:
+        parts = list(ex.map(lambda a: oracle.quantize_blockwise_i4(gh[a:a + step], B),
+                            range(0, n, step)))
+    assert_bits_equal(c4.cpu().numpy(), np.concatenate([c for c, _ in parts]),
+                      "int4 codes B=%d" % B)
+    assert_bits_equal(scales.cpu().numpy(), np.concatenate([sc for _, sc in parts]),
+                      "int4 scales B=%d" % B)
+
+
 @pytest.mark.parametrize("wl", [WL, F7], ids=["llama-2-13b-layer", "falcon-7b-layer"])
 def test_fullsize_gather(zpp, wl):
     """The whole gathered layer (317,204,480 or 207,070,080 elements, the
@@ -216,11 +260,13 @@ def test_fullsize_pipeline_properties(zpp, streams):
     torch.cuda.empty_cache()
 
 
-def test_fullsize_fused_step_refresh_quantize(zpp):
-    """The fused kernel on the whole Llama-2-13B partition: sampled whole
-    quantization blocks (and the short last block) against the oracle's Adam
-    followed by its quantizer on its own primary."""
-    n, B = WL.n, WL.block
+@pytest.mark.parametrize("B", [256, 320, 4096])
+def test_fullsize_fused_step_refresh_quantize(zpp, B):
+    """The fused step on the whole Llama-2-13B partition (one pass at 256;
+    the step with its copies, then the quantizer, at 320 and 4096): sampled
+    whole quantization blocks (and the short last block) against the
+    oracle's Adam followed by its quantizer on its own primary."""
+    n = WL.n
     nb = (n + B - 1) // B
     hp = f32hp(WL.adam)
     p = synth.device_normal_f32(n, synth.WEIGHT_STD, WL.cfg_id, synth.KIND_MASTER)
@@ -250,7 +296,10 @@ def test_fullsize_fused_step_refresh_quantize(zpp):
     full = kb.size * B
     rc, rs = oracle.quantize_blockwise_i8(rb[:full], B)
     same = (gb[:full].reshape(-1, B) == rb[:full].reshape(-1, B)).all(axis=1)
-    assert same.mean() > 0.99
+    # a primary element may differ by one bf16 ulp where the fp32 update
+    # lands near a rounding tie (within the Adam tolerance above); a block
+    # of 4096 holds such an element 16 times as often as one of 256
+    assert same.mean() > (0.99 if B <= 320 else 0.9)
     assert_bits_equal(gc[:full].reshape(-1, B)[same], rc.reshape(-1, B)[same], "sampled codes")
     gs = host(scales, torch.from_numpy(kb).cuda(), np.float32)
     assert_bits_equal(gs[same], rs[same], "sampled scales")
