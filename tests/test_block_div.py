@@ -27,14 +27,14 @@ def test_block_index_is_exact(tmp_path):
 
 
 @pytest.mark.skipif(not os.path.exists(CLANGXX), reason="ROCm clang++ not found")
-def test_chunk_shapes_cover_every_element(tmp_path):
+def test_work_shapes_cover_every_element(tmp_path):
     """The lane groups of the quantizers for blocks that are not powers of two
     and the per-XCD workgroup renumbering (csrc/zpp_chunk.h), checked on the
-    host by tests/chunk_shape_check.cpp."""
-    exe = str(tmp_path / "chunk_shape_check")
+    host by tests/work_shape_check.cpp."""
+    exe = str(tmp_path / "work_shape_check")
     cmd = [CLANGXX, "-std=c++17", "-O2", "-I", os.path.join(ROOT, "paper_2407_01614_amd", "csrc"),
-           os.path.join(HERE, "chunk_shape_check.cpp"), "-o", exe]
+           os.path.join(HERE, "work_shape_check.cpp"), "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, " ".join(cmd) + "\n" + r.stderr
     r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
-    assert r.returncode == 0 and "chunk shapes ok" in r.stdout, r.stdout + r.stderr
+    assert r.returncode == 0 and "work shapes ok" in r.stdout, r.stdout + r.stderr

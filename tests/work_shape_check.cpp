@@ -15,7 +15,7 @@
 // workgroups the ones that XCD x receives (positions x, x + 8, ...) take R
 // consecutive numbers.
 //
-// Prints the worst fills and "chunk shapes ok".
+// Prints the worst fills and "work shapes ok".
 #include <stdint.h>
 #include <stdio.h>
 
@@ -141,6 +141,6 @@ int main() {
         printf("%ld failures\n", bad);
         return 1;
     }
-    printf("chunk shapes ok\n");
+    printf("work shapes ok\n");
     return 0;
 }
