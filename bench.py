@@ -397,6 +397,68 @@ def patterns(wl, reps=20):
     return out
 
 
+def block_sizes(wl, reps=20, blocks=(256, 192, 320, 1088, 4032)):
+    """The kernels whose layout depends on the quantization block, at this
+    workload's partition and a few blocks other than its own: the int8
+    quantizer alone and with the secondary copy, the int4 quantizer and the
+    fused step (for blocks outside 64-512 the step with its copies, then the
+    quantizer over the primary).  Median of `reps` calls per kernel and
+    block, each call timed with events on the current stream (a call of
+    the fused step may be two kernels)."""
+    import torch
+    from paper_2407_01614_amd import synth, zpp
+    from paper_2407_01614_amd.workloads import (bytes_fused, bytes_quant, bytes_quant_i4,
+                                                bytes_refresh_quant)
+    stream = torch.cuda.current_stream()
+    n = wl.n
+
+    def timed(fn):
+        fn()
+        evs = []
+        for _ in range(reps):
+            a, b = zpp.Event(timing=True), zpp.Event(timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return sorted(a.elapsed_ms(b) for a, b in evs)[reps // 2]
+
+    x = synth.device_bf16_weights(n, wl.cfg_id, rank=0)
+    sec = torch.empty_like(x)
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    c4 = torch.empty((n + 1) // 2, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(n // 64 + 1, dtype=torch.float32, device="cuda")
+    p = synth.device_normal_f32(n, synth.WEIGHT_STD, wl.cfg_id, synth.KIND_MASTER)
+    g = synth.device_normal_f32(n, synth.GRAD_STD, wl.cfg_id, synth.KIND_GRAD)
+    m = torch.zeros(n, device="cuda")
+    v = torch.zeros(n, device="cuda")
+    prim = torch.empty_like(x)
+    hp = dict(wl.adam)
+    out = {}
+    for B in blocks:
+        calls = {
+            "quant_i8": (lambda: zpp.quantize_blockwise_i8(x, codes, scales, block=B),
+                         bytes_quant(n, B)),
+            "refresh_quant_i8": (lambda: zpp.refresh_quantize_i8(sec, x, codes, scales, block=B),
+                                 bytes_refresh_quant(n, B)),
+            "quant_i4": (lambda: zpp.quantize_blockwise_i4(g, c4, scales, block=B),
+                         bytes_quant_i4(n, B)),
+            "fused_step_refresh_quant": (
+                lambda: zpp.adam_step_refresh_quantize(p, m, v, g, prim, sec, codes, scales,
+                                                       step=2, block=B, **hp),
+                bytes_fused(n, B)),
+        }
+        row = {}
+        for name, (call, nbytes) in calls.items():
+            ms = timed(call)
+            gbps = nbytes / (ms * 1e-3) / 1e9
+            row[name] = {"bytes": nbytes, "median_us": round(ms * 1e3, 2),
+                         "GB/s": round(gbps, 1), "frac_of_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+        out[str(B)] = row
+    return out
+
+
 def _chunks(n, parts, align):
     """[a, b) ranges covering [0, n), each boundary a multiple of `align`."""
     step = max(align, -(-n // parts) // align * align)
@@ -769,6 +831,8 @@ def main():
     del pipe
     torch.cuda.empty_cache()
     line["forward_gather_qwz"] = forward_gather_measure(wl, args.steps)
+    torch.cuda.empty_cache()
+    line["block_sizes"] = block_sizes(wl)
     torch.cuda.empty_cache()
     if args.cpu_sample > 0:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample, steps=args.cpu_steps)
