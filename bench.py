@@ -54,7 +54,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="llama-2-13b")
+    from paper_2407_01614_amd.workloads import WORKLOADS
+    # a step stores its gather shards in the rank's own partition; the tiny
+    # configuration (4 ranks of 1 Mi elements gathering a 4 Mi layer from 2
+    # shards) does not fit that and is covered by the parity tests instead
+    benchable = [k for k, w in WORKLOADS.items() if w.distinct_layers * w.shard_elems <= w.n]
+    ap.add_argument("--workload", default="llama-2-13b", choices=benchable)
     ap.add_argument("--cpu-sample", type=float, default=1.0,
                     help="fraction of the workload the CPU oracle is timed on (0 = skip)")
     ap.add_argument("--cpu-steps", type=int, default=2,
@@ -82,14 +87,16 @@ _COMMON = ["zpp_device.h", "zpp_launch.h"]
 TRAFFIC_SOURCES = {
     "adam": ["adam.hip", "zpp_adam.h"] + _COMMON,
     "refresh": ["refresh.hip"] + _COMMON,
-    "quant": ["quant.hip", "zpp_quant.h"] + _COMMON,
-    "refresh_quant": ["quant.hip", "zpp_quant.h"] + _COMMON,
+    "quant": ["quant.hip", "zpp_quant.h", "zpp_chunk.h"] + _COMMON,
+    "refresh_quant": ["quant.hip", "zpp_quant.h", "zpp_chunk.h"] + _COMMON,
     "gather": ["gather.hip"] + _COMMON,
-    "fused": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
-    "quant_i4": ["qgz.hip", "zpp_quant.h"] + _COMMON,
-    "reduce_i4": ["qgz.hip", "zpp_i4grad.h", "zpp_quant.h"] + _COMMON,
-    "receive_adam": ["receive_adam.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
-    "fused_receive": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h"] + _COMMON,
+    "fused": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h", "zpp_chunk.h"] + _COMMON,
+    "quant_i4": ["qgz.hip", "zpp_quant.h", "zpp_i4grad.h", "zpp_chunk.h"] + _COMMON,
+    "reduce_i4": ["qgz.hip", "zpp_i4grad.h", "zpp_quant.h", "zpp_chunk.h"] + _COMMON,
+    "receive_adam": ["receive_adam.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h",
+                     "zpp_chunk.h"] + _COMMON,
+    "fused_receive": ["fused.hip", "zpp_adam.h", "zpp_quant.h", "zpp_i4grad.h",
+                      "zpp_chunk.h"] + _COMMON,
 }
 
 

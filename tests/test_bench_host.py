@@ -117,3 +117,42 @@ def test_sustain_runs_whole_chunks_for_the_asked_time(bench, monkeypatch):
     assert rec["steps"] == 15 and FakePipe.steps == 15 and rec["seconds"] == 3.0
     assert rec["GB/s"] == round(1000.0 * 15 / 3.0 / 1e9, 1)
     assert pipe.streams == 1 and pipe.fused is False and pipe.sync == "event"
+
+
+def test_traffic_sources_cover_every_include(bench):
+    """Each kernel's digest covers its .hip file and every header it
+    includes, directly or through another header, so that a change to any
+    of them invalidates the kernel's counter figures."""
+    import re
+    csrc = os.path.join(ROOT, "paper_2407_01614_amd", "csrc")
+
+    def includes(name, seen):
+        if name in seen:
+            return seen
+        seen.add(name)
+        with open(os.path.join(csrc, name)) as f:
+            for line in f:
+                m = re.match(r'#include "([^"]+)"', line)
+                if m:
+                    includes(m.group(1), seen)
+        return seen
+
+    for kernel, sources in bench.TRAFFIC_SOURCES.items():
+        need = includes(sources[0], set())
+        assert need <= set(sources), (kernel, sorted(need - set(sources)))
+
+
+def test_traffic_file_matches_current_sources(bench):
+    """The committed counter figures are those of the sources as they are."""
+    with open(os.path.join(ROOT, "profiles", "traffic.json")) as f:
+        t = json.load(f)
+    for kernel, v in t["kernels"].items():
+        assert v["source_digest"] == bench.source_digest(bench.TRAFFIC_SOURCES[kernel]), kernel
+
+
+def test_workloads_offered_fit_the_pipeline(bench):
+    """--workload offers only configurations whose gather shards fit in the
+    rank partition; the tiny one is refused with argparse's message."""
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "invalid choice" in r.stderr
