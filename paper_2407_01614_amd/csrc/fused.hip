@@ -192,6 +192,9 @@ hipError_t launch_fused_gs(const FusedArgs &a, const GS &gs, uint32_t block,
         // the step and its copies in one pass, then the quantization of
         // the primary it wrote (stream order)
         launch_fused_b<256, GS, false>(a, gs, stream);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
         const bool qvec = reinterpret_cast<uintptr_t>(a.primary) % 16 == 0 &&
                           reinterpret_cast<uintptr_t>(a.codes) % 8 == 0;
         return launch_quantize(a.primary, a.n, block, a.codes, a.scales, qvec, stream);
